@@ -1,0 +1,35 @@
+"""CPU oracle for shared-prefix decode attention -- TEST INFRASTRUCTURE ONLY.
+
+This package is the checker, not the product.  Only the test suite, the smoke
+check of the entry module and the CPU-baseline leg of the benchmark may import
+it; the library path never calls it and has no CPU fallback.
+
+What it computes (Section 5.3, "Sharing Prompt Prefix", and Section 6,
+"Kernel Optimization"): decode-phase softmax attention of one query per request
+over that request's whole context, i.e. the shared prefix of its group followed
+by its own non-shared tokens, with keys and values read from a paged KV cache
+through block tables.  The paper's two-stage kernel reaches exactly this result
+(up to rounding order), so the oracle is the plain definition written out, in
+float64, per request and per head, with no blocking, splitting or fusion.
+
+Pinning (the tests hold the pins): brute force in pure-Python loops on tiny
+inputs, a hand-computed worked example, torch's scaled_dot_product_attention
+in float64 on contiguous input, closed forms (zero query, single key,
+identical keys, a dominant "spike" key), softmax weights that sum to one,
+invariance under physical block permutation, and the prefix/suffix
+decomposition identity.  Every function here is pinned by at least one of them.
+"""
+from .attention import (
+    to_f64,
+    gather_sequence,
+    attend,
+    merge_segments,
+    softmax_weights,
+    request_kv,
+    shared_prefix_decode,
+)
+
+__all__ = [
+    "to_f64", "gather_sequence", "attend", "merge_segments", "softmax_weights",
+    "request_kv", "shared_prefix_decode",
+]

@@ -1,0 +1,161 @@
+"""Plain float64 decode attention over a paged KV cache (test infrastructure).
+
+Definitions (Section 5.3 and the "Kernel Optimization" paragraph of Section 6;
+the paper builds on the softmax attention of FlashAttention and PagedAttention
+and does not restate it, so the standard definition is written out here):
+
+  For request r and head h, with g = group_ids[r], P = prefix_lens[g] (P = 0
+  when g = -1) and S = suffix_lens[r], the keys are
+      K_j = prefix key j of group g         for 0 <= j < P
+      K_j = suffix key (j - P) of request r for P <= j < P + S
+  (values likewise), and
+      s_j    = sm_scale * sum_d q[r,h,d] * K_j[d]
+      m      = max_j s_j
+      lse    = m + ln sum_j exp(s_j - m)
+      w_j    = exp(s_j - lse)
+      out[d] = sum_j w_j * V_j[d]
+
+  Paged storage (Section 6, the per-request page table kept from
+  PagedAttention): token t of a sequence with block table row ``tbl`` lives at
+  pool[tbl[t // B], h, t % B, :] of a [num_blocks, H, B, D] pool.
+
+All inputs are upcast exactly to float64 before any arithmetic.
+"""
+from __future__ import annotations
+
+import math
+from typing import Iterable, Optional, Sequence
+
+import numpy as np
+
+try:  # torch is only needed to read bfloat16 / float16 tensors exactly
+    import torch
+except ImportError:  # pragma: no cover
+    torch = None
+
+
+def to_f64(x) -> np.ndarray:
+    """Exact upcast of a numpy array or torch CPU tensor to float64."""
+    if torch is not None and isinstance(x, torch.Tensor):
+        return x.detach().to("cpu", torch.float64).numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def _ints(x) -> np.ndarray:
+    if torch is not None and isinstance(x, torch.Tensor):
+        x = x.detach().cpu().numpy()
+    return np.asarray(x, dtype=np.int64)
+
+
+def gather_sequence(pool, table_row: Sequence[int], length: int) -> np.ndarray:
+    """Tokens 0..length-1 of one paged sequence as float64 [length, H, D].
+
+    Token t is pool[table_row[t // B], :, t % B, :] (Section 6, paged KV with a
+    per-request page table).
+    """
+    B = int(pool.shape[2])
+    H, D = int(pool.shape[1]), int(pool.shape[3])
+    if length == 0:
+        return np.zeros((0, H, D), dtype=np.float64)
+    nblk = -(-length // B)
+    blocks = _ints(table_row)[:nblk]
+    x = to_f64(pool[blocks])                       # [nblk, H, B, D]
+    x = x.transpose(0, 2, 1, 3).reshape(nblk * B, H, D)
+    return x[:length]
+
+
+def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray, sm_scale: float):
+    """Softmax attention of one query per head over N keys.
+
+    q: [H, D], K, V: [N, H, D] (float64).  Returns (out [H, D], lse [H]).
+    An empty key set gives out = 0 and lse = -inf (the neutral element of
+    ``merge_segments``).
+    """
+    H, D = q.shape
+    if K.shape[0] == 0:
+        return np.zeros((H, D)), np.full(H, -np.inf)
+    s = sm_scale * np.einsum("hd,nhd->hn", q, K)   # [H, N]
+    m = s.max(axis=1)
+    lse = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    w = np.exp(s - lse[:, None])
+    out = np.einsum("hn,nhd->hd", w, V)
+    return out, lse
+
+
+def softmax_weights(q: np.ndarray, K: np.ndarray, sm_scale: float) -> np.ndarray:
+    """The weights w_j of ``attend`` as [H, N]."""
+    s = sm_scale * np.einsum("hd,nhd->hn", q, K)
+    m = s.max(axis=1)
+    lse = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    return np.exp(s - lse[:, None])
+
+
+def merge_segments(parts: Iterable[tuple]) -> tuple:
+    """Combine attention results of disjoint key segments.
+
+    For segments i with results (o_i, l_i) computed by ``attend`` on each
+    segment alone, attention over their union is
+        l = ln sum_i exp(l_i),   o = sum_i exp(l_i - l) * o_i,
+    which is how the paper's kernel joins the prefix's interim results with
+    the non-shared tokens (Section 6, "Kernel Optimization").  Empty segments
+    (l_i = -inf) carry weight zero.
+    """
+    parts = list(parts)
+    ls = np.stack([p[1] for p in parts])            # [k, H]
+    os_ = np.stack([p[0] for p in parts])           # [k, H, D]
+    m = ls.max(axis=0)
+    m_safe = np.where(np.isfinite(m), m, 0.0)
+    wsum = np.exp(ls - m_safe).sum(axis=0)
+    l = m_safe + np.log(wsum)
+    w = np.exp(ls - np.where(np.isfinite(l), l, 0.0))   # [k, H]
+    o = np.einsum("kh,khd->hd", w, os_)
+    return o, l
+
+
+def request_kv(r: int, *, prefix_k, prefix_v, suffix_k, suffix_v,
+               prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids):
+    """Keys and values of request r: its group's prefix, then its own suffix."""
+    g = int(_ints(group_ids)[r])
+    S = int(_ints(suffix_lens)[r])
+    stab = _ints(suffix_tables)[r]
+    Ks = gather_sequence(suffix_k, stab, S)
+    Vs = gather_sequence(suffix_v, stab, S)
+    if g < 0:
+        return Ks, Vs
+    P = int(_ints(prefix_lens)[g])
+    ptab = _ints(prefix_tables)[g]
+    Kp = gather_sequence(prefix_k, ptab, P)
+    Vp = gather_sequence(prefix_v, ptab, P)
+    return np.concatenate([Kp, Ks]), np.concatenate([Vp, Vs])
+
+
+def shared_prefix_decode(q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_tables,
+                         prefix_lens, suffix_tables, suffix_lens, group_ids,
+                         sm_scale: float, requests: Optional[Sequence[int]] = None):
+    """Naive per-request decode attention over concat(prefix, suffix).
+
+    Returns (out [n, H, D], lse [n, H]) in float64 for the requests listed in
+    ``requests`` (all requests, in order, by default).
+    """
+    qf = to_f64(q)
+    R, H, D = qf.shape
+    if requests is None:
+        requests = range(R)
+    requests = list(requests)
+    out = np.zeros((len(requests), H, D))
+    lse = np.zeros((len(requests), H))
+    for i, r in enumerate(requests):
+        K, V = request_kv(r, prefix_k=prefix_k, prefix_v=prefix_v, suffix_k=suffix_k,
+                          suffix_v=suffix_v, prefix_tables=prefix_tables,
+                          prefix_lens=prefix_lens, suffix_tables=suffix_tables,
+                          suffix_lens=suffix_lens, group_ids=group_ids)
+        if K.shape[0] == 0:
+            raise ValueError(f"request {r} has an empty context")
+        out[i], lse[i] = attend(qf[r], K, V, sm_scale)
+    return out, lse
+
+
+def lse_natural(values: Sequence[float]) -> float:
+    """ln sum exp(values) for a short Python list (used by worked examples)."""
+    m = max(values)
+    return m + math.log(sum(math.exp(v - m) for v in values))

@@ -1,0 +1,285 @@
+"""Pins for a decode-attention implementation with the oracle's signature.
+
+Each ``pin_*`` function takes ``decode(q, prefix_k, prefix_v, suffix_k,
+suffix_v, prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids,
+sm_scale, requests=None) -> (out, lse)`` and raises AssertionError when the
+implementation disagrees with something the mathematics fixes independently
+of it.  The oracle must pass all of them; the mutation test plants plausible
+mistakes in the oracle and checks that some pin catches each one.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import torch
+
+from workloads import build_plan, make_batch, make_plan, get_config
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def decode_args(batch, **over):
+    p = batch.plan
+    args = dict(q=batch.q, prefix_k=batch.k_pool, prefix_v=batch.v_pool,
+                suffix_k=batch.k_pool, suffix_v=batch.v_pool,
+                prefix_tables=p.prefix_tables, prefix_lens=p.prefix_lens,
+                suffix_tables=p.suffix_tables, suffix_lens=p.suffix_lens,
+                group_ids=p.group_ids, sm_scale=p.sm_scale)
+    args.update(over)
+    return args
+
+
+def tiny_paged_batch(seed=3, dtype="float32", block_size=4):
+    """Two groups, an ungrouped request and a prefix-only request, paged."""
+    rng = np.random.default_rng(seed)
+    plan = build_plan(heads=2, head_dim=8, block_size=block_size, dtype=dtype,
+                      group_of_request=[0, 0, 1, -1, 1, 0],
+                      prefix_lens=[9, 5], suffix_lens=[3, 0, 7, 11, 4, 1],
+                      sm_scale=1.0 / math.sqrt(8.0), paged=True, shuffle=True, rng=rng)
+    return make_batch(plan, seed=seed)
+
+
+def c1_batch():
+    return make_batch(make_plan(get_config("tiny")))
+
+
+# ---------------------------------------------------------------- brute force
+def brute_force(batch):
+    """Pure-Python loops, math.exp without max shift, own index arithmetic."""
+    p = batch.plan
+    B = p.block_size
+    q = batch.q.double().tolist()
+    kp = batch.k_pool.double().tolist()
+    vp = batch.v_pool.double().tolist()
+    R, H, D = len(q), p.heads, p.head_dim
+    outs, lses = [], []
+    for r in range(R):
+        keys = []   # (block, slot) of every key, prefix first
+        g = int(p.group_ids[r])
+        if g >= 0:
+            for t in range(int(p.prefix_lens[g])):
+                keys.append((int(p.prefix_tables[g][t // B]), t % B))
+        for t in range(int(p.suffix_lens[r])):
+            keys.append((int(p.suffix_tables[r][t // B]), t % B))
+        orow, lrow = [], []
+        for h in range(H):
+            es = []
+            for (blk, slot) in keys:
+                s = 0.0
+                for d in range(D):
+                    s += q[r][h][d] * kp[blk][h][slot][d]
+                es.append(math.exp(p.sm_scale * s))
+            z = sum(es)
+            lrow.append(math.log(z))
+            orow.append([sum(es[j] * vp[blk][h][slot][d] for j, (blk, slot) in enumerate(keys)) / z
+                         for d in range(D)])
+        outs.append(orow)
+        lses.append(lrow)
+    return np.array(outs), np.array(lses)
+
+
+def _close(a, b, rtol, atol, what):
+    a, b = np.asarray(a, dtype=np.float64), np.asarray(b, dtype=np.float64)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} != {b.shape}"
+    assert np.all(np.isfinite(a)), f"{what}: non-finite values"
+    err = np.abs(a - b) - (atol + rtol * np.abs(b))
+    assert np.all(err <= 0), f"{what}: max excess {err.max():.3e}"
+
+
+# ----------------------------------------------------------------------- pins
+def pin_worked_example(decode):
+    with open(os.path.join(GOLDEN, "worked_example.json")) as f:
+        ex = json.load(f)
+    nan = lambda x: np.array([[[[np.nan if v is None else v for v in row] for row in hb]
+                               for hb in blk] for blk in x], dtype=np.float64)
+    kp, vp = nan(ex["k_pool"]), nan(ex["v_pool"])
+    out, lse = decode(np.array(ex["q"]), kp, vp, kp, vp, np.array(ex["prefix_tables"]),
+                      np.array(ex["prefix_lens"]), np.array(ex["suffix_tables"]),
+                      np.array(ex["suffix_lens"]), np.array(ex["group_ids"]), ex["sm_scale"])
+    _close(out, ex["expected_out"], 0, 1e-12, "worked example out")
+    _close(lse, ex["expected_lse"], 0, 1e-12, "worked example lse")
+
+
+def pin_brute_force(decode):
+    for batch in (c1_batch(), tiny_paged_batch(), tiny_paged_batch(seed=5, block_size=16)):
+        out, lse = decode(**decode_args(batch))
+        bo, bl = brute_force(batch)
+        _close(out, bo, 1e-12, 1e-13, "brute force out")
+        _close(lse, bl, 1e-12, 1e-13, "brute force lse")
+
+
+def pin_sdpa(decode):
+    batch = c1_batch()          # contiguous: identity block tables
+    p = batch.plan
+    out, _ = decode(**decode_args(batch))
+    for r in range(p.num_requests):
+        g = int(p.group_ids[r])
+        P, S = int(p.prefix_lens[g]), int(p.suffix_lens[r])
+        B = p.block_size
+        k = batch.k_pool.double().permute(0, 2, 1, 3)   # [NB, B, H, D]
+        pre = k[p.prefix_tables[g][: -(-P // B)]].reshape(-1, p.heads, p.head_dim)[:P]
+        suf = k[p.suffix_tables[r][: -(-S // B)]].reshape(-1, p.heads, p.head_dim)[:S]
+        v = batch.v_pool.double().permute(0, 2, 1, 3)
+        vpre = v[p.prefix_tables[g][: -(-P // B)]].reshape(-1, p.heads, p.head_dim)[:P]
+        vsuf = v[p.suffix_tables[r][: -(-S // B)]].reshape(-1, p.heads, p.head_dim)[:S]
+        K = torch.cat([pre, suf]).permute(1, 0, 2)[None]      # [1, H, N, D]
+        V = torch.cat([vpre, vsuf]).permute(1, 0, 2)[None]
+        qq = batch.q.double()[r][None, :, None, :]            # [1, H, 1, D]
+        ref = torch.nn.functional.scaled_dot_product_attention(qq, K, V, scale=p.sm_scale)
+        _close(out[r], ref[0, :, 0, :].numpy(), 0, 1e-12, f"sdpa request {r}")
+
+
+def pin_zero_query(decode):
+    """q = 0: every logit is 0, so lse = ln N and out = mean of the values."""
+    batch = tiny_paged_batch()
+    p = batch.plan
+    args = decode_args(batch, q=torch.zeros_like(batch.q))
+    out, lse = decode(**args)
+    N = p.context_lens()
+    _close(lse, np.log(N)[:, None].repeat(p.heads, 1), 0, 1e-13, "zero-query lse")
+    v = batch.v_pool.double()
+    B = p.block_size
+    for r in range(p.num_requests):
+        acc = torch.zeros(p.heads, p.head_dim, dtype=torch.float64)
+        g = int(p.group_ids[r])
+        if g >= 0:
+            for t in range(int(p.prefix_lens[g])):
+                acc += v[int(p.prefix_tables[g][t // B]), :, t % B, :]
+        for t in range(int(p.suffix_lens[r])):
+            acc += v[int(p.suffix_tables[r][t // B]), :, t % B, :]
+        _close(out[r], (acc / int(N[r])).numpy(), 1e-12, 1e-13, f"zero-query out {r}")
+
+
+def _key_location(plan, r, j):
+    g = int(plan.group_ids[r])
+    B = plan.block_size
+    P = int(plan.prefix_lens[g]) if g >= 0 else 0
+    if j < P:
+        return int(plan.prefix_tables[g][j // B]), j % B
+    t = j - P
+    return int(plan.suffix_tables[r][t // B]), t % B
+
+
+def pin_spike(decode):
+    """A key equal to c*q dominates: out = its value and lse = its logit."""
+    batch = tiny_paged_batch()
+    p = batch.plan
+    B = p.block_size
+    N = p.context_lens()
+    for r in range(p.num_requests):
+        g = int(p.group_ids[r])
+        P = int(p.prefix_lens[g]) if g >= 0 else 0
+        cand = {0, B - 1, B, P - 1, P, int(N[r]) - 1, int(N[r]) // 2}
+        for j in sorted(x for x in cand if 0 <= x < int(N[r])):
+            for h in range(p.heads):
+                k = batch.k_pool.clone()
+                blk, slot = _key_location(p, r, j)
+                qv = batch.q[r, h].double()
+                c = 40.0 / (p.sm_scale * float(qv @ qv))
+                k[blk, h, slot, :] = (c * qv).to(k.dtype)
+                out, lse = decode(**decode_args(batch, prefix_k=k, suffix_k=k),
+                                  requests=[r])
+                s_spike = p.sm_scale * float(batch.q[r, h].double() @ k[blk, h, slot].double())
+                _close(out[0, h], batch.v_pool[blk, h, slot].double().numpy(), 0, 1e-9,
+                       f"spike r={r} j={j} h={h}")
+                _close(lse[0, h], s_spike, 0, 1e-9, f"spike lse r={r} j={j} h={h}")
+
+
+def pin_single_and_identical_keys(decode):
+    """N = 1: out = V_0, lse = s_0.  All keys equal: lse = s + ln N, out = mean V."""
+    rng = np.random.default_rng(11)
+    plan = build_plan(heads=2, head_dim=8, block_size=4, dtype="float32",
+                      group_of_request=[0, -1, 1], prefix_lens=[1, 10],
+                      suffix_lens=[0, 1, 6], sm_scale=0.5, paged=True, rng=rng)
+    batch = make_batch(plan, seed=2)
+    out, lse = decode(**decode_args(batch))
+    for r in (0, 1):
+        blk, slot = _key_location(plan, r, 0)
+        s0 = 0.5 * (batch.q[r].double() * batch.k_pool[blk, :, slot].double()).sum(-1)
+        _close(out[r], batch.v_pool[blk, :, slot].double().numpy(), 0, 1e-13, f"single key {r}")
+        _close(lse[r], s0.numpy(), 0, 1e-13, f"single key lse {r}")
+    # request 2: make all 16 of its keys identical
+    k = batch.k_pool.clone()
+    ref_blk, ref_slot = _key_location(plan, 2, 0)
+    for j in range(16):
+        blk, slot = _key_location(plan, 2, j)
+        k[blk, :, slot] = batch.k_pool[ref_blk, :, ref_slot]
+    out, lse = decode(**decode_args(batch, prefix_k=k, suffix_k=k), requests=[2])
+    s = 0.5 * (batch.q[2].double() * k[ref_blk, :, ref_slot].double()).sum(-1)
+    _close(lse[0], (s + math.log(16)).numpy(), 0, 1e-12, "identical keys lse")
+    vs = torch.stack([batch.v_pool[_key_location(plan, 2, j)[0], :, _key_location(plan, 2, j)[1]]
+                      for j in range(16)]).double().mean(0)
+    _close(out[0], vs.numpy(), 1e-12, 1e-13, "identical keys out")
+
+
+def pin_scale(decode):
+    """(sigma*q, scale 1) and (q, scale sigma) give the same attention."""
+    batch = tiny_paged_batch()
+    sigma = batch.plan.sm_scale
+    a = decode(**decode_args(batch))
+    b = decode(**decode_args(batch, q=batch.q.double() * sigma, sm_scale=1.0))
+    _close(a[0], b[0], 1e-11, 1e-12, "scale out")
+    _close(a[1], b[1], 1e-12, 1e-12, "scale lse")
+
+
+def pin_layout_invariance(decode):
+    """Relabelling physical blocks changes nothing; reordering requests permutes."""
+    batch = tiny_paged_batch()
+    p = batch.plan
+    out, lse = decode(**decode_args(batch))
+    rng = np.random.default_rng(9)
+    perm = rng.permutation(p.num_blocks)           # old id -> new id
+    inv = np.argsort(perm)
+    k2, v2 = batch.k_pool[torch.from_numpy(inv)], batch.v_pool[torch.from_numpy(inv)]
+    o2, l2 = decode(**decode_args(batch, prefix_k=k2, prefix_v=v2, suffix_k=k2, suffix_v=v2,
+                                  prefix_tables=perm[p.prefix_tables],
+                                  suffix_tables=perm[p.suffix_tables]))
+    assert np.array_equal(out, o2) and np.array_equal(lse, l2), "block relabelling changed output"
+    order = rng.permutation(p.num_requests)
+    o3, l3 = decode(**decode_args(batch, q=batch.q[torch.from_numpy(order)],
+                                  suffix_tables=p.suffix_tables[order],
+                                  suffix_lens=p.suffix_lens[order],
+                                  group_ids=p.group_ids[order]))
+    assert np.array_equal(out[order], o3) and np.array_equal(lse[order], l3), \
+        "request reordering did not permute the output"
+
+
+def pin_decomposition(decode, merge):
+    """Prefix alone merged with suffix alone equals the whole context."""
+    batch = tiny_paged_batch()
+    p = batch.plan
+    whole = decode(**decode_args(batch))
+    pre = decode(**decode_args(batch, suffix_lens=np.zeros_like(p.suffix_lens)),
+                 requests=[r for r in range(p.num_requests) if p.group_ids[r] >= 0])
+    # suffix alone: the same requests made ungrouped
+    suf = decode(**decode_args(batch, group_ids=np.full_like(p.group_ids, -1)),
+                 requests=[r for r in range(p.num_requests) if p.suffix_lens[r] > 0])
+    grouped = [r for r in range(p.num_requests) if p.group_ids[r] >= 0]
+    withsuf = [r for r in range(p.num_requests) if p.suffix_lens[r] > 0]
+    H, D = p.heads, p.head_dim
+    for r in range(p.num_requests):
+        parts = []
+        if r in grouped:
+            i = grouped.index(r)
+            parts.append((pre[0][i], pre[1][i]))
+        if r in withsuf:
+            i = withsuf.index(r)
+            parts.append((suf[0][i], suf[1][i]))
+        o, l = merge(parts)
+        _close(o, whole[0][r], 1e-12, 1e-12, f"decomposition out {r}")
+        _close(l, whole[1][r], 1e-13, 1e-13, f"decomposition lse {r}")
+
+
+ALL_PINS = {
+    "worked_example": pin_worked_example,
+    "brute_force": pin_brute_force,
+    "sdpa": pin_sdpa,
+    "zero_query": pin_zero_query,
+    "spike": pin_spike,
+    "single_identical": pin_single_and_identical_keys,
+    "scale": pin_scale,
+    "layout_invariance": pin_layout_invariance,
+}

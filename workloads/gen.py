@@ -1,0 +1,283 @@
+"""Seeded generators for paged decode batches.
+
+Layout of a batch (the paged KV block layout of the library it feeds):
+  * K and V pools are [num_blocks, H, B, D] in the batch dtype.  Token t of a
+    sequence whose block table row is ``tbl`` lives at pool[tbl[t // B], h,
+    t % B, :].
+  * Each prefix group g owns a prefix block table row and a prefix length
+    P_g >= 1.  Each request r owns a suffix block table row and a suffix length
+    S_r >= 0; its group id is g, or -1 when it shares no prefix (then the whole
+    context is its suffix).  A request's keys are its group's P_g prefix tokens
+    followed by its own S_r suffix tokens.
+  * Unused token slots of a partly filled block are NaN, and unused block
+    table entries point at one all-NaN "poison" block, so any read past a
+    length shows up as NaN instead of a plausible number.
+
+Recipe (one plan per workload, shared by all its layers):
+  base = numpy default_rng(seed)  (PCG64)
+  1. prefix lengths, one per group, then suffix lengths of grouped requests
+     (group by group), then ungrouped context lengths;
+  2. physical block permutation (identity when the workload is contiguous);
+  3. request order permutation (identity when not shuffled).
+Values of layer l come from a torch CPU generator seeded with the first
+64-bit word (top bit cleared) of numpy's SeedSequence(seed).spawn(L)[l],
+drawn in this order:
+  q  = N(0,1) * q_scale  as float32, shape [R, H, D]
+  K  = N(0,1)            as float32, shape [NB, H, B, D]
+  V  = N(0,1)            as float32, shape [NB, H, B, D]
+then cast to the workload dtype with round-to-nearest-even.  The device
+recipe (``make_device_layers``) draws the same shapes with torch's Philox
+generator on the GPU instead; it is used where host generation of many
+gigabytes would be too slow, and its values differ from the host recipe.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from .configs import ConfigSpec
+
+TORCH_DTYPES = {
+    "float32": torch.float32,
+    "float16": torch.float16,
+    "bfloat16": torch.bfloat16,
+}
+
+
+def _draw_lengths(rng: np.random.Generator, recipe: tuple, n: int) -> np.ndarray:
+    kind = recipe[0]
+    if n == 0:
+        return np.zeros(0, dtype=np.int64)
+    if kind == "fixed":
+        return np.full(n, int(recipe[1]), dtype=np.int64)
+    if kind == "list":
+        vals = list(recipe[1])
+        if len(vals) != n:
+            raise ValueError(f"length list has {len(vals)} entries, need {n}")
+        return np.asarray(vals, dtype=np.int64)
+    if kind == "uniform":
+        a, b = int(recipe[1]), int(recipe[2])
+        return rng.integers(a, b, size=n, endpoint=True).astype(np.int64)
+    if kind == "lognormal":
+        median, sigma, lo, hi = recipe[1:]
+        x = rng.lognormal(mean=np.log(median), sigma=sigma, size=n)
+        return np.clip(np.round(x), lo, hi).astype(np.int64)
+    if kind == "sum_uniform":
+        (a1, b1), (a2, b2) = recipe[1], recipe[2]
+        x = rng.integers(a1, b1, size=n, endpoint=True)
+        y = rng.integers(a2, b2, size=n, endpoint=True)
+        return (x + y).astype(np.int64)
+    raise ValueError(f"unknown length recipe {recipe!r}")
+
+
+@dataclass
+class LayoutPlan:
+    """Lengths, group ids and block tables of one decode batch (no values)."""
+    heads: int
+    head_dim: int
+    block_size: int
+    dtype: str
+    sm_scale: float
+    q_scale: float
+    group_ids: np.ndarray        # int32 [R], -1 = no shared prefix
+    prefix_lens: np.ndarray      # int32 [NG]
+    suffix_lens: np.ndarray      # int32 [R]
+    prefix_tables: np.ndarray    # int32 [NG, prefix_stride]
+    suffix_tables: np.ndarray    # int32 [R, suffix_stride]
+    block_fill: np.ndarray       # int32 [NB] valid token slots per physical block
+    poison_block: int            # physical id of the all-NaN block
+
+    @property
+    def num_requests(self) -> int:
+        return int(self.group_ids.shape[0])
+
+    @property
+    def num_groups(self) -> int:
+        return int(self.prefix_lens.shape[0])
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self.block_fill.shape[0])
+
+    def group_sizes(self) -> list[int]:
+        return [int((self.group_ids == g).sum()) for g in range(self.num_groups)]
+
+    def context_lens(self) -> np.ndarray:
+        """P_{g(r)} + S_r for every request."""
+        p = np.where(self.group_ids >= 0,
+                     self.prefix_lens[np.maximum(self.group_ids, 0)] if self.num_groups
+                     else 0, 0)
+        return (p + self.suffix_lens).astype(np.int64)
+
+
+def build_plan(*, heads: int, head_dim: int, block_size: int, dtype: str,
+               group_of_request: Sequence[int], prefix_lens: Sequence[int],
+               suffix_lens: Sequence[int], sm_scale: float, q_scale: float = 1.0,
+               paged: bool = True, shuffle: bool = False,
+               rng: Optional[np.random.Generator] = None) -> LayoutPlan:
+    """Allocate blocks and tables for explicit lengths.
+
+    ``group_of_request``, ``suffix_lens`` are in pre-shuffle request order.
+    """
+    B = int(block_size)
+    gor = np.asarray(group_of_request, dtype=np.int64)
+    plen = np.asarray(prefix_lens, dtype=np.int64)
+    slen = np.asarray(suffix_lens, dtype=np.int64)
+    R, NG = gor.shape[0], plen.shape[0]
+    if slen.shape[0] != R:
+        raise ValueError("one suffix length per request is required")
+    if rng is None:
+        rng = np.random.default_rng(0)
+
+    # logical block ids: prefix blocks group by group, suffix blocks request by
+    # request, then the poison block
+    fills: list[int] = []
+    pre_logical: list[list[int]] = []
+    for g in range(NG):
+        n = -(-int(plen[g]) // B)
+        pre_logical.append(list(range(len(fills), len(fills) + n)))
+        fills += [B] * n
+        if n:
+            fills[-1] = int(plen[g]) - (n - 1) * B
+    suf_logical: list[list[int]] = []
+    for r in range(R):
+        n = -(-int(slen[r]) // B)
+        suf_logical.append(list(range(len(fills), len(fills) + n)))
+        fills += [B] * n
+        if n:
+            fills[-1] = int(slen[r]) - (n - 1) * B
+    poison_logical = len(fills)
+    fills.append(0)
+    NB = len(fills)
+
+    phys = rng.permutation(NB) if paged else np.arange(NB)
+    block_fill = np.zeros(NB, dtype=np.int32)
+    block_fill[phys] = np.asarray(fills, dtype=np.int32)
+    poison = int(phys[poison_logical])
+
+    pstride = max([1] + [len(x) for x in pre_logical])
+    sstride = max([1] + [len(x) for x in suf_logical])
+    ptab = np.full((NG, pstride), poison, dtype=np.int32)
+    for g, blocks in enumerate(pre_logical):
+        ptab[g, :len(blocks)] = phys[blocks]
+    stab = np.full((R, sstride), poison, dtype=np.int32)
+    for r, blocks in enumerate(suf_logical):
+        stab[r, :len(blocks)] = phys[blocks]
+
+    order = rng.permutation(R) if shuffle else np.arange(R)
+    return LayoutPlan(
+        heads=int(heads), head_dim=int(head_dim), block_size=B, dtype=dtype,
+        sm_scale=float(sm_scale), q_scale=float(q_scale),
+        group_ids=gor[order].astype(np.int32),
+        prefix_lens=plen.astype(np.int32),
+        suffix_lens=slen[order].astype(np.int32),
+        prefix_tables=ptab, suffix_tables=stab[order].copy(),
+        block_fill=block_fill, poison_block=poison)
+
+
+def make_plan(cfg: ConfigSpec) -> LayoutPlan:
+    rng = np.random.default_rng(cfg.seed)
+    NG = cfg.num_groups
+    plen = _draw_lengths(rng, cfg.prefix_len, NG)
+    n_grouped = sum(cfg.group_sizes)
+    slen_grouped = _draw_lengths(rng, cfg.suffix_len, n_grouped)
+    slen_ungrouped = _draw_lengths(rng, cfg.ungrouped_len, cfg.ungrouped)
+    gor = [g for g, n in enumerate(cfg.group_sizes) for _ in range(n)] + [-1] * cfg.ungrouped
+    slen = np.concatenate([slen_grouped, slen_ungrouped])
+    return build_plan(heads=cfg.heads, head_dim=cfg.head_dim, block_size=cfg.block_size,
+                      dtype=cfg.dtype, group_of_request=gor, prefix_lens=plen,
+                      suffix_lens=slen, sm_scale=cfg.sm_scale, q_scale=cfg.q_scale,
+                      paged=cfg.paged, shuffle=cfg.shuffle_requests, rng=rng)
+
+
+@dataclass
+class DecodeBatch:
+    """One layer of one decode iteration: a plan plus its values (CPU tensors)."""
+    plan: LayoutPlan
+    q: torch.Tensor          # [R, H, D]
+    k_pool: torch.Tensor     # [NB, H, B, D]
+    v_pool: torch.Tensor     # [NB, H, B, D]
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return TORCH_DTYPES[self.plan.dtype]
+
+    def int_arrays(self) -> dict:
+        p = self.plan
+        return dict(prefix_tables=p.prefix_tables, prefix_lens=p.prefix_lens,
+                    suffix_tables=p.suffix_tables, suffix_lens=p.suffix_lens,
+                    group_ids=p.group_ids)
+
+    def to(self, device) -> dict:
+        """Tensors of this batch on ``device`` (int arrays as int32 tensors)."""
+        out = {k: torch.from_numpy(np.ascontiguousarray(v)).to(device)
+               for k, v in self.int_arrays().items()}
+        out.update(q=self.q.to(device), k_pool=self.k_pool.to(device),
+                   v_pool=self.v_pool.to(device))
+        return out
+
+
+def _nan_slots_mask(plan: LayoutPlan) -> np.ndarray:
+    """bool [NB, B]: True where a block slot holds no token."""
+    slot = np.arange(plan.block_size)[None, :]
+    return slot >= plan.block_fill[:, None]
+
+
+def _layer_seed(seed: int, layer: int, layers: int) -> int:
+    child = np.random.SeedSequence(seed).spawn(layers)[layer]
+    return int(child.generate_state(1, dtype=np.uint64)[0] & ((1 << 63) - 1))
+
+
+def make_batch(plan: LayoutPlan, layer: int = 0, layers: int = 1, seed: int = 0) -> DecodeBatch:
+    """Host-drawn values for layer ``layer`` of ``layers``."""
+    g = torch.Generator()
+    g.manual_seed(_layer_seed(seed, layer, layers))
+    R, H, D, B, NB = plan.num_requests, plan.heads, plan.head_dim, plan.block_size, plan.num_blocks
+    q = torch.randn((R, H, D), generator=g, dtype=torch.float32)
+    if plan.q_scale != 1.0:
+        q.mul_(plan.q_scale)
+    k = torch.randn((NB, H, B, D), generator=g, dtype=torch.float32)
+    v = torch.randn((NB, H, B, D), generator=g, dtype=torch.float32)
+    mask = torch.from_numpy(_nan_slots_mask(plan))[:, None, :, None]
+    k.masked_fill_(mask, float("nan"))
+    v.masked_fill_(mask, float("nan"))
+    td = TORCH_DTYPES[plan.dtype]
+    return DecodeBatch(plan=plan, q=q.to(td), k_pool=k.to(td), v_pool=v.to(td))
+
+
+def make_device_layers(plan: LayoutPlan, layers: int, device, seed: int = 0) -> list[dict]:
+    """Device-drawn values for ``layers`` layers (torch Philox, seeded per layer).
+
+    Returns one dict per layer with q, k_pool, v_pool on ``device``; the int
+    arrays are shared by all layers and returned under the same keys.
+    """
+    td = TORCH_DTYPES[plan.dtype]
+    R, H, D, B, NB = plan.num_requests, plan.heads, plan.head_dim, plan.block_size, plan.num_blocks
+    ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(device)
+            for k, v in DecodeBatch(plan, None, None, None).int_arrays().items()}
+    mask = torch.from_numpy(_nan_slots_mask(plan)).to(device)[:, None, :, None]
+    out = []
+    for layer in range(layers):
+        g = torch.Generator(device=device)
+        g.manual_seed(int(seed) * 1_000_003 + 7919 * layer + 1)
+        q = torch.randn((R, H, D), generator=g, device=device, dtype=torch.float32)
+        if plan.q_scale != 1.0:
+            q.mul_(plan.q_scale)
+        pools = []
+        for _ in range(2):
+            x = torch.empty((NB, H, B, D), device=device, dtype=td)
+            # draw in slabs to bound the float32 staging buffer
+            step = max(1, (1 << 28) // max(1, H * B * D))
+            for s in range(0, NB, step):
+                e = min(NB, s + step)
+                x[s:e] = torch.randn((e - s, H, B, D), generator=g, device=device,
+                                     dtype=torch.float32).to(td)
+            x.masked_fill_(mask, float("nan"))
+            pools.append(x)
+        d = dict(ints)
+        d.update(q=q.to(td), k_pool=pools[0], v_pool=pools[1])
+        out.append(d)
+    return out
