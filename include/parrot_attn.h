@@ -1,0 +1,191 @@
+/*
+ * libparrot_attn -- shared-prefix decode attention for AMD MI355X (gfx950).
+ *
+ * One decode iteration of one attention layer for a batch of requests, where
+ * requests forked from a common parent context share that context's prompt
+ * prefix (Section 5.3, "Sharing Prompt Prefix"; Section 6, the engine's
+ * Fill/Generate with parent_context_id).  The shared prefix's keys and values
+ * are read once per group, not once per request: a prefix stage computes
+ * interim results (running max and exp-sum, here kept as an output vector and
+ * a log-sum-exp) for every member of the group, a non-shared stage does the
+ * same for each request's own tokens, and a merge joins them into the final
+ * attention output (Section 6, "Kernel Optimization").
+ *
+ * Result (per request r and head h; the paper defers the formula to the
+ * FlashAttention and PagedAttention work it builds on):
+ *   keys/values j = 0..N-1 are group g's P prefix tokens followed by r's S
+ *   own tokens (g = group_ids[r], P = prefix_lens[g] or 0 when g = -1,
+ *   S = suffix_lens[r], N = P + S >= 1),
+ *   s_j = sm_scale * <q[r,h,:], K_j>,  lse[r,h] = ln sum_j exp(s_j),
+ *   out[r,h,:] = sum_j exp(s_j - lse[r,h]) * V_j.
+ *
+ * Paged KV layout (Section 6: KV cache in non-contiguous blocks located
+ * through a per-request page table): a K or V pool is
+ *   [num_blocks][H][B][D] elements of `dtype`, row-major,
+ * and token t of a sequence with block-table row `tbl` is
+ *   pool[tbl[t / B]][h][t % B][:].
+ * A request's suffix starts at slot 0 of its own first block; the last block
+ * of a prefix or suffix may be partly filled (slots past the length are never
+ * read into a result, whatever they hold).
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns all
+ *     memory and the stream.  The library allocates nothing and keeps no
+ *     pointer after returning.  Calls are reentrant; concurrent calls need
+ *     distinct workspaces and outputs.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
+ *     and the call returns without synchronising.  Outputs are valid once the
+ *     stream reaches the end of the call's work.
+ *   - Every argument check runs before the first launch, so a call that
+ *     returns an error other than PARROT_ERR_HIP enqueued nothing.
+ *   - Device-side contents (lengths, group ids, block ids) are trusted: values
+ *     outside the bounds stated in parrot_problem give unspecified results,
+ *     but the kernels clamp every index so no access leaves the buffers whose
+ *     sizes the problem describes.  parrot_validate_inputs checks them.
+ *   - On error, parrot_last_error() returns a message for the calling thread.
+ */
+#ifndef PARROT_ATTN_H
+#define PARROT_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PARROT_ABI_VERSION 1
+
+typedef enum {
+  PARROT_OK = 0,
+  PARROT_ERR_INVALID_ARGUMENT = 1,   /* bad scalar, NULL or misaligned pointer */
+  PARROT_ERR_UNSUPPORTED = 2,        /* head_dim, block_size or dtype not built */
+  PARROT_ERR_WORKSPACE_TOO_SMALL = 3,
+  PARROT_ERR_HIP = 4                 /* a HIP call failed (launch, event, sync) */
+} parrot_status;
+
+typedef enum {
+  PARROT_DTYPE_F32 = 0,
+  PARROT_DTYPE_F16 = 1,
+  PARROT_DTYPE_BF16 = 2
+} parrot_dtype;
+
+/* Problem description: host scalars only.  Sizing and validation never read
+ * device memory. */
+typedef struct {
+  int32_t num_requests;        /* R >= 0; R = 0 is a no-op */
+  int32_t num_heads;           /* H >= 1; query heads = KV heads (multi-head) */
+  int32_t head_dim;            /* D: 64 or 128 */
+  int32_t block_size;          /* B: 16 tokens per KV block */
+  int32_t num_groups;          /* NG >= 0 prefix groups */
+  int32_t max_group_size;      /* >= members of any group; >= 1 when NG > 0 */
+  int32_t max_prefix_len;      /* >= prefix_lens[g] for all g; >= 1 when NG > 0 */
+  int32_t max_suffix_len;      /* >= suffix_lens[r] for all r; >= 0 */
+  int32_t prefix_table_stride; /* entries per prefix table row, >= ceil(max_prefix_len / B) */
+  int32_t suffix_table_stride; /* entries per suffix table row, >= ceil(max_suffix_len / B) */
+  int32_t num_prefix_blocks;   /* blocks in the prefix pools (>= 1 when NG > 0) */
+  int32_t num_suffix_blocks;   /* blocks in the suffix pools (>= 1) */
+  parrot_dtype dtype;          /* element type of q, the KV pools and out */
+  float sm_scale;              /* logits are sm_scale * q.k; finite */
+} parrot_problem;
+
+/* Optional timing hooks: hipEvent_t handles (may each be NULL) recorded on
+ * `stream` around the kernels of one call.  For parrot_per_request_decode the
+ * prefix kernel does not run and after_prefix is recorded right after
+ * `before`. */
+typedef struct {
+  void* before;          /* before the first kernel */
+  void* after_prefix;    /* after the prefix-group (MFMA) kernel */
+  void* after_splitkv;   /* after the split-KV (non-shared tokens) kernel */
+  void* after_merge;     /* after the log-sum-exp merge kernel */
+} parrot_trace;
+
+/* Bytes of device workspace either decode entry point needs for `p`
+ * (0 when R = 0).  Returns (size_t)-1 if `p` is invalid; the reason is then
+ * in parrot_last_error(). */
+size_t parrot_workspace_bytes(const parrot_problem* p);
+
+/*
+ * Shared-prefix decode attention (Section 5.3; Section 6, "Kernel
+ * Optimization").  Three kernels run on `stream` in order:
+ *   1. prefix-group kernel: for each (group, head, prefix chunk) the chunk's
+ *      K/V tiles are staged in LDS once and all members' queries are computed
+ *      against them on MFMA with an online softmax; one partial result per
+ *      member is written to the workspace;
+ *   2. split-KV kernel: each request's own tokens, in chunks, with 128-bit
+ *      coalesced loads; one partial per chunk;
+ *   3. merge kernel: log-sum-exp combination of all partials of (r, h).
+ *
+ *   q                    [R][H][D] dtype, 16-byte aligned
+ *   prefix_k, prefix_v   [num_prefix_blocks][H][B][D] dtype, 16-byte aligned
+ *                        (may be NULL when NG = 0)
+ *   suffix_k, suffix_v   [num_suffix_blocks][H][B][D] dtype, 16-byte aligned;
+ *                        may be the same pools as prefix_k / prefix_v
+ *   prefix_block_tables  int32 [NG][prefix_table_stride]
+ *   prefix_lens          int32 [NG], each in [1, max_prefix_len]
+ *   suffix_block_tables  int32 [R][suffix_table_stride]
+ *   suffix_lens          int32 [R], each in [0, max_suffix_len]
+ *   group_ids            int32 [R], -1 (no shared prefix) or in [0, NG);
+ *                        every request needs P + S >= 1
+ *   out                  [R][H][D] dtype (written, round-to-nearest-even)
+ *   lse                  float32 [R][H] natural-log log-sum-exp of the logits
+ *   workspace            >= parrot_workspace_bytes(p) bytes, 256-byte aligned;
+ *                        contents on entry are ignored
+ *   trace                optional (host) timing hooks, may be NULL
+ */
+parrot_status parrot_shared_prefix_decode(
+    const parrot_problem* p,
+    const void* q,
+    const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
+    void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/*
+ * Per-request decode attention over the same inputs without sharing: every
+ * request reads its group's prefix blocks itself, as a paged-attention
+ * decode kernel does (the baseline the paper compares against in Section 8.3).
+ * Same arguments, same results up to rounding; the prefix kernel is skipped.
+ */
+parrot_status parrot_per_request_decode(
+    const parrot_problem* p,
+    const void* q,
+    const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
+    void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/*
+ * Checks the device-side contents against `p` (a debugging aid; it
+ * synchronises `stream`): group ids in [-1, NG), prefix lengths in
+ * [1, max_prefix_len], suffix lengths in [0, max_suffix_len], P + S >= 1,
+ * and every block id a length reaches in [0, pool size).  Returns
+ * PARROT_ERR_INVALID_ARGUMENT with a message naming the first bad entry.
+ * `scratch` is >= 64 bytes of device memory, 4-byte aligned.
+ */
+parrot_status parrot_validate_inputs(
+    const parrot_problem* p,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, int32_t* scratch, void* stream);
+
+/* Message for the last failed call on this thread ("" if none).  Valid until
+ * the next call of this library on the same thread. */
+const char* parrot_last_error(void);
+
+/* PARROT_ABI_VERSION of the built library. */
+int parrot_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARROT_ATTN_H */

@@ -1,0 +1,230 @@
+"""ctypes binding of libparrot_attn (argument marshalling only).
+
+Every function here forwards to the C entry point of the same name in
+``include/parrot_attn.h``; torch tensors are passed as raw device pointers and
+the stream as torch's current HIP stream.  There is no fallback: if the shared
+library is missing or a call fails, an exception says so.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libparrot_attn.so")
+
+PARROT_OK = 0
+PARROT_ERR_INVALID_ARGUMENT = 1
+PARROT_ERR_UNSUPPORTED = 2
+PARROT_ERR_WORKSPACE_TOO_SMALL = 3
+PARROT_ERR_HIP = 4
+
+DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+
+class ParrotError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libparrot_attn status {status}: {msg}")
+        self.status = status
+
+
+class ParrotProblem(ctypes.Structure):
+    _fields_ = [
+        ("num_requests", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("num_groups", ctypes.c_int32),
+        ("max_group_size", ctypes.c_int32),
+        ("max_prefix_len", ctypes.c_int32),
+        ("max_suffix_len", ctypes.c_int32),
+        ("prefix_table_stride", ctypes.c_int32),
+        ("suffix_table_stride", ctypes.c_int32),
+        ("num_prefix_blocks", ctypes.c_int32),
+        ("num_suffix_blocks", ctypes.c_int32),
+        ("dtype", ctypes.c_int),
+        ("sm_scale", ctypes.c_float),
+    ]
+
+
+class ParrotTrace(ctypes.Structure):
+    _fields_ = [
+        ("before", ctypes.c_void_p),
+        ("after_prefix", ctypes.c_void_p),
+        ("after_splitkv", ctypes.c_void_p),
+        ("after_merge", ctypes.c_void_p),
+    ]
+
+
+EXPORTED = (
+    "parrot_workspace_bytes", "parrot_shared_prefix_decode", "parrot_per_request_decode",
+    "parrot_validate_inputs", "parrot_last_error", "parrot_abi_version",
+)
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2405_19888_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(path)
+    vp, i32p, sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t
+    prob_p = ctypes.POINTER(ParrotProblem)
+    lib.parrot_workspace_bytes.argtypes = [prob_p]
+    lib.parrot_workspace_bytes.restype = sz
+    dec_args = [prob_p, vp, vp, vp, vp, vp, i32p, i32p, i32p, i32p, i32p, vp, vp, vp, sz, vp,
+                ctypes.POINTER(ParrotTrace)]
+    for name in ("parrot_shared_prefix_decode", "parrot_per_request_decode"):
+        f = getattr(lib, name)
+        f.argtypes = dec_args
+        f.restype = ctypes.c_int
+    lib.parrot_validate_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, vp, vp]
+    lib.parrot_validate_inputs.restype = ctypes.c_int
+    lib.parrot_last_error.argtypes = []
+    lib.parrot_last_error.restype = ctypes.c_char_p
+    lib.parrot_abi_version.argtypes = []
+    lib.parrot_abi_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def parrot_last_error() -> str:
+    return load_library().parrot_last_error().decode()
+
+
+def parrot_abi_version() -> int:
+    return load_library().parrot_abi_version()
+
+
+def make_problem(*, num_requests, num_heads, head_dim, block_size, num_groups, max_group_size,
+                 max_prefix_len, max_suffix_len, prefix_table_stride, suffix_table_stride,
+                 num_prefix_blocks, num_suffix_blocks, dtype, sm_scale) -> ParrotProblem:
+    code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return ParrotProblem(int(num_requests), int(num_heads), int(head_dim), int(block_size),
+                         int(num_groups), int(max_group_size), int(max_prefix_len),
+                         int(max_suffix_len), int(prefix_table_stride), int(suffix_table_stride),
+                         int(num_prefix_blocks), int(num_suffix_blocks), code, float(sm_scale))
+
+
+def parrot_workspace_bytes(problem: ParrotProblem) -> int:
+    n = load_library().parrot_workspace_bytes(ctypes.byref(problem))
+    if n == ctypes.c_size_t(-1).value:
+        raise ParrotError(PARROT_ERR_INVALID_ARGUMENT, parrot_last_error())
+    return int(n)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _check(status: int):
+    if status != PARROT_OK:
+        raise ParrotError(status, parrot_last_error())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _decode(fn_name, problem, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+            prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+            stream=None, trace: Optional[ParrotTrace] = None):
+    lib = load_library()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    status = getattr(lib, fn_name)(
+        ctypes.byref(problem), _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(suffix_k),
+        _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(suffix_block_tables),
+        _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes,
+        _stream_handle(stream), ctypes.byref(trace) if trace is not None else None)
+    _check(status)
+
+
+def parrot_shared_prefix_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+                                prefix_block_tables, prefix_lens, suffix_block_tables,
+                                suffix_lens, group_ids, out, lse, workspace, stream=None,
+                                trace=None):
+    """Shared-prefix decode attention; writes ``out`` and ``lse`` (see the C header)."""
+    _decode("parrot_shared_prefix_decode", problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+            prefix_block_tables, prefix_lens, suffix_block_tables, suffix_lens, group_ids,
+            out, lse, workspace, stream, trace)
+
+
+def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+                              prefix_block_tables, prefix_lens, suffix_block_tables,
+                              suffix_lens, group_ids, out, lse, workspace, stream=None,
+                              trace=None):
+    """Per-request (no sharing) decode attention over the same inputs."""
+    _decode("parrot_per_request_decode", problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+            prefix_block_tables, prefix_lens, suffix_block_tables, suffix_lens, group_ids,
+            out, lse, workspace, stream, trace)
+
+
+def parrot_validate_inputs(problem, prefix_block_tables, prefix_lens, suffix_block_tables,
+                           suffix_lens, group_ids, scratch, stream=None):
+    """Device-side content check (synchronises the stream)."""
+    lib = load_library()
+    _check(lib.parrot_validate_inputs(
+        ctypes.byref(problem), _ptr(prefix_block_tables), _ptr(prefix_lens),
+        _ptr(suffix_block_tables), _ptr(suffix_lens), _ptr(group_ids), _ptr(scratch),
+        _stream_handle(stream)))
+
+
+def problem_from_host(*, num_heads, head_dim, block_size, dtype, sm_scale, group_ids, prefix_lens,
+                      suffix_lens, prefix_table_stride, suffix_table_stride, num_prefix_blocks,
+                      num_suffix_blocks) -> ParrotProblem:
+    """Fill a ParrotProblem from host copies of the batch metadata.
+
+    ``group_ids``, ``prefix_lens`` and ``suffix_lens`` are host sequences; only
+    their sizes and maxima are used (the serving engine knows them on the host).
+    """
+    import numpy as np
+    gid = np.asarray(group_ids)
+    plen = np.asarray(prefix_lens)
+    slen = np.asarray(suffix_lens)
+    ng = int(plen.shape[0])
+    sizes = np.bincount(gid[gid >= 0], minlength=max(ng, 1)) if gid.size else np.zeros(1, int)
+    return make_problem(
+        num_requests=gid.shape[0], num_heads=num_heads, head_dim=head_dim,
+        block_size=block_size, num_groups=ng, max_group_size=int(sizes.max()) if ng else 0,
+        max_prefix_len=int(plen.max()) if ng else 0,
+        max_suffix_len=int(slen.max()) if slen.size else 0,
+        prefix_table_stride=prefix_table_stride, suffix_table_stride=suffix_table_stride,
+        num_prefix_blocks=num_prefix_blocks, num_suffix_blocks=num_suffix_blocks,
+        dtype=dtype, sm_scale=sm_scale)
+
+
+class Decoder:
+    """Owns the output, lse and workspace buffers for one problem shape."""
+
+    def __init__(self, problem: ParrotProblem, device="cuda", out_dtype=None):
+        self.problem = problem
+        self.device = torch.device(device)
+        inv = {v: k for k, v in DTYPE_CODES.items()}
+        self.dtype = inv[problem.dtype] if out_dtype is None else out_dtype
+        R, H, D = problem.num_requests, problem.num_heads, problem.head_dim
+        self.out = torch.empty((R, H, D), dtype=self.dtype, device=self.device)
+        self.lse = torch.empty((R, H), dtype=torch.float32, device=self.device)
+        nbytes = parrot_workspace_bytes(problem)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+
+    def __call__(self, t: dict, shared: bool = True, stream=None, trace=None):
+        fn = parrot_shared_prefix_decode if shared else parrot_per_request_decode
+        fn(self.problem, t["q"], t.get("prefix_k", t.get("k_pool")), t.get("prefix_v", t.get("v_pool")),
+           t.get("suffix_k", t.get("k_pool")), t.get("suffix_v", t.get("v_pool")),
+           t["prefix_tables"], t["prefix_lens"], t["suffix_tables"], t["suffix_lens"],
+           t["group_ids"], self.out, self.lse, self.workspace, stream=stream, trace=trace)
+        return self.out, self.lse

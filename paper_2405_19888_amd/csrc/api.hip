@@ -1,0 +1,265 @@
+// C ABI of libparrot_attn: argument checks, work sizing and kernel launches.
+// Everything here runs on host scalars; no call reads device memory except
+// parrot_validate_inputs, which synchronises on purpose.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "parrot_attn.h"
+#include "common.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+parrot_status fail(parrot_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+long ceil_div(long a, long b) { return (a + b - 1) / b; }
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+// Chunk sizes and slot counts.  Chunks are whole 16-token blocks.  The prefix
+// chunk bounds both the per-workgroup LDS pipeline depth and the number of
+// partials written per member; the non-shared chunk is one wavefront's work.
+constexpr int kPrefixChunk = 256;
+constexpr int kSuffixChunk = 128;
+
+parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
+  if (!p) return fail(PARROT_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (p->num_requests < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_requests %d < 0", p->num_requests);
+  if (p->num_heads < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_heads %d < 1", p->num_heads);
+  if (p->num_groups < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_groups %d < 0", p->num_groups);
+  if (p->dtype != PARROT_DTYPE_F32 && p->dtype != PARROT_DTYPE_F16 && p->dtype != PARROT_DTYPE_BF16)
+    return fail(PARROT_ERR_UNSUPPORTED, "dtype %d is not f32, f16 or bf16", (int)p->dtype);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(PARROT_ERR_UNSUPPORTED, "head_dim %d (built for 64 and 128)", p->head_dim);
+  if (p->block_size != parrot::kBlock)
+    return fail(PARROT_ERR_UNSUPPORTED, "block_size %d (built for 16)", p->block_size);
+  if (!std::isfinite(p->sm_scale)) return fail(PARROT_ERR_INVALID_ARGUMENT, "sm_scale is not finite");
+  if (p->max_suffix_len < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_suffix_len %d < 0", p->max_suffix_len);
+  if (p->max_prefix_len < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_prefix_len %d < 0", p->max_prefix_len);
+  const int B = p->block_size;
+  if (p->num_groups > 0) {
+    if (p->max_prefix_len < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_prefix_len must be >= 1 when num_groups > 0");
+    if (p->max_group_size < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_group_size must be >= 1 when num_groups > 0");
+    if (p->max_group_size > p->num_requests && p->num_requests > 0)
+      return fail(PARROT_ERR_INVALID_ARGUMENT, "max_group_size %d > num_requests %d", p->max_group_size, p->num_requests);
+    if (p->prefix_table_stride < ceil_div(p->max_prefix_len, B))
+      return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_table_stride %d < ceil(max_prefix_len / block_size) = %ld",
+                  p->prefix_table_stride, ceil_div(p->max_prefix_len, B));
+    if (p->num_prefix_blocks < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_prefix_blocks must be >= 1 when num_groups > 0");
+  }
+  if (p->suffix_table_stride < ceil_div(p->max_suffix_len, B) || p->suffix_table_stride < 0)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "suffix_table_stride %d < ceil(max_suffix_len / block_size) = %ld",
+                p->suffix_table_stride, ceil_div(p->max_suffix_len, B));
+  if (p->num_suffix_blocks < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_suffix_blocks must be >= 1");
+  if (p->num_requests > 0 && p->num_groups == 0 && p->max_suffix_len == 0)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "no request can have a non-empty context (no groups, max_suffix_len 0)");
+
+  pl->cp = kPrefixChunk;
+  pl->cs = kSuffixChunk;
+  pl->seg_p = p->num_groups > 0 ? (int)ceil_div(p->max_prefix_len, pl->cp) : 0;
+  pl->seg_s = (int)ceil_div(p->max_suffix_len, pl->cs);
+  pl->seg = pl->seg_p + pl->seg_s;
+  const long mg = p->num_groups > 0 ? p->max_group_size : 1;
+  long waves = ceil_div(mg, 16);
+  waves = waves < 4 ? 4 : (waves > 8 ? 8 : waves);
+  pl->prefix_waves = (int)waves;
+  pl->prefix_qtiles = (int)ceil_div(mg, 16 * waves);
+
+  const double slots = (double)p->num_requests * p->num_heads * pl->seg;
+  const double grid_a = slots;                                               // split-KV waves
+  const double grid_b = (double)p->num_groups * pl->seg_p * p->num_heads * pl->prefix_qtiles;
+  if (grid_a / 4 > 2e9 || grid_b > 2e9 || slots * p->head_dim * 4.0 > 9e18)
+    return fail(PARROT_ERR_UNSUPPORTED, "problem too large for one launch (%.3g work items)", grid_a);
+  const size_t n_slots = (size_t)p->num_requests * p->num_heads * pl->seg;
+  auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
+  pl->lse_bytes = align256(n_slots * sizeof(float));
+  pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes : 0;
+  return PARROT_OK;
+}
+
+parrot_status record(void* ev, hipStream_t s) {
+  if (!ev) return PARROT_OK;
+  hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  return PARROT_OK;
+}
+
+parrot_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
+  return PARROT_OK;
+}
+
+#define PARROT_TRY(x) do { parrot_status _s = (x); if (_s != PARROT_OK) return _s; } while (0)
+
+parrot_status decode(bool shared, const parrot_problem* p, const void* q, const void* prefix_k,
+                     const void* prefix_v, const void* suffix_k, const void* suffix_v,
+                     const int32_t* ptab, const int32_t* plen, const int32_t* stab,
+                     const int32_t* slen, const int32_t* gid, void* out, float* lse,
+                     void* workspace, size_t workspace_bytes, void* stream,
+                     const parrot_trace* trace) {
+  parrot::Plan pl;
+  PARROT_TRY(check_problem(p, &pl));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr};
+  const parrot_trace& tr = trace ? *trace : none;
+  if (p->num_requests == 0) {
+    PARROT_TRY(record(tr.before, s)); PARROT_TRY(record(tr.after_prefix, s));
+    PARROT_TRY(record(tr.after_splitkv, s)); PARROT_TRY(record(tr.after_merge, s));
+    g_err.clear();
+    return PARROT_OK;
+  }
+  struct { const void* ptr; const char* name; size_t align; } req[] = {
+      {q, "q", 16}, {suffix_k, "suffix_k", 16}, {suffix_v, "suffix_v", 16},
+      {stab, "suffix_block_tables", 4}, {slen, "suffix_lens", 4}, {gid, "group_ids", 4},
+      {out, "out", 16}, {lse, "lse", 4}, {workspace, "workspace", 256}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", r.name);
+    if (!aligned(r.ptr, r.align)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", r.name, r.align);
+  }
+  if (p->num_groups > 0) {
+    struct { const void* ptr; const char* name; size_t align; } preq[] = {
+        {prefix_k, "prefix_k", 16}, {prefix_v, "prefix_v", 16},
+        {ptab, "prefix_block_tables", 4}, {plen, "prefix_lens", 4}};
+    for (auto& r : preq) {
+      if (!r.ptr) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", r.name);
+      if (!aligned(r.ptr, r.align)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", r.name, r.align);
+    }
+  }
+  if (workspace_bytes < pl.total_bytes)
+    return fail(PARROT_ERR_WORKSPACE_TOO_SMALL, "workspace is %zu bytes, need %zu", workspace_bytes, pl.total_bytes);
+
+  float* o_part = reinterpret_cast<float*>(workspace);
+  float* lse_part = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + pl.o_bytes);
+  const float scale_log2 = p->sm_scale * parrot::kLog2e;
+  const int D = p->head_dim, dt = (int)p->dtype;
+
+  PARROT_TRY(record(tr.before, s));
+  if (shared && p->num_groups > 0 && pl.seg_p > 0) {
+    parrot::PrefixArgs a{};
+    a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.ptab = ptab; a.plen = plen; a.gid = gid;
+    a.o_part = o_part; a.lse_part = lse_part;
+    a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
+    a.pstride = p->prefix_table_stride; a.max_p = p->max_prefix_len; a.npblk = p->num_prefix_blocks;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.qtiles = pl.prefix_qtiles;
+    a.scale_log2 = scale_log2;
+    PARROT_TRY(launched(parrot::launch_prefix(a, dt, D, pl.prefix_waves, s), "prefix-group kernel"));
+  }
+  PARROT_TRY(record(tr.after_prefix, s));
+  {
+    parrot::SplitKVArgs a{};
+    a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
+    a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
+    a.o_part = o_part; a.lse_part = lse_part;
+    a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
+    a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
+    a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
+    a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.cs = pl.cs;
+    a.first_c = shared ? pl.seg_p : 0;
+    a.nc = shared ? pl.seg_s : pl.seg;
+    a.scale_log2 = scale_log2;
+    if (a.nc > 0) PARROT_TRY(launched(parrot::launch_splitkv(a, dt, D, s), "split-KV kernel"));
+  }
+  PARROT_TRY(record(tr.after_splitkv, s));
+  {
+    parrot::MergeArgs a{};
+    a.o_part = o_part; a.lse_part = lse_part; a.plen = plen; a.slen = slen; a.gid = gid;
+    a.out = out; a.lse = lse;
+    a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
+    a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.cs = pl.cs;
+    PARROT_TRY(launched(parrot::launch_merge(a, dt, D, s), "merge kernel"));
+  }
+  PARROT_TRY(record(tr.after_merge, s));
+  g_err.clear();
+  return PARROT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t parrot_workspace_bytes(const parrot_problem* p) {
+  parrot::Plan pl;
+  if (check_problem(p, &pl) != PARROT_OK) return (size_t)-1;
+  g_err.clear();
+  return pl.total_bytes;
+}
+
+parrot_status parrot_shared_prefix_decode(
+    const parrot_problem* p, const void* q, const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v, const int32_t* prefix_block_tables,
+    const int32_t* prefix_lens, const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, void* out, float* lse, void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace) {
+  return decode(true, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+                prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+                workspace_bytes, stream, trace);
+}
+
+parrot_status parrot_per_request_decode(
+    const parrot_problem* p, const void* q, const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v, const int32_t* prefix_block_tables,
+    const int32_t* prefix_lens, const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, void* out, float* lse, void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace) {
+  return decode(false, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+                prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+                workspace_bytes, stream, trace);
+}
+
+parrot_status parrot_validate_inputs(const parrot_problem* p, const int32_t* prefix_block_tables,
+                                     const int32_t* prefix_lens, const int32_t* suffix_block_tables,
+                                     const int32_t* suffix_lens, const int32_t* group_ids,
+                                     int32_t* scratch, void* stream) {
+  parrot::Plan pl;
+  PARROT_TRY(check_problem(p, &pl));
+  if (p->num_requests == 0) { g_err.clear(); return PARROT_OK; }
+  if (!scratch || !aligned(scratch, 4)) return fail(PARROT_ERR_INVALID_ARGUMENT, "scratch is NULL or misaligned");
+  if (!suffix_block_tables || !suffix_lens || !group_ids)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "suffix tables, suffix lengths and group ids are required");
+  if (p->num_groups > 0 && (!prefix_block_tables || !prefix_lens))
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix tables and lengths are required when num_groups > 0");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemsetAsync(scratch, 0, 3 * sizeof(int32_t), s);
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "hipMemsetAsync: %s", hipGetErrorString(e));
+  parrot::ValidateArgs a{};
+  a.ptab = prefix_block_tables; a.plen = prefix_lens; a.stab = suffix_block_tables;
+  a.slen = suffix_lens; a.gid = group_ids; a.result = scratch;
+  a.R = p->num_requests; a.NG = p->num_groups; a.B = p->block_size;
+  a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
+  a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
+  a.npblk = p->num_prefix_blocks; a.nsblk = p->num_suffix_blocks;
+  PARROT_TRY(launched(parrot::launch_validate(a, s), "validation kernel"));
+  int32_t res[3] = {0, 0, 0};
+  e = hipMemcpyAsync(res, scratch, sizeof res, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "reading validation result: %s", hipGetErrorString(e));
+  static const char* what[] = {"", "group id out of [-1, num_groups)", "prefix length out of [1, max_prefix_len]",
+                               "suffix length out of [0, max_suffix_len]", "empty context (prefix + suffix = 0)",
+                               "prefix block id out of [0, num_prefix_blocks)",
+                               "suffix block id out of [0, num_suffix_blocks)"};
+  if (res[0] != 0)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "%s at entry %d (value %d)",
+                (res[0] > 0 && res[0] <= 6) ? what[res[0]] : "unknown", res[1], res[2]);
+  g_err.clear();
+  return PARROT_OK;
+}
+
+const char* parrot_last_error(void) { return g_err.c_str(); }
+
+int parrot_abi_version(void) { return PARROT_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,205 @@
+// Internal declarations shared by the kernels and the C-ABI layer of
+// libparrot_attn (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace parrot {
+
+// ---------------------------------------------------------------- constants
+constexpr int kBlock = 16;          // tokens per KV block
+constexpr int kWave = 64;           // CDNA wavefront
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Partial results live in the workspace as
+//   o_part  [R][H][seg][D] float32   (normalised partial output of one chunk)
+//   lse_part[R][H][seg]    float32   (base-2 log-sum-exp of the chunk's scaled logits)
+// Slots [0, seg_p) hold prefix chunks (chunk c covers prefix tokens
+// [c*cp, (c+1)*cp)), slots [seg_p, seg) hold the request's own tokens in chunks
+// of cs.  Both chunk sizes are multiples of kBlock.
+struct Plan {
+  int cp, cs;            // chunk tokens, prefix / non-shared
+  int seg_p, seg_s, seg; // slots per (request, head)
+  int prefix_waves;      // waves per prefix-kernel workgroup (16 queries each)
+  int prefix_qtiles;     // query tiles per group
+  size_t o_bytes, lse_bytes, total_bytes;
+};
+
+struct SplitKVArgs {
+  const void* q;
+  const void* pk; const void* pv;
+  const void* sk; const void* sv;
+  const int* ptab; const int* plen;
+  const int* stab; const int* slen;
+  const int* gid;
+  float* o_part; float* lse_part;
+  int R, H, NG;
+  int pstride, sstride;
+  int max_p, max_s;
+  int npblk, nsblk;
+  int seg, seg_p, cp, cs;
+  int first_c, nc;       // this launch covers slots [first_c, first_c + nc)
+  float scale_log2;      // sm_scale * log2(e)
+};
+
+struct PrefixArgs {
+  const void* q;
+  const void* pk; const void* pv;
+  const int* ptab; const int* plen; const int* gid;
+  float* o_part; float* lse_part;
+  int R, H, NG;
+  int pstride, max_p, npblk;
+  int seg, seg_p, cp;
+  int qtiles;            // query tiles per group (grid factor)
+  float scale_log2;
+};
+
+struct MergeArgs {
+  const float* o_part; const float* lse_part;
+  const int* plen; const int* slen; const int* gid;
+  void* out; float* lse;
+  int R, H, NG;
+  int max_p, max_s;
+  int seg, seg_p, cp, cs;
+};
+
+struct ValidateArgs {
+  const int* ptab; const int* plen; const int* stab; const int* slen; const int* gid;
+  int* result;           // [0] = error code, [1] = index, [2] = value
+  int R, NG, B;
+  int pstride, sstride, max_p, max_s, npblk, nsblk;
+};
+
+// dtype codes follow parrot_dtype
+enum Dtype { kF32 = 0, kF16 = 1, kBF16 = 2 };
+
+hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s);
+hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s);
+hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s);
+hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------ device helpers
+#if defined(__HIP_DEVICE_COMPILE__)
+#define PARROT_DEV __device__ __forceinline__
+#else
+#define PARROT_DEV __device__ inline
+#endif
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// DPP lane moves inside rows of 16 lanes (bound_ctrl: out-of-row reads give 0,
+// never used here because every control below stays inside its row).
+template <int CTRL>
+PARROT_DEV float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7-i within each 8
+constexpr int kDppMirror = 0x140;     // lane i <-> 15-i within each 16
+
+// Sum over aligned groups of N lanes (N = 4, 8, 16, 32, 64); every lane of the
+// group receives the total.
+template <int N>
+PARROT_DEV float group_sum(float x) {
+  static_assert(N == 4 || N == 8 || N == 16 || N == 32 || N == 64, "group size");
+  x += dpp_f<kDppXor1>(x);
+  x += dpp_f<kDppXor2>(x);
+  if constexpr (N >= 8) x += dpp_f<kDppHalfMirror>(x);
+  if constexpr (N >= 16) x += dpp_f<kDppMirror>(x);
+  if constexpr (N >= 32) x += __shfl_xor(x, 16);
+  if constexpr (N >= 64) x += __shfl_xor(x, 32);
+  return x;
+}
+
+PARROT_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+PARROT_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// 16-byte global load (kept as a plain vector load so the compiler emits
+// global_load_dwordx4).
+PARROT_DEV u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Reinterpret one 32-bit word as a pair of 16-bit floats.  The word is taken
+// by value on purpose: this compiler's __builtin_bit_cast applied directly to an
+// ext-vector element such as v.y reads element 0 instead.
+PARROT_DEV f16x2 as_f16x2(unsigned u) { return __builtin_bit_cast(f16x2, u); }
+PARROT_DEV bf16x2 as_bf16x2(unsigned u) { return __builtin_bit_cast(bf16x2, u); }
+
+// Element traits: conversion of the 16 bytes a lane loads into floats, and the
+// dot product of those bytes with the lane's query slice.
+template <int DT> struct Elem;
+
+template <> struct Elem<kF32> {
+  static constexpr int kBytes = 4;
+  static constexpr int kPerLoad = 4;
+  PARROT_DEV static void to_f32(const u32x4& v, float* f) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+  PARROT_DEV static float dot(const u32x4& k, const u32x4& q) {
+    float f[4], g[4];
+    to_f32(k, f); to_f32(q, g);
+    float s = f[0] * g[0];
+    s = __builtin_fmaf(f[1], g[1], s);
+    s = __builtin_fmaf(f[2], g[2], s);
+    return __builtin_fmaf(f[3], g[3], s);
+  }
+  PARROT_DEV static void store1(void* p, float x) { *reinterpret_cast<float*>(p) = x; }
+};
+
+template <> struct Elem<kF16> {
+  static constexpr int kBytes = 2;
+  static constexpr int kPerLoad = 8;
+  PARROT_DEV static void to_f32(const u32x4& v, float* f) {
+    const unsigned w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f16x2 h = as_f16x2(w[i]);
+      f[2 * i] = (float)h.x;
+      f[2 * i + 1] = (float)h.y;
+    }
+  }
+  PARROT_DEV static float dot(const u32x4& k, const u32x4& q) {
+    float s = __builtin_amdgcn_fdot2(as_f16x2(k.x), as_f16x2(q.x), 0.0f, false);
+    s = __builtin_amdgcn_fdot2(as_f16x2(k.y), as_f16x2(q.y), s, false);
+    s = __builtin_amdgcn_fdot2(as_f16x2(k.z), as_f16x2(q.z), s, false);
+    return __builtin_amdgcn_fdot2(as_f16x2(k.w), as_f16x2(q.w), s, false);
+  }
+  PARROT_DEV static void store1(void* p, float x) { *reinterpret_cast<_Float16*>(p) = (_Float16)x; }
+};
+
+template <> struct Elem<kBF16> {
+  static constexpr int kBytes = 2;
+  static constexpr int kPerLoad = 8;
+  PARROT_DEV static void to_f32(const u32x4& v, float* f) {
+    const unsigned w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  PARROT_DEV static float dot(const u32x4& k, const u32x4& q) {
+    float s = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.x), as_bf16x2(q.x), 0.0f, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.y), as_bf16x2(q.y), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.z), as_bf16x2(q.z), s, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(k.w), as_bf16x2(q.w), s, false);
+  }
+  PARROT_DEV static void store1(void* p, float x) { *reinterpret_cast<__bf16*>(p) = (__bf16)x; }
+};
+
+// Clamp helpers: device contents are trusted, but indices are clamped so that
+// a bad value can never move an access outside the buffers.
+PARROT_DEV int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+}  // namespace parrot

@@ -1,0 +1,138 @@
+// Log-sum-exp merge of the partial results of every (request, head), and the
+// device-side input validator.
+//
+// Partials of disjoint key sets combine exactly: with base-2 log-sum-exps
+// l_i and normalised outputs o_i, the union has l = log2 sum_i 2^{l_i} and
+// o = sum_i 2^{l_i - l} o_i (Section 6, "Kernel Optimization": the prefix's
+// interim results are amalgamated with the non-shared part).
+#include "common.h"
+
+namespace parrot {
+
+template <int N>
+PARROT_DEV float group_max(float x) {
+  x = fmaxf(x, dpp_f<kDppXor1>(x));
+  x = fmaxf(x, dpp_f<kDppXor2>(x));
+  x = fmaxf(x, dpp_f<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp_f<kDppMirror>(x));
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+
+// One wave per (request, head); each lane owns D/64 output elements.
+template <int DT, int D>
+__global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
+  using E = Elem<DT>;
+  constexpr int EPL = D / kWave;
+  const int lane = threadIdx.x & 63;
+  const long w = (long)blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (w >= (long)a.R * a.H) return;
+  const int r = (int)(w / a.H);
+  const int h = (int)(w % a.H);
+  const int g = a.gid[r];
+  const int P = (g >= 0 && g < a.NG) ? clampi(a.plen[g], 0, a.max_p) : 0;
+  const int S = clampi(a.slen[r], 0, a.max_s);
+  const int np = (P + a.cp - 1) / a.cp;
+  const int ns = (S + a.cs - 1) / a.cs;
+  const int n = np + ns;
+  const size_t base = (size_t)(r * a.H + h) * a.seg;
+  char* outp = (char*)a.out + ((size_t)(r * a.H + h) * D + lane * EPL) * E::kBytes;
+  if (n == 0) {  // empty context: defined as out = 0, lse = -inf
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) E::store1(outp + e * E::kBytes, 0.f);
+    if (lane == 0) a.lse[r * a.H + h] = -INFINITY;
+    return;
+  }
+  float mx = -INFINITY;
+  for (int i = lane; i < n; i += kWave) {
+    const int slot = i < np ? i : a.seg_p + (i - np);
+    mx = fmaxf(mx, a.lse_part[base + slot]);
+  }
+  mx = group_max<64>(mx);
+  float tot = 0.f;
+  for (int i = lane; i < n; i += kWave) {
+    const int slot = i < np ? i : a.seg_p + (i - np);
+    tot += fast_exp2(a.lse_part[base + slot] - mx);
+  }
+  tot = group_sum<64>(tot);
+  const float inv = 1.f / tot;
+  float acc[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  for (int i = 0; i < n; ++i) {
+    const int slot = i < np ? i : a.seg_p + (i - np);
+    const float wgt = fast_exp2(a.lse_part[base + slot] - mx) * inv;
+    const float* src = a.o_part + (base + slot) * D + lane * EPL;
+    if constexpr (EPL == 2) {
+      const float2 v = *reinterpret_cast<const float2*>(src);
+      acc[0] = __builtin_fmaf(wgt, v.x, acc[0]);
+      acc[1] = __builtin_fmaf(wgt, v.y, acc[1]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wgt, src[e], acc[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) E::store1(outp + e * E::kBytes, acc[e]);
+  if (lane == 0) a.lse[r * a.H + h] = (mx + fast_log2(tot)) * kLn2;
+}
+
+template <int DT, int D>
+static hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
+  const long waves = (long)a.R * a.H;
+  if (waves <= 0) return hipSuccess;
+  hipLaunchKernelGGL((k_merge<DT, D>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s) {
+  switch (dtype * 1000 + D) {
+    case kF32 * 1000 + 64: return launch_merge_t<kF32, 64>(a, s);
+    case kF32 * 1000 + 128: return launch_merge_t<kF32, 128>(a, s);
+    case kF16 * 1000 + 64: return launch_merge_t<kF16, 64>(a, s);
+    case kF16 * 1000 + 128: return launch_merge_t<kF16, 128>(a, s);
+    case kBF16 * 1000 + 64: return launch_merge_t<kBF16, 64>(a, s);
+    case kBF16 * 1000 + 128: return launch_merge_t<kBF16, 128>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// --------------------------------------------------------------- validation
+// Error codes written to result[0] (first failure wins): 1 bad group id,
+// 2 bad prefix length, 3 bad suffix length, 4 empty context, 5 prefix block id
+// out of the pool, 6 suffix block id out of the pool.  result[1] is the entry
+// index, result[2] the offending value.
+PARROT_DEV void report(int* res, int code, int idx, int val) {
+  if (atomicCAS(res, 0, code) == 0) { res[1] = idx; res[2] = val; }
+}
+
+__global__ __launch_bounds__(256) void k_validate(ValidateArgs a) {
+  for (int g = threadIdx.x; g < a.NG; g += blockDim.x) {
+    const int P = a.plen[g];
+    if (P < 1 || P > a.max_p) { report(a.result, 2, g, P); continue; }
+    for (int b = 0; b < (P + a.B - 1) / a.B; ++b) {
+      const int id = a.ptab[(long)g * a.pstride + b];
+      if (id < 0 || id >= a.npblk) report(a.result, 5, g * a.pstride + b, id);
+    }
+  }
+  for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
+    const int g = a.gid[r];
+    if (g < -1 || g >= a.NG) { report(a.result, 1, r, g); continue; }
+    const int S = a.slen[r];
+    if (S < 0 || S > a.max_s) { report(a.result, 3, r, S); continue; }
+    const int P = g >= 0 ? a.plen[g] : 0;
+    if (P + S < 1) report(a.result, 4, r, P + S);
+    for (int b = 0; b < (S + a.B - 1) / a.B; ++b) {
+      const int id = a.stab[(long)r * a.sstride + b];
+      if (id < 0 || id >= a.nsblk) report(a.result, 6, r * a.sstride + b, id);
+    }
+  }
+}
+
+hipError_t launch_validate(const ValidateArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_validate, dim3(1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace parrot

@@ -27,3 +27,13 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.fixture(scope="session")
+def parrot_lib():
+    """The built C library (built in-tree first if it is missing)."""
+    from paper_2405_19888_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2405_19888_amd.build import build
+        build()
+    return binding.load_library()

@@ -1,0 +1,73 @@
+"""Helpers for the GPU tests: run the HIP library on a workload and compare
+with the oracle at the stated tolerances.  No attention arithmetic here."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2405_19888_amd import Decoder, parrot_validate_inputs, problem_from_host
+from workloads.gen import TORCH_DTYPES
+
+# Tolerances: max |out_gpu - out_ref| over all elements (fp32-accumulated
+# results of fp16 / fp32 inputs 2e-3, bf16 inputs 8e-3); lse relative error
+# |d| / max(1, |ref|) <= 1e-4.  fp32 inputs also meet a tighter 1e-5.
+OUT_TOL = {"float16": 2e-3, "bfloat16": 8e-3, "float32": 2e-3}
+OUT_TOL_INTERNAL = {"float32": 1e-5}
+LSE_RTOL = 1e-4
+
+
+def problem_for(plan, num_prefix_blocks=None, num_suffix_blocks=None):
+    return problem_from_host(
+        num_heads=plan.heads, head_dim=plan.head_dim, block_size=plan.block_size,
+        dtype=TORCH_DTYPES[plan.dtype], sm_scale=plan.sm_scale, group_ids=plan.group_ids,
+        prefix_lens=plan.prefix_lens, suffix_lens=plan.suffix_lens,
+        prefix_table_stride=plan.prefix_tables.shape[1],
+        suffix_table_stride=plan.suffix_tables.shape[1],
+        num_prefix_blocks=num_prefix_blocks or plan.num_blocks,
+        num_suffix_blocks=num_suffix_blocks or plan.num_blocks)
+
+
+def run_gpu(plan, dev: dict, shared: bool = True, problem=None, poison: bool = True,
+            decoder: Decoder = None):
+    """Validate inputs on the device, poison outputs and workspace, run, sync."""
+    prob = problem or problem_for(plan)
+    dec = decoder or Decoder(prob)
+    scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
+    parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
+                           dev["suffix_lens"], dev["group_ids"], scratch)
+    if poison:
+        dec.out.fill_(float("nan"))
+        dec.lse.fill_(float("nan"))
+        dec.workspace.fill_(0xFF)          # every float slot reads as NaN
+    out, lse = dec(dev, shared=shared)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def to_np(out, lse):
+    return out.detach().double().cpu().numpy(), lse.detach().double().cpu().numpy()
+
+
+def oracle_for(batch_like, plan, requests=None, pools=None):
+    """The oracle on a batch (host tensors) or on device pools (gathered blocks only)."""
+    q = batch_like["q"] if isinstance(batch_like, dict) else batch_like.q
+    kp = pools[0] if pools else batch_like.k_pool
+    vp = pools[1] if pools else batch_like.v_pool
+    return oracle.shared_prefix_decode(
+        q.cpu() if isinstance(q, torch.Tensor) else q, kp, vp, kp, vp, plan.prefix_tables,
+        plan.prefix_lens, plan.suffix_tables, plan.suffix_lens, plan.group_ids, plan.sm_scale,
+        requests=requests)
+
+
+def assert_close(out, lse, ref_out, ref_lse, dtype: str, what: str = ""):
+    out = np.asarray(out, dtype=np.float64)
+    lse = np.asarray(lse, dtype=np.float64)
+    assert np.all(np.isfinite(out)), f"{what}: non-finite output"
+    assert np.all(np.isfinite(lse)), f"{what}: non-finite lse"
+    err = np.max(np.abs(out - ref_out)) if out.size else 0.0
+    lerr = np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) if lse.size else 0.0
+    tol = OUT_TOL_INTERNAL.get(dtype, OUT_TOL[dtype])
+    assert err <= tol, f"{what}: max |out err| {err:.3e} > {tol:.1e}"
+    assert lerr <= LSE_RTOL, f"{what}: max lse rel err {lerr:.3e} > {LSE_RTOL:.0e}"
+    return err, lerr

@@ -1,0 +1,143 @@
+"""The C ABI on the host: the library loads, exports every declared symbol,
+sizes workspaces, and rejects bad arguments before any device work.
+Runs without a GPU (no call here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2405_19888_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "parrot_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(parrot_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(parrot_lib):
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTED), names
+    for n in names:
+        assert hasattr(parrot_lib, n), f"{n} not exported"
+
+
+def test_abi_version(parrot_lib):
+    assert B.parrot_abi_version() == 1
+
+
+def base_problem(**over):
+    kw = dict(num_requests=32, num_heads=32, head_dim=128, block_size=16, num_groups=1,
+              max_group_size=32, max_prefix_len=2048, max_suffix_len=512,
+              prefix_table_stride=128, suffix_table_stride=32, num_prefix_blocks=1000,
+              num_suffix_blocks=1000, dtype=1, sm_scale=0.088)
+    kw.update(over)
+    return B.make_problem(**kw)
+
+
+def test_struct_layout_matches_header():
+    assert ctypes.sizeof(B.ParrotProblem) == 14 * 4
+    assert ctypes.sizeof(B.ParrotTrace) == 4 * ctypes.sizeof(ctypes.c_void_p)
+
+
+def test_workspace_sizes(parrot_lib):
+    assert B.parrot_workspace_bytes(base_problem(num_requests=0)) == 0
+    w0 = B.parrot_workspace_bytes(base_problem())
+    # 2048/256 prefix slots + 512/128 suffix slots, each D + 1 floats
+    assert w0 >= 32 * 32 * (8 + 4) * 129 * 4
+    for field, bigger in [("num_requests", 64), ("num_heads", 40), ("max_prefix_len", 4096),
+                          ("max_suffix_len", 1024), ("head_dim", 128)]:
+        kw = {field: bigger}
+        if field == "max_prefix_len":
+            kw["prefix_table_stride"] = 256
+        if field == "max_suffix_len":
+            kw["suffix_table_stride"] = 64
+        assert B.parrot_workspace_bytes(base_problem(**kw)) >= w0, field
+    assert B.parrot_workspace_bytes(base_problem(head_dim=64)) < w0
+
+
+@pytest.mark.parametrize("over,status,msg", [
+    (dict(head_dim=96), B.PARROT_ERR_UNSUPPORTED, "head_dim"),
+    (dict(block_size=32), B.PARROT_ERR_UNSUPPORTED, "block_size"),
+    (dict(dtype=7), B.PARROT_ERR_UNSUPPORTED, "dtype"),
+    (dict(num_heads=0), B.PARROT_ERR_INVALID_ARGUMENT, "num_heads"),
+    (dict(num_requests=-1), B.PARROT_ERR_INVALID_ARGUMENT, "num_requests"),
+    (dict(prefix_table_stride=10), B.PARROT_ERR_INVALID_ARGUMENT, "prefix_table_stride"),
+    (dict(suffix_table_stride=1), B.PARROT_ERR_INVALID_ARGUMENT, "suffix_table_stride"),
+    (dict(max_group_size=0), B.PARROT_ERR_INVALID_ARGUMENT, "max_group_size"),
+    (dict(max_group_size=33), B.PARROT_ERR_INVALID_ARGUMENT, "max_group_size"),
+    (dict(sm_scale=float("nan")), B.PARROT_ERR_INVALID_ARGUMENT, "sm_scale"),
+    (dict(num_groups=0, max_suffix_len=0, suffix_table_stride=0), B.PARROT_ERR_INVALID_ARGUMENT,
+     "non-empty"),
+])
+def test_bad_problem_rejected(parrot_lib, over, status, msg):
+    with pytest.raises(B.ParrotError) as e:
+        B.parrot_workspace_bytes(base_problem(**over))
+    assert msg in str(e.value)
+    # the decode entry points report the same status before touching the device
+    st = parrot_lib.parrot_shared_prefix_decode(ctypes.byref(base_problem(**over)), *([None] * 13),
+                                                0, None, None)
+    assert st == status and msg in B.parrot_last_error()
+
+
+FAKE = 1 << 20          # aligned fake device addresses: never dereferenced here
+
+
+def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
+    names = ["q", "pk", "pv", "sk", "sv", "ptab", "plen", "stab", "slen", "gid", "out", "lse", "ws"]
+    vals = {n: FAKE + 4096 * i for i, n in enumerate(names)}
+    vals.update(ptrs)
+    ws_bytes = ptrs.get("ws_bytes", 1 << 40)
+    vals.pop("ws_bytes", None)
+    return getattr(lib, fn)(ctypes.byref(prob), *[vals[n] for n in names], ws_bytes, None, None)
+
+
+@pytest.mark.parametrize("fn", ["parrot_shared_prefix_decode", "parrot_per_request_decode"])
+@pytest.mark.parametrize("field", ["q", "sk", "sv", "stab", "slen", "gid", "out", "lse", "ws",
+                                   "pk", "pv", "ptab", "plen"])
+def test_null_pointer_rejected(parrot_lib, fn, field):
+    st = call(parrot_lib, base_problem(), fn, **{field: None})
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT
+    assert "NULL" in B.parrot_last_error()
+
+
+@pytest.mark.parametrize("field,off", [("q", 8), ("out", 2), ("sk", 4), ("ws", 128), ("lse", 2),
+                                       ("gid", 1)])
+def test_misaligned_pointer_rejected(parrot_lib, field, off):
+    st = call(parrot_lib, base_problem(), **{field: FAKE + off})
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT
+    assert "aligned" in B.parrot_last_error()
+
+
+def test_workspace_too_small(parrot_lib):
+    prob = base_problem()
+    need = B.parrot_workspace_bytes(prob)
+    st = call(parrot_lib, prob, ws_bytes=need - 1)
+    assert st == B.PARROT_ERR_WORKSPACE_TOO_SMALL
+    assert str(need) in B.parrot_last_error()
+
+
+def test_prefix_pointers_optional_without_groups(parrot_lib):
+    prob = base_problem(num_groups=0, max_group_size=0, max_prefix_len=0, num_requests=0)
+    assert call(parrot_lib, prob, pk=None, pv=None, ptab=None, plen=None) == B.PARROT_OK
+
+
+def test_empty_batch_is_ok_without_device(parrot_lib):
+    prob = base_problem(num_requests=0)
+    assert call(parrot_lib, prob, q=None, out=None, lse=None, ws=None, ws_bytes=0) == B.PARROT_OK
+    assert B.parrot_last_error() == ""
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        B._lib_saved = B._lib
+        try:
+            B._lib = None
+            B.load_library(str(tmp_path / "nope.so"))
+        finally:
+            B._lib = B._lib_saved

@@ -1,0 +1,292 @@
+"""GPU parity: the HIP library (through its C ABI) against the float64 oracle.
+
+Every case prints its name before touching the GPU, validates the device-side
+inputs with parrot_validate_inputs, NaN-poisons the outputs and the workspace,
+and compares element by element (sampled requests at the largest sizes).
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import assert_close, oracle_for, problem_for, run_gpu, to_np
+from workloads import build_plan, get_config, make_batch, make_device_layer, make_plan
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["float16", "bfloat16", "float32"]
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def sample_requests(plan, k=12, seed=0):
+    R = plan.num_requests
+    rng = np.random.default_rng(seed)
+    ctx = plan.context_lens()
+    pick = {0, R - 1, int(np.argmax(ctx)), int(np.argmin(ctx)),
+            int(np.argmax(plan.suffix_lens)), int(np.argmin(plan.suffix_lens))}
+    pick |= set(rng.choice(R, size=min(k, R), replace=False).tolist())
+    return sorted(pick)
+
+
+# ------------------------------------------------------------------ workloads
+@pytest.mark.parametrize("shared", [True, False], ids=["shared", "per_request"])
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_config_full_parity(name, shared):
+    cfg = get_config(name)
+    say(name, cfg.name, "shared" if shared else "per_request")
+    plan = make_plan(cfg)
+    batch = make_batch(plan)
+    out, lse = run_gpu(plan, batch.to("cuda"), shared=shared)
+    ref = oracle_for(batch, plan)
+    assert_close(*to_np(out, lse), *ref, plan.dtype, f"{cfg.name} shared={shared}")
+
+
+@pytest.mark.parametrize("name", ["c3", "c4"])
+def test_config_sampled_parity(name):
+    cfg = get_config(name)
+    say(name, cfg.name)
+    plan = make_plan(cfg)
+    batch = make_batch(plan)
+    dev = batch.to("cuda")
+    out, lse = run_gpu(plan, dev, shared=True)
+    out_s, lse_s = to_np(out, lse)
+    reqs = sample_requests(plan)
+    ref = oracle_for(batch, plan, requests=reqs)
+    assert_close(out_s[reqs], lse_s[reqs], *ref, plan.dtype, f"{cfg.name} sampled")
+    # every request: finite, and the unshared path agrees within the same bar
+    out2, lse2 = run_gpu(plan, dev, shared=False)
+    o2, l2 = to_np(out2, lse2)
+    assert np.all(np.isfinite(out_s)) and np.all(np.isfinite(lse_s))
+    assert np.max(np.abs(out_s - o2)) <= 2e-3
+    assert np.max(np.abs(lse_s - l2) / np.maximum(1, np.abs(l2))) <= 1e-4
+
+
+def test_mixed_32_layer_serving_step():
+    """32 layers resident on the device (about 4 GB of bf16 KV each); every
+    layer is decoded, layers 0, 15 and 31 are checked on sampled requests."""
+    cfg = get_config("c5")
+    plan = make_plan(cfg)
+    say(cfg.name, "layers", cfg.layers, "blocks", plan.num_blocks)
+    layers = [make_device_layer(plan, l, "cuda") for l in range(cfg.layers)]
+    from paper_2405_19888_amd import Decoder
+    prob = problem_for(plan)
+    dec = Decoder(prob)
+    results = {}
+    for l, dev in enumerate(layers):
+        out, lse = dec(dev, shared=True)
+        if l in (0, 15, 31):
+            results[l] = (out.clone(), lse.clone())
+    torch.cuda.synchronize()
+    reqs = sample_requests(plan, k=6)
+    for l, (out, lse) in results.items():
+        say(cfg.name, "check layer", l, "requests", reqs)
+        o, s = to_np(out, lse)
+        assert np.all(np.isfinite(o)) and np.all(np.isfinite(s))
+        ref = oracle_for(layers[l], plan, requests=reqs,
+                         pools=(layers[l]["k_pool"], layers[l]["v_pool"]))
+        assert_close(o[reqs], s[reqs], *ref, plan.dtype, f"layer {l}")
+
+
+# ----------------------------------------------------------------- edge cases
+def edge_plan(kind, dtype, D, seed=0):
+    rng = np.random.default_rng(seed)
+    scale = 1.0 / math.sqrt(D)
+    if kind == "boundaries":
+        # groups of 3, 17 and 1 members; prefix lengths at chunk/block edges;
+        # suffix lengths at block and chunk edges, including 0; two ungrouped
+        gor = [0] * 3 + [1] * 17 + [2] + [-1, -1]
+        plen = [1, 257, 16]
+        sl = [0, 1, 15, 16, 17, 127, 128, 129, 255, 256, 257, 0, 3, 31, 33, 64, 100, 2, 5, 9,
+              129, 1, 300]
+        return build_plan(heads=3, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
+                          prefix_lens=plen, suffix_lens=sl, sm_scale=scale, shuffle=True, rng=rng)
+    if kind == "big_group":
+        n = 130
+        return build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype,
+                          group_of_request=[0] * n, prefix_lens=[40],
+                          suffix_lens=rng.integers(0, 40, size=n).tolist(), sm_scale=scale,
+                          shuffle=True, rng=rng)
+    if kind == "ungrouped":
+        return build_plan(heads=4, head_dim=D, block_size=16, dtype=dtype,
+                          group_of_request=[-1] * 5, prefix_lens=[],
+                          suffix_lens=[1, 16, 200, 513, 7], sm_scale=scale, rng=rng)
+    if kind == "single_key":
+        return build_plan(heads=1, head_dim=D, block_size=16, dtype=dtype, group_of_request=[0],
+                          prefix_lens=[1], suffix_lens=[0], sm_scale=scale, rng=rng)
+    if kind == "chunk_multiples":
+        return build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype,
+                          group_of_request=[0, 0, 1, 1, 1], prefix_lens=[256, 512],
+                          suffix_lens=[128, 256, 0, 384, 16], sm_scale=scale, shuffle=True, rng=rng)
+    raise ValueError(kind)
+
+
+EDGE_KINDS = ["boundaries", "big_group", "ungrouped", "single_key", "chunk_multiples"]
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("kind", EDGE_KINDS)
+def test_edge_cases(kind, dtype, D):
+    say("edge", kind, dtype, D)
+    plan = edge_plan(kind, dtype, D)
+    batch = make_batch(plan, seed=1)
+    dev = batch.to("cuda")
+    ref = oracle_for(batch, plan)
+    for shared in (True, False):
+        out, lse = run_gpu(plan, dev, shared=shared)
+        assert_close(*to_np(out, lse), *ref, dtype, f"{kind} {dtype} D={D} shared={shared}")
+
+
+def test_empty_batch_is_noop():
+    say("empty batch")
+    plan = edge_plan("ungrouped", "float16", 128)
+    prob = problem_for(plan)
+    prob.num_requests = 0
+    from paper_2405_19888_amd import parrot_shared_prefix_decode
+    z = torch.zeros(16, dtype=torch.float16, device="cuda")
+    zi = torch.zeros(4, dtype=torch.int32, device="cuda")
+    parrot_shared_prefix_decode(prob, z, z, z, z, z, zi, zi, zi, zi, zi, z, None, None)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
+def test_separate_prefix_and_suffix_pools(dtype):
+    """Prefix blocks are read from the prefix pools only, suffix blocks from the
+    suffix pools only: each pool has the other's blocks set to NaN."""
+    say("separate pools", dtype)
+    plan = edge_plan("boundaries", dtype, 128)
+    batch = make_batch(plan, seed=2)
+    dev = batch.to("cuda")
+    pre_blocks = set(int(x) for g in range(plan.num_groups)
+                     for x in plan.prefix_tables[g][: -(-int(plan.prefix_lens[g]) // 16)])
+    pre_idx = torch.tensor(sorted(pre_blocks), device="cuda")
+    suf_mask = torch.ones(plan.num_blocks, dtype=torch.bool, device="cuda")
+    suf_mask[pre_idx] = False
+    pk, pv = dev["k_pool"].clone(), dev["v_pool"].clone()
+    sk, sv = dev["k_pool"].clone(), dev["v_pool"].clone()
+    pk[suf_mask] = float("nan"); pv[suf_mask] = float("nan")
+    sk[pre_idx] = float("nan"); sv[pre_idx] = float("nan")
+    dev2 = dict(dev, prefix_k=pk, prefix_v=pv, suffix_k=sk, suffix_v=sv)
+    ref = oracle_for(batch, plan)
+    for shared in (True, False):
+        out, lse = run_gpu(plan, dev2, shared=shared)
+        assert_close(*to_np(out, lse), *ref, dtype, f"separate pools shared={shared}")
+
+
+# --------------------------------------------------------------------- probes
+def probe_plan(dtype):
+    rng = np.random.default_rng(7)
+    return build_plan(heads=2, head_dim=128, block_size=16, dtype=dtype,
+                      group_of_request=[0, 0, 0, -1], prefix_lens=[530],
+                      suffix_lens=[300, 0, 17, 260], sm_scale=1 / math.sqrt(128), shuffle=False,
+                      rng=rng)
+
+
+@pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
+def test_zero_query_probe(dtype):
+    """q = 0: lse = ln N exactly and out = mean of the N values (pins lengths)."""
+    say("zero-query probe", dtype)
+    plan = probe_plan(dtype)
+    batch = make_batch(plan, seed=3)
+    batch.q.zero_()
+    dev = batch.to("cuda")
+    ref_out, ref_lse = oracle_for(batch, plan)
+    N = plan.context_lens()
+    assert np.allclose(ref_lse, np.log(N)[:, None], rtol=1e-12, atol=0)
+    for shared in (True, False):
+        out, lse = run_gpu(plan, dev, shared=shared)
+        o, l = to_np(out, lse)
+        assert np.max(np.abs(l - ref_lse) / ref_lse) < 1e-6, f"shared={shared}"
+        assert np.max(np.abs(o - ref_out)) < (4e-3 if dtype == "bfloat16" else 5e-4)
+
+
+@pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
+def test_spike_probe(dtype):
+    """A key c*q with logit 40 dominates: out = its value, lse = its logit.
+    Positions cover block, prefix-chunk, suffix-chunk and sequence edges."""
+    say("spike probe", dtype)
+    plan = probe_plan(dtype)
+    base = make_batch(plan, seed=4)
+    B = 16
+    for r in (0, 3):
+        g = int(plan.group_ids[r])
+        P = int(plan.prefix_lens[g]) if g >= 0 else 0
+        N = int(plan.context_lens()[r])
+        for j in sorted({0, 15, 16, 255, 256, P - 1, P, P + 127, P + 128, N - 1}):
+            if not 0 <= j < N:
+                continue
+            k = base.k_pool.clone()
+            if j < P:
+                blk, slot = int(plan.prefix_tables[g][j // B]), j % B
+            else:
+                t = j - P
+                blk, slot = int(plan.suffix_tables[r][t // B]), t % B
+            for h in range(plan.heads):
+                qv = base.q[r, h].double()
+                c = 40.0 / (plan.sm_scale * float(qv @ qv))
+                k[blk, h, slot] = (c * qv).to(k.dtype)
+            batch = type(base)(plan=plan, q=base.q, k_pool=k, v_pool=base.v_pool)
+            dev = batch.to("cuda")
+            for shared in (True, False):
+                out, lse = run_gpu(plan, dev, shared=shared)
+                o, l = to_np(out, lse)
+                v = base.v_pool[blk, :, slot].double().numpy()
+                s = plan.sm_scale * (base.q[r].double() * k[blk, :, slot].double()).sum(-1).numpy()
+                assert np.max(np.abs(o[r] - v)) <= 1e-3 * max(1.0, np.abs(v).max()), \
+                    f"spike r={r} j={j} shared={shared}"
+                assert np.max(np.abs(l[r] - s) / np.abs(s)) < 1e-5, f"spike lse r={r} j={j}"
+
+
+# ------------------------------------------------------------ other properties
+def test_bitwise_reproducible():
+    say("reproducibility")
+    plan = make_plan(get_config("c2"))
+    dev = make_batch(plan).to("cuda")
+    a = [t.clone() for t in run_gpu(plan, dev)]
+    b = run_gpu(plan, dev)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_validate_inputs_reports_bad_entries():
+    say("validate")
+    from paper_2405_19888_amd import ParrotError, parrot_validate_inputs
+    plan = edge_plan("boundaries", "float16", 128)
+    dev = make_batch(plan).to("cuda")
+    prob = problem_for(plan)
+    scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
+    parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
+                           dev["suffix_lens"], dev["group_ids"], scratch)
+    bad = dev["suffix_tables"].clone()
+    r = int(np.argmax(plan.suffix_lens))
+    bad[r, 0] = plan.num_blocks + 5
+    with pytest.raises(ParrotError, match="suffix block id"):
+        parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], bad,
+                               dev["suffix_lens"], dev["group_ids"], scratch)
+    badg = dev["group_ids"].clone()
+    badg[1] = plan.num_groups
+    with pytest.raises(ParrotError, match="group id"):
+        parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
+                               dev["suffix_lens"], badg, scratch)
+
+
+def test_trace_events_bracket_the_kernels():
+    say("trace events")
+    from paper_2405_19888_amd import Decoder, ParrotTrace
+    plan = make_plan(get_config("c2"))
+    dev = make_batch(plan).to("cuda")
+    dec = Decoder(problem_for(plan))
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in evs:
+        e.record()
+    torch.cuda.synchronize()
+    tr = ParrotTrace(*[e.cuda_event for e in evs])
+    dec(dev, shared=True, trace=tr)
+    torch.cuda.synchronize()
+    times = [evs[i].elapsed_time(evs[i + 1]) for i in range(3)]
+    assert all(t >= 0 for t in times) and sum(times) > 0

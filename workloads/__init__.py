@@ -6,9 +6,9 @@ arithmetic, so that the CPU oracle (``oracle/``) and the HIP library
 (``paper_2405_19888_amd``) can both be fed from it without sharing code.
 """
 from .configs import CONFIGS, ConfigSpec, get_config, zipf_group_sizes
-from .gen import DecodeBatch, LayoutPlan, build_plan, make_plan, make_batch, make_device_layers
+from .gen import DecodeBatch, LayoutPlan, build_plan, make_plan, make_batch, make_device_layer, make_device_layers
 
 __all__ = [
     "CONFIGS", "ConfigSpec", "get_config", "zipf_group_sizes",
-    "DecodeBatch", "LayoutPlan", "build_plan", "make_plan", "make_batch", "make_device_layers",
+    "DecodeBatch", "LayoutPlan", "build_plan", "make_plan", "make_batch", "make_device_layer", "make_device_layers",
 ]

@@ -248,36 +248,37 @@ def make_batch(plan: LayoutPlan, layer: int = 0, layers: int = 1, seed: int = 0)
     return DecodeBatch(plan=plan, q=q.to(td), k_pool=k.to(td), v_pool=v.to(td))
 
 
-def make_device_layers(plan: LayoutPlan, layers: int, device, seed: int = 0) -> list[dict]:
-    """Device-drawn values for ``layers`` layers (torch Philox, seeded per layer).
+def make_device_layer(plan: LayoutPlan, layer: int, device, seed: int = 0) -> dict:
+    """Device-drawn values of one layer (torch Philox on ``device``).
 
-    Returns one dict per layer with q, k_pool, v_pool on ``device``; the int
-    arrays are shared by all layers and returned under the same keys.
+    Returns q, k_pool, v_pool on ``device`` plus the int arrays as int32
+    tensors.  Layer l uses generator seed seed * 1000003 + 7919 * l + 1.
     """
     td = TORCH_DTYPES[plan.dtype]
     R, H, D, B, NB = plan.num_requests, plan.heads, plan.head_dim, plan.block_size, plan.num_blocks
-    ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(device)
-            for k, v in DecodeBatch(plan, None, None, None).int_arrays().items()}
+    out = {k: torch.from_numpy(np.ascontiguousarray(v)).to(device)
+           for k, v in DecodeBatch(plan, None, None, None).int_arrays().items()}
     mask = torch.from_numpy(_nan_slots_mask(plan)).to(device)[:, None, :, None]
-    out = []
-    for layer in range(layers):
-        g = torch.Generator(device=device)
-        g.manual_seed(int(seed) * 1_000_003 + 7919 * layer + 1)
-        q = torch.randn((R, H, D), generator=g, device=device, dtype=torch.float32)
-        if plan.q_scale != 1.0:
-            q.mul_(plan.q_scale)
-        pools = []
-        for _ in range(2):
-            x = torch.empty((NB, H, B, D), device=device, dtype=td)
-            # draw in slabs to bound the float32 staging buffer
-            step = max(1, (1 << 28) // max(1, H * B * D))
-            for s in range(0, NB, step):
-                e = min(NB, s + step)
-                x[s:e] = torch.randn((e - s, H, B, D), generator=g, device=device,
-                                     dtype=torch.float32).to(td)
-            x.masked_fill_(mask, float("nan"))
-            pools.append(x)
-        d = dict(ints)
-        d.update(q=q.to(td), k_pool=pools[0], v_pool=pools[1])
-        out.append(d)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1_000_003 + 7919 * int(layer) + 1)
+    q = torch.randn((R, H, D), generator=g, device=device, dtype=torch.float32)
+    if plan.q_scale != 1.0:
+        q.mul_(plan.q_scale)
+    pools = []
+    for _ in range(2):
+        x = torch.empty((NB, H, B, D), device=device, dtype=td)
+        # draw in slabs to bound the float32 staging buffer
+        step = max(1, (1 << 27) // max(1, H * B * D))
+        for s in range(0, NB, step):
+            e = min(NB, s + step)
+            x[s:e] = torch.randn((e - s, H, B, D), generator=g, device=device,
+                                 dtype=torch.float32).to(td)
+        x.masked_fill_(mask, float("nan"))
+        pools.append(x)
+    out.update(q=q.to(td), k_pool=pools[0], v_pool=pools[1])
     return out
+
+
+def make_device_layers(plan: LayoutPlan, layers: int, device, seed: int = 0) -> list[dict]:
+    """``make_device_layer`` for layers 0..layers-1."""
+    return [make_device_layer(plan, l, device, seed) for l in range(layers)]
