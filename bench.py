@@ -1,0 +1,241 @@
+"""Benchmark: shared-prefix decode attention on one MI355X.
+
+One step is one call of parrot_shared_prefix_decode (prefix-group kernel,
+split-KV kernel, merge kernel) for one layer of a decode batch.  The default
+workload is the LLaMA-7B layer shape: 32 heads x 128, fp16 KV in 16-token
+blocks with permuted block tables, one prefix group of 32 requests sharing a
+2048-token prefix, own lengths U[64,512].  Steps cycle through `--layers`
+layers with distinct KV values, all resident in HBM, so a layer's KV is not
+still in the 256 MB Infinity Cache when it is read again.
+
+Prints one JSON line.  `value` is requests per second per layer
+(R / seconds per step).  The `roofline` object describes the dominant kernel
+(split-KV) from HIP events recorded on the launch stream around it during the
+timed steps; `cpu_baseline` times the float64 CPU oracle on a bounded sample
+of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16/bf16 MFMA
+ELT_BYTES = {"float32": 4, "float16": 2, "bfloat16": 2}
+DTYPE_TAG = {"float32": "f32", "float16": "f16", "bfloat16": "bf16"}
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "splitkv_counters.json")
+KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/splitkv.hip", "paper_2405_19888_amd/csrc/common.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(plan):
+    """Bytes the method must move, per layer (no partials, no re-reads)."""
+    elt = ELT_BYTES[plan.dtype]
+    kv_tok = 2 * plan.heads * plan.head_dim * elt
+    R = plan.num_requests
+    q = R * plan.heads * plan.head_dim * elt
+    out = q
+    lse = R * plan.heads * 4
+    prefix_kv = int(plan.prefix_lens.sum()) * kv_tok
+    suffix_kv = int(plan.suffix_lens.sum()) * kv_tok
+    naive_kv = int(plan.context_lens().sum()) * kv_tok
+    sizes = plan.group_sizes()
+    prefix_flops = sum(4 * plan.head_dim * plan.heads * sizes[g] * int(plan.prefix_lens[g])
+                       for g in range(plan.num_groups))
+    return dict(prefix_kv=prefix_kv, suffix_kv=suffix_kv, q=q, out=out, lse=lse,
+                shared_total=prefix_kv + suffix_kv + q + out + lse,
+                splitkv=suffix_kv + q,
+                naive_total=naive_kv + q + out + lse,
+                prefix_flops=prefix_flops)
+
+
+def cpu_baseline(plan, layer_dev, budget_s: float):
+    """The oracle on host copies of one layer, request by request, for ~budget_s."""
+    import numpy as np
+    import torch
+    import oracle
+
+    q = layer_dev["q"].cpu()
+    kp = layer_dev["k_pool"].cpu()
+    vp = layer_dev["v_pool"].cpu()
+    t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
+    done = 0
+    order = np.random.default_rng(0).permutation(plan.num_requests)
+    while True:
+        r = int(order[done % plan.num_requests])
+        oracle.shared_prefix_decode(q, kp, vp, kp, vp, plan.prefix_tables, plan.prefix_lens,
+                                    plan.suffix_tables, plan.suffix_lens, plan.group_ids,
+                                    plan.sm_scale, requests=[r])
+        done += 1
+        wall = time.perf_counter() - t_wall0
+        if wall >= budget_s:
+            break
+    cpu = time.process_time() - t_cpu0
+    return {
+        "value": done / wall,
+        "unit": "req/s per layer",
+        "cores": max(1, int(round(cpu / wall))),
+        "cores_available": len(os.sched_getaffinity(0)),
+        "kind": "oracle",
+        "sample": f"{done} requests of one layer of the same workload, one oracle call each, "
+                  f"{wall:.1f} s wall, {cpu:.1f} s CPU",
+    }
+
+
+def traffic_from_counters(plan_key: str):
+    """HBM bytes per split-KV launch from committed rocprofv3 counter runs,
+    only if they were taken on the current kernel source."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    with open(COUNTERS_FILE) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != kernel_source_hash() or rec.get("workload") != plan_key:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--layers", type=int, default=8, help="distinct-KV layers cycled by the steps")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle timing")
+    ap.add_argument("--no-baselines", action="store_true", help="skip the per-request and CPU legs")
+    ap.add_argument("--no-trace", action="store_true", help="time without per-kernel events")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU: run with --gpus 1 "
+                                   "(no multi-GPU path exists)"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2405_19888_amd import Decoder, ParrotTrace, parrot_validate_inputs, problem_from_host
+    from workloads import get_config, make_device_layer, make_plan
+    from workloads.gen import TORCH_DTYPES
+
+    cfg = get_config(args.config)
+    if cfg.layers != 1:
+        raise SystemExit(f"{cfg.name} has {cfg.layers} layers; bench one-layer workloads")
+    plan = make_plan(cfg)
+    dev = "cuda"
+    layers = [make_device_layer(plan, l, dev, seed=cfg.seed) for l in range(args.layers)]
+    prob = problem_from_host(
+        num_heads=plan.heads, head_dim=plan.head_dim, block_size=plan.block_size,
+        dtype=TORCH_DTYPES[plan.dtype], sm_scale=plan.sm_scale, group_ids=plan.group_ids,
+        prefix_lens=plan.prefix_lens, suffix_lens=plan.suffix_lens,
+        prefix_table_stride=plan.prefix_tables.shape[1],
+        suffix_table_stride=plan.suffix_tables.shape[1],
+        num_prefix_blocks=plan.num_blocks, num_suffix_blocks=plan.num_blocks)
+    scratch = torch.zeros(16, dtype=torch.int32, device=dev)
+    parrot_validate_inputs(prob, layers[0]["prefix_tables"], layers[0]["prefix_lens"],
+                           layers[0]["suffix_tables"], layers[0]["suffix_lens"],
+                           layers[0]["group_ids"], scratch)
+    dec = Decoder(prob, device=dev)
+    stream = torch.cuda.current_stream()
+    ab = algorithmic_bytes(plan)
+    K, W, L = args.steps, args.warmup, args.layers
+
+    def run(shared: bool, trace: bool):
+        events = None
+        if trace:
+            events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+            for evs in events:
+                for e in evs:
+                    e.record(stream)
+        traces = [ParrotTrace(*[e.cuda_event for e in evs]) for evs in events] if trace else None
+        for i in range(W):
+            dec(layers[i % L], shared=shared, stream=stream)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            dec(layers[i % L], shared=shared, stream=stream,
+                trace=traces[i] if trace else None)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per = None
+        if trace:
+            per = {"prefix_us": 0.0, "splitkv_us": 0.0, "merge_us": 0.0}
+            for evs in events:
+                per["prefix_us"] += evs[0].elapsed_time(evs[1]) * 1e3
+                per["splitkv_us"] += evs[1].elapsed_time(evs[2]) * 1e3
+                per["merge_us"] += evs[2].elapsed_time(evs[3]) * 1e3
+            per = {k: v / K for k, v in per.items()}
+        return wall, per
+
+    wall, per = run(shared=True, trace=not args.no_trace)
+    ms_per_step = wall / K * 1e3
+    R = plan.num_requests
+    value = R / (wall / K)
+    result = {
+        "metric": "decode-attention requests/sec per layer",
+        "value": round(value, 1),
+        "unit": "req/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": DTYPE_TAG[plan.dtype],
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name, "requests": R, "heads": plan.heads, "head_dim": plan.head_dim,
+            "prefix_groups": plan.num_groups, "group_sizes": plan.group_sizes(),
+            "prefix_lens": [int(x) for x in plan.prefix_lens],
+            "suffix_len_mean": round(float(plan.suffix_lens.mean()), 1),
+            "kv_block": plan.block_size, "kv_dtype": DTYPE_TAG[plan.dtype],
+            "layers_cycled": L, "timing": "HBM-resident inputs, distinct KV per cycled layer",
+        },
+        "hbm_gbps": round(ab["shared_total"] / (wall / K) / 1e9, 1),
+    }
+    result["hbm_frac"] = round(result["hbm_gbps"] / HBM_PEAK_GBPS, 4)
+    if per is not None:
+        achieved = ab["splitkv"] / (per["splitkv_us"] * 1e-6) / 1e9
+        traffic = traffic_from_counters(cfg.name)
+        result["roofline"] = {
+            "kernel": "k_splitkv (own tokens of every request)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": ab["splitkv"],
+            "avg_us": round(per["splitkv_us"], 3),
+        }
+        prefix_s = per["prefix_us"] * 1e-6
+        result["kernels_us"] = {k: round(v, 3) for k, v in per.items()}
+        result["prefix_kernel"] = {
+            "hbm_gbps": round(ab["prefix_kv"] / prefix_s / 1e9, 1),
+            "mfma_tflops": round(ab["prefix_flops"] / prefix_s / 1e12, 2),
+            "mfma_util": round(ab["prefix_flops"] / prefix_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+        }
+    if not args.no_baselines:
+        wall_n, _ = run(shared=False, trace=False)
+        result["per_request_baseline"] = {
+            "value": round(R / (wall_n / K), 1), "unit": "req/s",
+            "ms_per_step": round(wall_n / K * 1e3, 5),
+            "speedup_of_shared": round(wall_n / wall, 3),
+            "hbm_gbps": round(ab["naive_total"] / (wall_n / K) / 1e9, 1),
+        }
+        result["cpu_baseline"] = cpu_baseline(plan, layers[0], args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
