@@ -118,6 +118,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle timing")
     ap.add_argument("--no-baselines", action="store_true", help="skip the per-request and CPU legs")
     ap.add_argument("--no-trace", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--trace-every", type=int, default=16,
+                    help="attach per-kernel HIP events to every N-th timed step (each traced "
+                         "launch costs a few microseconds of stream time)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -152,31 +155,37 @@ def main():
     ab = algorithmic_bytes(plan)
     K, W, L = args.steps, args.warmup, args.layers
 
+    names = ("prefix", "splitkv", "merge")
+
     def run(shared: bool, trace: bool):
-        events = None
-        if trace:
-            events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-            for evs in events:
-                for e in evs:
-                    e.record(stream)
-        traces = [ParrotTrace(*[e.cuda_event for e in evs]) for evs in events] if trace else None
+        """W untimed steps, then K timed steps; every `trace_every`-th timed step
+        carries per-kernel (start, stop) event pairs when `trace` is set."""
+        calls = [dec.bind(layers[l], shared=shared, stream=stream) for l in range(L)]
+        every = max(1, args.trace_every)
+        traced = list(range(0, K, every)) if trace else []
+        events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for i in traced}
+        for evs in events.values():       # materialise the events outside the timed region
+            for e in evs:
+                e.record(stream)
+        torch.cuda.synchronize()
+        traces = {i: ParrotTrace(*[e.cuda_event for e in evs]) for i, evs in events.items()}
         for i in range(W):
-            dec(layers[i % L], shared=shared, stream=stream)
+            calls[i % L]()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(K):
-            dec(layers[i % L], shared=shared, stream=stream,
-                trace=traces[i] if trace else None)
+            calls[i % L](traces.get(i))
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         per = None
         if trace:
-            per = {"prefix_us": 0.0, "splitkv_us": 0.0, "merge_us": 0.0}
-            for evs in events:
-                per["prefix_us"] += evs[0].elapsed_time(evs[1]) * 1e3
-                per["splitkv_us"] += evs[1].elapsed_time(evs[2]) * 1e3
-                per["merge_us"] += evs[2].elapsed_time(evs[3]) * 1e3
-            per = {k: v / K for k, v in per.items()}
+            per = {}
+            for k, name in enumerate(names):
+                if name == "prefix" and not shared:
+                    continue
+                per[name + "_us"] = sum(evs[2 * k].elapsed_time(evs[2 * k + 1])
+                                        for evs in events.values()) * 1e3 / len(events)
+            per["traced_steps"] = len(events)
         return wall, per
 
     wall, per = run(shared=True, trace=not args.no_trace)
@@ -219,7 +228,8 @@ def main():
             "avg_us": round(per["splitkv_us"], 3),
         }
         prefix_s = per["prefix_us"] * 1e-6
-        result["kernels_us"] = {k: round(v, 3) for k, v in per.items()}
+        result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
+        result["kernels_us"]["traced_steps"] = per["traced_steps"]
         result["prefix_kernel"] = {
             "hbm_gbps": round(ab["prefix_kv"] / prefix_s / 1e9, 1),
             "mfma_tflops": round(ab["prefix_flops"] / prefix_s / 1e12, 2),

@@ -89,15 +89,18 @@ typedef struct {
   float sm_scale;              /* logits are sm_scale * q.k; finite */
 } parrot_problem;
 
-/* Optional timing hooks: hipEvent_t handles (may each be NULL) recorded on
- * `stream` around the kernels of one call.  For parrot_per_request_decode the
- * prefix kernel does not run and after_prefix is recorded right after
- * `before`. */
+/* Optional timing hooks: hipEvent_t handles (each may be NULL), created by the
+ * caller with timing enabled.  Each kernel of a call is launched with its pair
+ * attached (hipExtLaunchKernel start/stop events), so the events carry that
+ * kernel's own start and end time and add no marker work to the stream.  Pairs
+ * of kernels a call does not run are left untouched. */
 typedef struct {
-  void* before;          /* before the first kernel */
-  void* after_prefix;    /* after the prefix-group (MFMA) kernel */
-  void* after_splitkv;   /* after the split-KV (non-shared tokens) kernel */
-  void* after_merge;     /* after the log-sum-exp merge kernel */
+  void* prefix_start;    /* prefix-group (MFMA) kernel */
+  void* prefix_stop;
+  void* splitkv_start;   /* split-KV (non-shared tokens) kernel */
+  void* splitkv_stop;
+  void* merge_start;     /* log-sum-exp merge kernel */
+  void* merge_stop;
 } parrot_trace;
 
 /* Bytes of device workspace either decode entry point needs for `p`

@@ -52,10 +52,12 @@ class ParrotProblem(ctypes.Structure):
 
 class ParrotTrace(ctypes.Structure):
     _fields_ = [
-        ("before", ctypes.c_void_p),
-        ("after_prefix", ctypes.c_void_p),
-        ("after_splitkv", ctypes.c_void_p),
-        ("after_merge", ctypes.c_void_p),
+        ("prefix_start", ctypes.c_void_p),
+        ("prefix_stop", ctypes.c_void_p),
+        ("splitkv_start", ctypes.c_void_p),
+        ("splitkv_stop", ctypes.c_void_p),
+        ("merge_start", ctypes.c_void_p),
+        ("merge_stop", ctypes.c_void_p),
     ]
 
 
@@ -220,6 +222,23 @@ class Decoder:
         self.lse = torch.empty((R, H), dtype=torch.float32, device=self.device)
         nbytes = parrot_workspace_bytes(problem)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+
+    def bind(self, t: dict, shared: bool = True, stream=None):
+        """Marshal the arguments once; the returned callable re-issues the same
+        call (same tensors, stream and buffers) with only the optional trace."""
+        lib = load_library()
+        fn = getattr(lib, "parrot_shared_prefix_decode" if shared else "parrot_per_request_decode")
+        pk = t.get("prefix_k", t.get("k_pool")); pv = t.get("prefix_v", t.get("v_pool"))
+        sk = t.get("suffix_k", t.get("k_pool")); sv = t.get("suffix_v", t.get("v_pool"))
+        ws = self.workspace
+        args = (ctypes.byref(self.problem), _ptr(t["q"]), _ptr(pk), _ptr(pv), _ptr(sk), _ptr(sv),
+                _ptr(t["prefix_tables"]), _ptr(t["prefix_lens"]), _ptr(t["suffix_tables"]),
+                _ptr(t["suffix_lens"]), _ptr(t["group_ids"]), _ptr(self.out), _ptr(self.lse),
+                _ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream))
+
+        def call(trace: Optional[ParrotTrace] = None):
+            _check(fn(*args, ctypes.byref(trace) if trace is not None else None))
+        return call
 
     def __call__(self, t: dict, shared: bool = True, stream=None, trace=None):
         fn = parrot_shared_prefix_decode if shared else parrot_per_request_decode

@@ -49,13 +49,15 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False, extra_flags=()) -> str:
+def build(verbose: bool = False, extra_flags=(), out_path: str = LIB_PATH,
+          build_dir: str = BUILD) -> str:
+    """Compile every source and link ``out_path``; ``extra_flags`` go to hipcc."""
     hipcc = _hipcc()
-    os.makedirs(BUILD, exist_ok=True)
+    os.makedirs(build_dir, exist_ok=True)
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(build_dir, src.replace(".hip", ".o"))
         objs.append(obj)
         cmds.append([hipcc, *HIP_FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC, "-c",
                      os.path.join(CSRC, src), "-o", obj])
@@ -63,12 +65,12 @@ def build(verbose: bool = False, extra_flags=()) -> str:
         for out in ex.map(_run, cmds):
             if verbose and out:
                 print(out)
-    tmp = LIB_PATH + ".tmp"
+    tmp = out_path + ".tmp"
     _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, out_path)
     if verbose:
-        print(f"built {LIB_PATH}")
-    return LIB_PATH
+        print(f"built {out_path}")
+    return out_path
 
 
 if __name__ == "__main__":

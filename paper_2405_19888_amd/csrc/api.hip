@@ -1,9 +1,11 @@
 // C ABI of libparrot_attn: argument checks, work sizing and kernel launches.
 // Everything here runs on host scalars; no call reads device memory except
 // parrot_validate_inputs, which synchronises on purpose.
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <string>
 
 #include "parrot_attn.h"
@@ -30,8 +32,31 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 // Chunk sizes and slot counts.  Chunks are whole 16-token blocks.  The prefix
 // chunk bounds both the per-workgroup LDS pipeline depth and the number of
 // partials written per member; the non-shared chunk is one wavefront's work.
-constexpr int kPrefixChunk = 256;
-constexpr int kSuffixChunk = 128;
+#ifndef PARROT_PREFIX_CHUNK
+#define PARROT_PREFIX_CHUNK 256
+#endif
+#ifndef PARROT_SPLITKV_WAVES_PER_CU
+#define PARROT_SPLITKV_WAVES_PER_CU 8   // must match the split-KV kernel's setting
+#endif
+#ifndef PARROT_SPLITKV_MIN_BLOCKS
+#define PARROT_SPLITKV_MIN_BLOCKS 2
+#endif
+constexpr int kPrefixChunk = PARROT_PREFIX_CHUNK;
+constexpr int kSplitkvWavesPerCu = PARROT_SPLITKV_WAVES_PER_CU;
+constexpr int kSplitkvMinBlocks = PARROT_SPLITKV_MIN_BLOCKS;
+
+// Compute units of the current device (cached per device; no device sync).
+int num_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
 
 parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   if (!p) return fail(PARROT_ERR_INVALID_ARGUMENT, "problem is NULL");
@@ -65,36 +90,42 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   if (p->num_requests > 0 && p->num_groups == 0 && p->max_suffix_len == 0)
     return fail(PARROT_ERR_INVALID_ARGUMENT, "no request can have a non-empty context (no groups, max_suffix_len 0)");
 
+  if (p->num_requests > parrot::kMaxRequests)
+    return fail(PARROT_ERR_UNSUPPORTED, "num_requests %d > %d per call", p->num_requests, parrot::kMaxRequests);
   pl->cp = kPrefixChunk;
-  pl->cs = kSuffixChunk;
+  pl->skv_min_q = kSplitkvMinBlocks;
+  // slots: shared path = prefix chunks + split-KV pieces of the own tokens;
+  // per-request path = split-KV pieces of prefix + own tokens.  One stride
+  // serves both.
+  const long nbp_max = p->num_groups > 0 ? ceil_div(p->max_prefix_len, B) : 0;
+  const long nbs_max = ceil_div(p->max_suffix_len, B);
+  const long pieces_shared = nbs_max > 0 ? ceil_div(nbs_max, pl->skv_min_q) + 1 : 0;
+  const long pieces_naive = ceil_div(nbp_max + nbs_max, pl->skv_min_q) + 1;
   pl->seg_p = p->num_groups > 0 ? (int)ceil_div(p->max_prefix_len, pl->cp) : 0;
-  pl->seg_s = (int)ceil_div(p->max_suffix_len, pl->cs);
-  pl->seg = pl->seg_p + pl->seg_s;
+  pl->seg_s = (int)pieces_shared;
+  const long seg = std::max<long>(pl->seg_p + pieces_shared, pieces_naive);
+  pl->seg = (int)seg;
   const long mg = p->num_groups > 0 ? p->max_group_size : 1;
-  long waves = ceil_div(mg, 16);
-  waves = waves < 4 ? 4 : (waves > 8 ? 8 : waves);
+  const long waves = ceil_div(mg, 16) <= 4 ? 4 : 8;
   pl->prefix_waves = (int)waves;
   pl->prefix_qtiles = (int)ceil_div(mg, 16 * waves);
+  pl->skv_waves = 0;   // set at launch from the device's CU count
 
-  const double slots = (double)p->num_requests * p->num_heads * pl->seg;
-  const double grid_a = slots;                                               // split-KV waves
+  const double slots = (double)p->num_requests * p->num_heads * seg;
+  const double flat = (double)p->num_requests * (double)(nbp_max + nbs_max);
   const double grid_b = (double)p->num_groups * pl->seg_p * p->num_heads * pl->prefix_qtiles;
-  if (grid_a / 4 > 2e9 || grid_b > 2e9 || slots * p->head_dim * 4.0 > 9e18)
-    return fail(PARROT_ERR_UNSUPPORTED, "problem too large for one launch (%.3g work items)", grid_a);
-  const size_t n_slots = (size_t)p->num_requests * p->num_heads * pl->seg;
+  if (flat > 2e9 || grid_b > 2e9 || slots * p->head_dim * 4.0 > 9e18)
+    return fail(PARROT_ERR_UNSUPPORTED, "problem too large for one launch (%.3g blocks)", flat);
+  const size_t n_slots = (size_t)p->num_requests * p->num_heads * seg;
   auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
   pl->lse_bytes = align256(n_slots * sizeof(float));
-  pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes : 0;
+  pl->info_bytes = align256(((size_t)p->num_requests + 1) * sizeof(int32_t));
+  pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes + pl->info_bytes : 0;
   return PARROT_OK;
 }
 
-parrot_status record(void* ev, hipStream_t s) {
-  if (!ev) return PARROT_OK;
-  hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
-  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-  return PARROT_OK;
-}
+hipEvent_t ev(void* p) { return reinterpret_cast<hipEvent_t>(p); }
 
 parrot_status launched(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(PARROT_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
@@ -112,11 +143,9 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr};
+  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   const parrot_trace& tr = trace ? *trace : none;
   if (p->num_requests == 0) {
-    PARROT_TRY(record(tr.before, s)); PARROT_TRY(record(tr.after_prefix, s));
-    PARROT_TRY(record(tr.after_splitkv, s)); PARROT_TRY(record(tr.after_merge, s));
     g_err.clear();
     return PARROT_OK;
   }
@@ -142,10 +171,10 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
 
   float* o_part = reinterpret_cast<float*>(workspace);
   float* lse_part = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + pl.o_bytes);
+  int* seq_info = reinterpret_cast<int*>(reinterpret_cast<char*>(workspace) + pl.o_bytes + pl.lse_bytes);
   const float scale_log2 = p->sm_scale * parrot::kLog2e;
   const int D = p->head_dim, dt = (int)p->dtype;
 
-  PARROT_TRY(record(tr.before, s));
   if (shared && p->num_groups > 0 && pl.seg_p > 0) {
     parrot::PrefixArgs a{};
     a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.ptab = ptab; a.plen = plen; a.gid = gid;
@@ -154,35 +183,40 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.pstride = p->prefix_table_stride; a.max_p = p->max_prefix_len; a.npblk = p->num_prefix_blocks;
     a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.qtiles = pl.prefix_qtiles;
     a.scale_log2 = scale_log2;
-    PARROT_TRY(launched(parrot::launch_prefix(a, dt, D, pl.prefix_waves, s), "prefix-group kernel"));
+    PARROT_TRY(launched(parrot::launch_prefix(a, dt, D, pl.prefix_waves, s, ev(tr.prefix_start),
+                                              ev(tr.prefix_stop)), "prefix-group kernel"));
   }
-  PARROT_TRY(record(tr.after_prefix, s));
   {
     parrot::SplitKVArgs a{};
     a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
     a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
-    a.o_part = o_part; a.lse_part = lse_part;
+    a.o_part = o_part; a.lse_part = lse_part; a.seq_info = seq_info;
     a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
     a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
     a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
     a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
-    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.cs = pl.cs;
-    a.first_c = shared ? pl.seg_p : 0;
-    a.nc = shared ? pl.seg_s : pl.seg;
+    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0;
+    a.with_prefix = shared ? 0 : 1;
+    // one workgroup per CU; a multiple of H waves so every column group has all heads
+    a.nwaves = num_cus() * kSplitkvWavesPerCu;
+    if (a.nwaves < a.H) a.nwaves = (int)ceil_div(a.H, kSplitkvWavesPerCu) * kSplitkvWavesPerCu;
+    a.min_q = pl.skv_min_q;
     a.scale_log2 = scale_log2;
-    if (a.nc > 0) PARROT_TRY(launched(parrot::launch_splitkv(a, dt, D, s), "split-KV kernel"));
+    PARROT_TRY(launched(parrot::launch_splitkv(a, dt, D, s, ev(tr.splitkv_start), ev(tr.splitkv_stop)),
+                        "split-KV kernel"));
   }
-  PARROT_TRY(record(tr.after_splitkv, s));
   {
     parrot::MergeArgs a{};
-    a.o_part = o_part; a.lse_part = lse_part; a.plen = plen; a.slen = slen; a.gid = gid;
+    a.o_part = o_part; a.lse_part = lse_part; a.seq_info = seq_info;
+    a.plen = plen; a.slen = slen; a.gid = gid;
     a.out = out; a.lse = lse;
     a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
     a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
-    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.cs = pl.cs;
-    PARROT_TRY(launched(parrot::launch_merge(a, dt, D, s), "merge kernel"));
+    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0; a.cp = pl.cp;
+    a.with_prefix = shared ? 0 : 1;
+    PARROT_TRY(launched(parrot::launch_merge(a, dt, D, s, ev(tr.merge_start), ev(tr.merge_stop)),
+                        "merge kernel"));
   }
-  PARROT_TRY(record(tr.after_merge, s));
   g_err.clear();
   return PARROT_OK;
 }

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 namespace parrot {
@@ -14,18 +15,27 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Partial results live in the workspace as
-//   o_part  [R][H][seg][D] float32   (normalised partial output of one chunk)
-//   lse_part[R][H][seg]    float32   (base-2 log-sum-exp of the chunk's scaled logits)
-// Slots [0, seg_p) hold prefix chunks (chunk c covers prefix tokens
-// [c*cp, (c+1)*cp)), slots [seg_p, seg) hold the request's own tokens in chunks
-// of cs.  Both chunk sizes are multiples of kBlock.
+//   o_part  [R][H][seg][D] float32   (normalised partial output of one piece)
+//   lse_part[R][H][seg]    float32   (base-2 log-sum-exp of the piece's scaled logits)
+//   seq_info[R + 1]        int32     (split-KV: first flat block of each request,
+//                                     then the blocks-per-wave of the launch)
+// Slots [0, seg_p) hold the prefix-group kernel's chunks (chunk c covers prefix
+// tokens [c*cp, (c+1)*cp)); slots [seg_p, seg) hold split-KV pieces.  The
+// split-KV kernel sees every request's blocks (own tokens, preceded by its
+// group's prefix on the per-request path) as one flat list ordered by
+// (request, head, block) and gives each wave an equal run of it; piece p of
+// sequence (r, h) is the part that the p-th wave touching that sequence owns.
 struct Plan {
-  int cp, cs;            // chunk tokens, prefix / non-shared
+  int cp;                // prefix chunk tokens (prefix-group kernel)
   int seg_p, seg_s, seg; // slots per (request, head)
   int prefix_waves;      // waves per prefix-kernel workgroup (16 queries each)
   int prefix_qtiles;     // query tiles per group
-  size_t o_bytes, lse_bytes, total_bytes;
+  int skv_waves;         // split-KV grid, in waves
+  int skv_min_q;         // blocks per split-KV wave, lower bound
+  size_t o_bytes, lse_bytes, info_bytes, total_bytes;
 };
+
+constexpr int kMaxRequests = 1024;   // per call (split-KV keeps per-request data in LDS)
 
 struct SplitKVArgs {
   const void* q;
@@ -35,12 +45,15 @@ struct SplitKVArgs {
   const int* stab; const int* slen;
   const int* gid;
   float* o_part; float* lse_part;
+  int* seq_info;
   int R, H, NG;
   int pstride, sstride;
   int max_p, max_s;
   int npblk, nsblk;
-  int seg, seg_p, cp, cs;
-  int first_c, nc;       // this launch covers slots [first_c, first_c + nc)
+  int seg, seg_p;
+  int with_prefix;       // 1: each sequence is the group prefix, then the own tokens
+  int nwaves;            // waves launched
+  int min_q;             // blocks per wave >= min_q
   float scale_log2;      // sm_scale * log2(e)
 };
 
@@ -58,11 +71,13 @@ struct PrefixArgs {
 
 struct MergeArgs {
   const float* o_part; const float* lse_part;
+  const int* seq_info;
   const int* plen; const int* slen; const int* gid;
   void* out; float* lse;
   int R, H, NG;
   int max_p, max_s;
-  int seg, seg_p, cp, cs;
+  int seg, seg_p, cp;
+  int with_prefix;       // split-KV sequences include the group prefix (per-request path)
 };
 
 struct ValidateArgs {
@@ -75,9 +90,11 @@ struct ValidateArgs {
 // dtype codes follow parrot_dtype
 enum Dtype { kF32 = 0, kF16 = 1, kBF16 = 2 };
 
-hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s);
-hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s);
-hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s);
+// Each launcher attaches the optional (start, stop) timing events to its kernel.
+hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s, hipEvent_t e0,
+                         hipEvent_t e1);
+hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------ device helpers
@@ -120,6 +137,80 @@ PARROT_DEV float group_sum(float x) {
   if constexpr (N >= 32) x += __shfl_xor(x, 16);
   if constexpr (N >= 64) x += __shfl_xor(x, 32);
   return x;
+}
+
+// Workgroup barrier that orders LDS traffic only.  __syncthreads() is a
+// release/acquire fence on all address spaces, and on gfx9 loads and stores
+// share one counter, so it would wait for every global load still in flight
+// (register prefetches included).  Fencing only the local address space keeps
+// those loads in flight across the barrier.
+PARROT_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier for kernels that manage their own memory counters: this
+// wave's LDS operations complete (lgkmcnt 0), then s_barrier.  No hardware
+// fence and no wait on vector-memory loads, so direct-to-LDS loads issued
+// earlier stay in flight; the empty asm statements keep the compiler from
+// moving memory accesses across the barrier.
+PARROT_DEV void lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt untouched
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16-byte direct-to-LDS load (global_load_lds_dwordx4): lane l's 16 bytes
+// from `src` land at LDS byte address lds_base + 16 * l.  lds_base must be
+// wave-uniform.  Written as inline assembly so that the compiler does not
+// attach its own (conservative) waits for these loads: the caller owns the
+// vmcnt accounting, must have no other vector-memory loads outstanding where
+// it waits, and must drain its loads (wait_vmcnt<0>) before the wave ends.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // m0 is clobbered on purpose
+PARROT_DEV void lds_dma16(const void* src, unsigned lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off"
+      :
+      : "s"(lds_base), "v"(src)
+      : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+PARROT_DEV unsigned lds_addr(const void* p) {
+  return (unsigned)(size_t)((__attribute__((address_space(3))) const char*)p);
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14).
+template <int N>
+PARROT_DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// max(x[l], x[l ^ 16]) and max(x[l], x[l ^ 32]) with the gfx950 lane-swap
+// instructions (VALU, no trip through the LDS crossbar): the two outputs of a
+// self-swap hold x[l] and x[l ^ 16] (resp. x[l ^ 32]) in some order.
+PARROT_DEV float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+PARROT_DEV float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+PARROT_DEV float sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+PARROT_DEV float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 PARROT_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

@@ -20,11 +20,15 @@ PARROT_DEV float group_max(float x) {
   return x;
 }
 
-// One wave per (request, head); each lane owns D/64 output elements.
+// One wave per (request, head); each lane owns D/64 output elements.  Lane i
+// reads the log-sum-exp of slot i, so one round of loads gives every weight;
+// the weights are then broadcast with readlane while the partial outputs of
+// up to kUnroll slots are loaded together.
 template <int DT, int D>
 __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   using E = Elem<DT>;
   constexpr int EPL = D / kWave;
+  constexpr int kUnroll = 8;
   const int lane = threadIdx.x & 63;
   const long w = (long)blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (w >= (long)a.R * a.H) return;
@@ -33,8 +37,16 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   const int g = a.gid[r];
   const int P = (g >= 0 && g < a.NG) ? clampi(a.plen[g], 0, a.max_p) : 0;
   const int S = clampi(a.slen[r], 0, a.max_s);
-  const int np = (P + a.cp - 1) / a.cp;
-  const int ns = (S + a.cs - 1) / a.cs;
+  // prefix-group kernel chunks (shared path) occupy slots [0, np)
+  const int np = a.with_prefix ? 0 : (P + a.cp - 1) / a.cp;
+  // split-KV pieces: the waves whose runs cover this sequence
+  const int cnt = (a.with_prefix ? (P + kBlock - 1) / kBlock : 0) + (S + kBlock - 1) / kBlock;
+  int ns = 0;
+  if (cnt > 0) {
+    const int Q = a.seq_info[a.R];
+    const int first = a.seq_info[r];
+    ns = (first + cnt - 1) / Q - first / Q + 1;
+  }
   const int n = np + ns;
   const size_t base = (size_t)(r * a.H + h) * a.seg;
   char* outp = (char*)a.out + ((size_t)(r * a.H + h) * D + lane * EPL) * E::kBytes;
@@ -44,56 +56,59 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     if (lane == 0) a.lse[r * a.H + h] = -INFINITY;
     return;
   }
+  auto slot_of = [&](int i) { return i < np ? i : a.seg_p + (i - np); };
   float mx = -INFINITY;
-  for (int i = lane; i < n; i += kWave) {
-    const int slot = i < np ? i : a.seg_p + (i - np);
-    mx = fmaxf(mx, a.lse_part[base + slot]);
-  }
+  for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, a.lse_part[base + slot_of(i)]);
   mx = group_max<64>(mx);
   float tot = 0.f;
-  for (int i = lane; i < n; i += kWave) {
-    const int slot = i < np ? i : a.seg_p + (i - np);
-    tot += fast_exp2(a.lse_part[base + slot] - mx);
-  }
-  tot = group_sum<64>(tot);
-  const float inv = 1.f / tot;
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-  for (int i = 0; i < n; ++i) {
-    const int slot = i < np ? i : a.seg_p + (i - np);
-    const float wgt = fast_exp2(a.lse_part[base + slot] - mx) * inv;
-    const float* src = a.o_part + (base + slot) * D + lane * EPL;
-    if constexpr (EPL == 2) {
-      const float2 v = *reinterpret_cast<const float2*>(src);
-      acc[0] = __builtin_fmaf(wgt, v.x, acc[0]);
-      acc[1] = __builtin_fmaf(wgt, v.y, acc[1]);
-    } else {
+  for (int i0 = 0; i0 < n; i0 += kWave) {
+    const int cnt = min(kWave, n - i0);
+    const float wl = lane < cnt ? fast_exp2(a.lse_part[base + slot_of(i0 + lane)] - mx) : 0.f;
+    tot += group_sum<64>(wl);
+    for (int j0 = 0; j0 < cnt; j0 += kUnroll) {
+      float v[kUnroll][EPL];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wgt, src[e], acc[e]);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int j = min(j0 + u, cnt - 1);
+        const float* src = a.o_part + (base + slot_of(i0 + j)) * D + lane * EPL;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) v[u][e] = src[e];
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        if (j0 + u < cnt) {
+          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), j0 + u));
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wu, v[u][e], acc[e]);
+        }
+      }
     }
   }
+  const float inv = 1.f / tot;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) E::store1(outp + e * E::kBytes, acc[e]);
+  for (int e = 0; e < EPL; ++e) E::store1(outp + e * E::kBytes, acc[e] * inv);
   if (lane == 0) a.lse[r * a.H + h] = (mx + fast_log2(tot)) * kLn2;
 }
 
 template <int DT, int D>
-static hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
+static hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const long waves = (long)a.R * a.H;
   if (waves <= 0) return hipSuccess;
-  hipLaunchKernelGGL((k_merge<DT, D>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
+  hipExtLaunchKernelGGL((k_merge<DT, D>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 
-hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s) {
+hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (dtype * 1000 + D) {
-    case kF32 * 1000 + 64: return launch_merge_t<kF32, 64>(a, s);
-    case kF32 * 1000 + 128: return launch_merge_t<kF32, 128>(a, s);
-    case kF16 * 1000 + 64: return launch_merge_t<kF16, 64>(a, s);
-    case kF16 * 1000 + 128: return launch_merge_t<kF16, 128>(a, s);
-    case kBF16 * 1000 + 64: return launch_merge_t<kBF16, 64>(a, s);
-    case kBF16 * 1000 + 128: return launch_merge_t<kBF16, 128>(a, s);
+    case kF32 * 1000 + 64: return launch_merge_t<kF32, 64>(a, s, e0, e1);
+    case kF32 * 1000 + 128: return launch_merge_t<kF32, 128>(a, s, e0, e1);
+    case kF16 * 1000 + 64: return launch_merge_t<kF16, 64>(a, s, e0, e1);
+    case kF16 * 1000 + 128: return launch_merge_t<kF16, 128>(a, s, e0, e1);
+    case kBF16 * 1000 + 64: return launch_merge_t<kBF16, 64>(a, s, e0, e1);
+    case kBF16 * 1000 + 128: return launch_merge_t<kBF16, 128>(a, s, e0, e1);
   }
   return hipErrorInvalidValue;
 }

@@ -1,31 +1,47 @@
 // Prefix-group decode attention on MFMA (gfx950).
 //
 // One workgroup owns (group g, head h, prefix chunk c, query tile qt).  The
-// chunk's K and V blocks are staged through LDS in 16 KiB tiles per tensor,
-// double-buffered, so the shared prefix is read from HBM once per group
-// (Section 6, "Kernel Optimization": prefix KV tiles are loaded to on-chip
-// memory once and reused by every request of the group).  Each wave owns 16 of
-// the group's queries and computes, per 16-token block,
-//   S^T = K * Q^T   (16 tokens x 16 queries; v_mfma_f32_16x16x32_{f16,bf16})
-//   O^T += V^T * P^T (D x 16 queries; v_mfma_f32_16x16x16{f16,bf16_1k})
-// with an online softmax in fp32.  Computing the transposed products keeps
-// every per-query quantity (running max, sum, output rows) in the lanes that
-// own that query, so the softmax needs no lane shuffles besides the block max.
+// chunk's K and V blocks pass through LDS in 16 KiB stages (K and V together),
+// so the shared prefix is read from HBM once per group (Section 6, "Kernel
+// Optimization": prefix KV tiles are loaded to on-chip memory once and reused
+// by every request of the group).  Stages are fetched with direct-to-LDS loads
+// (global_load_lds_dwordx4) into a ring of three stage buffers, two stages
+// ahead of the one being computed; the wait for a stage is an explicit vmcnt,
+// so the loads need no registers and stay in flight across the barriers.
+//
+// Each wave owns 16 of the group's queries and computes, per 16-token block,
+//   S^T  = K Q^T    (16 tokens x 16 queries; v_mfma_f32_16x16x32_{f16,bf16})
+//   O^T += V^T P^T  (D x 16 queries; v_mfma_f32_16x16x16{f16,bf16_1k})
+// with an online softmax in fp32.  Computing the transposed products keeps the
+// per-query running max, sum and output rows in the lanes that own the query,
+// so only the block max crosses lanes (lane-swap instructions, no LDS trip).
 // V^T operands come straight from the row-major LDS tile through
 // ds_read_b64_tr_b16.  fp32 inputs use v_mfma_f32_16x16x4f32 with the same
-// tiling.  Each member's partial result (normalised output, base-2
-// log-sum-exp) is written to its own workspace slot.
+// tiling.
+//
+// LDS rows are swizzled: 16-byte granule j of token row t is stored at granule
+// j ^ f(t), f(t) = ((t & 3) << 1) | ((t >> 2) & 1).  Eight consecutive rows then
+// hit eight distinct granules (conflict-free 128-bit K reads by 16 lanes of
+// different tokens), and four consecutive rows hit four distinct granule pairs
+// (conflict-free transposed V reads).  The swizzle is applied on the global
+// side: each lane of a direct-to-LDS load fetches the granule that belongs at
+// its fixed LDS slot.
 #include "common.h"
 
 namespace parrot {
 
 namespace {
 
-constexpr int kTileBytes = 16384;   // per tensor per stage
+constexpr int kTensorStage = 8192;   // bytes of K (and of V) per stage
+constexpr int kStageBytes = 2 * kTensorStage;
+constexpr int kStageChunks = kStageBytes / 1024;  // 1 KiB per direct-to-LDS instruction
+constexpr int kRing = 4;             // stage buffers in LDS (kRing - 1 stages in flight)
+constexpr int kMaxChunkBlocks = 64;  // prefix chunk <= 1024 tokens
+
 
 typedef __attribute__((address_space(3))) char lds_char;
 
-PARROT_DEV u32x4 lds_ld16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+PARROT_DEV int swz(int t) { return ((t & 3) << 1) | ((t >> 2) & 1); }
 
 template <int DT> struct Mfma;
 
@@ -38,7 +54,6 @@ template <> struct Mfma<kF16> {
     return __builtin_bit_cast(unsigned long long, h);
   }
   PARROT_DEV static unsigned long long tr_read(const char* lds_ptr) {
-    typedef __attribute__((address_space(3))) f16x4 lds_v4;
     typedef __fp16 fp16x4_ __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(3))) fp16x4_ lds_fp16x4;
     fp16x4_ v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_fp16x4*)(lds_char*)lds_ptr);
@@ -46,6 +61,13 @@ template <> struct Mfma<kF16> {
   }
   PARROT_DEV static f32x4 pv(unsigned long long a, unsigned long long b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b), c, 0, 0, 0);
+  }
+  // k = 32 over two blocks: operand halves (lo, hi) hold block A and block B
+  PARROT_DEV static f32x4 pv2(unsigned long long alo, unsigned long long ahi, unsigned long long blo,
+                               unsigned long long bhi, f32x4 c) {
+    const u32x4 a = {(unsigned)alo, (unsigned)(alo >> 32), (unsigned)ahi, (unsigned)(ahi >> 32)};
+    const u32x4 b = {(unsigned)blo, (unsigned)(blo >> 32), (unsigned)bhi, (unsigned)(bhi >> 32)};
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
   }
 };
 
@@ -65,27 +87,34 @@ template <> struct Mfma<kBF16> {
   PARROT_DEV static f32x4 pv(unsigned long long a, unsigned long long b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a), __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
   }
+  PARROT_DEV static f32x4 pv2(unsigned long long alo, unsigned long long ahi, unsigned long long blo,
+                               unsigned long long bhi, f32x4 c) {
+    const u32x4 a = {(unsigned)alo, (unsigned)(alo >> 32), (unsigned)ahi, (unsigned)(ahi >> 32)};
+    const u32x4 b = {(unsigned)blo, (unsigned)(blo >> 32), (unsigned)bhi, (unsigned)(bhi >> 32)};
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
 };
 
 }  // namespace
 
-template <int DT, int D>
-__global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
+template <int DT, int D, int W>
+__global__ __launch_bounds__(W * 64) void k_prefix(PrefixArgs a) {
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;
+  constexpr int GRAN = ROW_B / 16;                    // 16-byte granules per row
   constexpr int BLK_B = kBlock * ROW_B;               // one block of one head
-  constexpr int TILE_BLK = kTileBytes / BLK_B;        // blocks per stage
-  constexpr int CHUNKS = 2 * kTileBytes / 16;         // 16-byte pieces per stage (K and V)
-  constexpr int MAX_PER_THREAD = CHUNKS / 256;        // workgroups have >= 4 waves
+  constexpr int STAGE_BLK = kTensorStage / BLK_B;     // blocks per stage
   constexpr int DT16 = D / 16;                        // 16-wide d tiles
-  static_assert(TILE_BLK >= 1, "tile holds a block");
+  constexpr int KS = (DT == kF32) ? D / 4 : D / 32;   // MFMA k-steps over D
+  constexpr int PER_WAVE = kStageChunks / W;          // direct-to-LDS loads per wave per stage
+  static_assert(STAGE_BLK >= 1 && GRAN >= 8, "stage holds a block; swizzle fits a row");
+  static_assert(kStageChunks % W == 0, "stage chunks split evenly over waves");
 
-  __shared__ __attribute__((aligned(16))) char smem[2][2][kTileBytes];
-  __shared__ int members[128];
+  __shared__ __attribute__((aligned(1024))) char smem[kRing][kStageBytes];
+  __shared__ int members[W * 16];
+  __shared__ int s_tbl[kMaxChunkBlocks];
   __shared__ int s_count;
 
-  const int nthreads = blockDim.x;
-  const int nwaves = nthreads >> 6;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -101,9 +130,13 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
   const int t0 = c * a.cp;
   if (t0 >= P) return;
   const int t1 = min(P, t0 + a.cp);
-  const int qbase = qt * nwaves * 16;
+  const int qbase = qt * W * 16;
+  const int b0 = t0 / kBlock;
+  const int nb = (t1 - t0 + kBlock - 1) / kBlock;     // <= cp / 16 <= kMaxChunkBlocks
+  const int* tbl = a.ptab + (long)g * a.pstride;
 
-  // members of group g, in request order; this tile takes [qbase, qbase + 16*nwaves)
+  // members of group g in request order (this tile takes [qbase, qbase + 16 W));
+  // the chunk's block ids, clamped into the pool
   if (wave == 0) {
     int count = 0;
     for (int base = 0; base < a.R; base += kWave) {
@@ -111,13 +144,15 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
       const bool is = r < a.R && a.gid[r] == g;
       const unsigned long long mask = __ballot(is);
       const int pos = count + __popcll(mask & ((1ull << lane) - 1ull));
-      if (is && pos >= qbase && pos < qbase + nwaves * 16) members[pos - qbase] = r;
+      if (is && pos >= qbase && pos < qbase + W * 16) members[pos - qbase] = r;
       count += __popcll(mask);
     }
     if (lane == 0) s_count = count;
+  } else if (wave == 1) {
+    for (int i = lane; i < nb; i += kWave) s_tbl[i] = clampi(tbl[b0 + i], 0, a.npblk - 1);
   }
   __syncthreads();
-  const int nq = min(s_count - qbase, nwaves * 16);
+  const int nq = min(s_count - qbase, W * 16);
   if (nq <= 0) return;                                 // uniform over the workgroup
 
   const int qi = wave * 16 + (lane & 15);              // this lane's query column
@@ -126,7 +161,6 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
   const int rq = q_ok ? members[qi] : 0;
 
   // query operand (B of S^T = K Q^T): lane holds query lane%16, k-slice lane/16
-  constexpr int KS = (DT == kF32) ? D / 4 : D / 32;   // MFMA k-steps over D
   u32x4 qf16[(DT == kF32) ? 1 : KS];
   float qf32[(DT == kF32) ? KS : 1];
   {
@@ -141,48 +175,33 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
         qf16[ks] = q_ok ? ld16(qrow + (32 * ks + 8 * (lane >> 4)) * 2) : u32x4{0u, 0u, 0u, 0u};
     }
   }
-
-  const int b0 = t0 / kBlock;
-  const int nb = (t1 - t0 + kBlock - 1) / kBlock;
-  const int nstages = (nb + TILE_BLK - 1) / TILE_BLK;
-  const int* tbl = a.ptab + (long)g * a.pstride;
+  // Direct-to-LDS stage loads.  Wave w issues chunks w, w + W, ... of each
+  // stage; lane l of a chunk writes LDS bytes [16 l, 16 l + 16) of that chunk,
+  // i.e. block bl, token row t, granule slot pos, and fetches the global
+  // granule pos ^ f(t) of that row.
   const size_t blk_stride = (size_t)H * BLK_B;
-  const size_t head_off = (size_t)h * BLK_B;
-  const char* kpool = (const char*)a.pk;
-  const char* vpool = (const char*)a.pv;
-
-  // cooperative stage load: piece e in [0, CHUNKS): tensor e / (CHUNKS/2),
-  // block (e % (CHUNKS/2)) / (BLK_B/16), 16-byte offset inside that block
-  u32x4 stage_regs[MAX_PER_THREAD];
-  auto load_stage = [&](int st) {
+  const char* pool_k = (const char*)a.pk + (size_t)h * BLK_B;
+  const char* pool_v = (const char*)a.pv + (size_t)h * BLK_B;
+  int c_bl[PER_WAVE], c_src[PER_WAVE];
+  bool c_v[PER_WAVE];
 #pragma unroll
-    for (int j = 0; j < MAX_PER_THREAD; ++j) {
-      const int e = tid + j * nthreads;
-      stage_regs[j] = u32x4{0u, 0u, 0u, 0u};
-      if (e < CHUNKS) {
-        const int tensor = e / (CHUNKS / 2);
-        const int w = e % (CHUNKS / 2);
-        const int bl = w / (BLK_B / 16);
-        const int off = w % (BLK_B / 16);
-        const int b = st * TILE_BLK + bl;              // block index within the chunk
-        const int tok = (b0 + b) * kBlock + (off * 16) / ROW_B;
-        if (b < nb && tok < t1) {
-          const int blk = clampi(tbl[b0 + b], 0, a.npblk - 1);
-          const char* src = (tensor ? vpool : kpool) + blk * blk_stride + head_off + off * 16;
-          stage_regs[j] = ld16(src);
-        }
-      }
-    }
-  };
-  auto store_stage = [&](int buf) {
+  for (int j = 0; j < PER_WAVE; ++j) {
+    const int q = wave + j * W;                        // chunk index in the stage
+    const int off = (q % (kStageChunks / 2)) * 1024 + lane * 16;   // byte in the tensor stage
+    c_v[j] = q >= kStageChunks / 2;
+    c_bl[j] = off / BLK_B;
+    const int t = (off % BLK_B) / ROW_B;
+    const int pos = (off % ROW_B) / 16;
+    c_src[j] = t * ROW_B + ((pos ^ swz(t)) << 4);
+  }
+  const int nstages = (nb + STAGE_BLK - 1) / STAGE_BLK;
+  const int last = nstages - 1;
+  auto issue = [&](int st, int buf) {
 #pragma unroll
-    for (int j = 0; j < MAX_PER_THREAD; ++j) {
-      const int e = tid + j * nthreads;
-      if (e < CHUNKS) {
-        const int tensor = e / (CHUNKS / 2);
-        const int w = e % (CHUNKS / 2);
-        *reinterpret_cast<u32x4*>(&smem[buf][tensor][w * 16]) = stage_regs[j];
-      }
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const int b = min(st * STAGE_BLK + c_bl[j], nb - 1);   // past the chunk: re-read, unused
+      const char* src = (c_v[j] ? pool_v : pool_k) + (size_t)s_tbl[b] * blk_stride + c_src[j];
+      lds_dma16(src, lds_addr(&smem[buf][(wave + j * W) * 1024]));
     }
   };
 
@@ -191,73 +210,161 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
 #pragma unroll
   for (int i = 0; i < DT16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-  for (int st = 0; st < nstages; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nstages) load_stage(st + 1);
-    if (has_q) {
-      const char* ktile = smem[buf][0];
-      const char* vtile = smem[buf][1];
-      const int nbl = min(TILE_BLK, nb - st * TILE_BLK);
-      for (int bl = 0; bl < nbl; ++bl) {
-        const char* kb = ktile + bl * BLK_B;
-        const char* vb = vtile + bl * BLK_B;
-        // S^T[token 4*(lane/16)+i][query lane%16]
-        f32x4 s4 = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (DT == kF32) {
-          const float* kf = reinterpret_cast<const float*>(kb + (lane & 15) * ROW_B);
+  // lane-constant parts of the LDS read addresses
+  const int kt_row = lane & 15;                               // K: token row of this lane
+  const int vt_row = 4 * (lane >> 4) + ((lane & 15) >> 2);    // V^T: token row (16-bit types)
+  const int vt_half = 8 * (lane & 1);
+  const int vt_pair = (lane & 3) >> 1;
+
+  // S^T of one block into s4 (16 tokens x 16 queries)
+  auto scores = [&](const char* kb) {
+    f32x4 s4 = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (DT == kF32) {
+      const char* krow = kb + kt_row * ROW_B + 4 * (lane >> 4);
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            s4 = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[4 * ks + (lane >> 4)], qf32[ks], s4, 0, 0, 0);
-        } else {
+      for (int ks = 0; ks < KS; ++ks) {
+        const float kv = *reinterpret_cast<const float*>(krow + ((ks ^ swz(kt_row)) << 4));
+        s4 = __builtin_amdgcn_mfma_f32_16x16x4f32(kv, qf32[ks], s4, 0, 0, 0);
+      }
+    } else {
+      const char* krow = kb + kt_row * ROW_B;
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            s4 = Mfma<DT>::qk(lds_ld16(kb + (lane & 15) * ROW_B + (32 * ks + 8 * (lane >> 4)) * 2), qf16[ks], s4);
-        }
-        const int tok_base = (b0 + st * TILE_BLK + bl) * kBlock + 4 * (lane >> 4);
-        float s[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s[i] = (tok_base + i < t1) ? s4[i] * a.scale_log2 : -INFINITY;
-        float bm = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-        bm = fmaxf(bm, __shfl_xor(bm, 16));
-        bm = fmaxf(bm, __shfl_xor(bm, 32));
-        const float mn = fmaxf(m, bm);                 // finite: the block has a token
-        const float alpha = fast_exp2(m - mn);
-        float p[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s[i] - mn);
-        lsum = lsum * alpha + (p[0] + p[1]) + (p[2] + p[3]);
-#pragma unroll
-        for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
-        if constexpr (DT == kF32) {
-          // O^T[d][q] += V^T[d][t] P^T[t][q] with k index kk <-> token 4*kk + kt
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt) {
-            const float* vrow = reinterpret_cast<const float*>(vb + (4 * (lane >> 4) + kt) * ROW_B);
-#pragma unroll
-            for (int dt = 0; dt < DT16; ++dt)
-              o[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vrow[dt * 16 + (lane & 15)], p[kt], o[dt], 0, 0, 0);
-          }
-        } else {
-          const unsigned long long pb = Mfma<DT>::pack_p(p);
-          // lane k of 16-lane group G reads V[4G + k/4][dt*16 + 4*(k%4) .. +3]
-          const char* vsrc = vb + (4 * (lane >> 4) + ((lane & 15) >> 2)) * ROW_B + 4 * (lane & 3) * 2;
-#pragma unroll
-          for (int dt = 0; dt < DT16; ++dt)
-            o[dt] = Mfma<DT>::pv(Mfma<DT>::tr_read(vsrc + dt * 32), pb, o[dt]);
-        }
-        m = mn;
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz(kt_row)) << 4));
+        s4 = Mfma<DT>::qk(kv, qf16[ks], s4);
       }
     }
-    if (st + 1 < nstages) store_stage(buf ^ 1);
-    __syncthreads();
+    return s4;
+  };
+  // masked, scaled logits of the lane's 4 tokens of block `blk` (chunk-relative)
+  auto logits = [&](const f32x4& s4, int blk, float* s) {
+    const int tok_base = (b0 + blk) * kBlock + 4 * (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s[i] = (tok_base + i < t1) ? s4[i] * a.scale_log2 : -INFINITY;
+  };
+  // online-softmax update with n logits per lane; returns the probabilities
+  auto update = [&](float* s, float* p, int n) {
+    float bm = s[0];
+    for (int i = 1; i < n; ++i) bm = fmaxf(bm, s[i]);
+    bm = max_xor32(max_xor16(bm));
+    const float mn = fmaxf(m, bm);                   // finite: every block has a token
+    const float alpha = fast_exp2(m - mn);
+    float ps = 0.f;
+    for (int i = 0; i < n; ++i) { p[i] = fast_exp2(s[i] - mn); ps += p[i]; }
+    lsum = lsum * alpha + ps;
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
+    m = mn;
+  };
+
+  auto compute = [&](int st, int buf) {
+    const int nbl = min(STAGE_BLK, nb - st * STAGE_BLK);
+    int bl = 0;
+    if constexpr (DT != kF32) {
+      // two blocks per softmax update and per k = 32 PV product
+      for (; bl + 1 < nbl; bl += 2) {
+        const char* kbA = &smem[buf][bl * BLK_B];
+        const char* vbA = &smem[buf][kTensorStage + bl * BLK_B];
+        const f32x4 sA = scores(kbA);
+        const f32x4 sB = scores(kbA + BLK_B);
+        float s[8], p[8];
+        logits(sA, st * STAGE_BLK + bl, s);
+        logits(sB, st * STAGE_BLK + bl + 1, s + 4);
+        {
+          float bm = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
+          bm = max_xor32(max_xor16(bm));
+          const float mn = fmaxf(m, bm);
+          const float alpha = fast_exp2(m - mn);
+          float ps = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) { p[i] = fast_exp2(s[i] - mn); ps += p[i]; }
+          lsum = lsum * alpha + ps;
+#pragma unroll
+          for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
+          m = mn;
+        }
+        const unsigned long long pA = Mfma<DT>::pack_p(p), pB = Mfma<DT>::pack_p(p + 4);
+        const char* vrowA = vbA + vt_row * ROW_B + vt_half;
+#pragma unroll
+        for (int dt = 0; dt < DT16; ++dt) {
+          const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+          o[dt] = Mfma<DT>::pv2(Mfma<DT>::tr_read(vrowA + off), Mfma<DT>::tr_read(vrowA + BLK_B + off),
+                                pA, pB, o[dt]);
+        }
+      }
+    }
+    for (; bl < nbl; ++bl) {
+      const char* kb = &smem[buf][bl * BLK_B];
+      const char* vb = &smem[buf][kTensorStage + bl * BLK_B];
+      float s[4], p[4];
+      logits(scores(kb), st * STAGE_BLK + bl, s);
+      update(s, p, 4);
+      if constexpr (DT == kF32) {
+        // O^T[d][q] += V^T[d][t] P^T[t][q] with k index kk <-> token 4*kk + kt
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          const int row = 4 * (lane >> 4) + kt;
+          const char* vrow = vb + row * ROW_B + 4 * (lane & 3);
+#pragma unroll
+          for (int dt = 0; dt < DT16; ++dt) {
+            const float vv = *reinterpret_cast<const float*>(vrow + (((4 * dt + ((lane & 15) >> 2)) ^ swz(row)) << 4));
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv, p[kt], o[dt], 0, 0, 0);
+          }
+        }
+      } else {
+        const unsigned long long pb = Mfma<DT>::pack_p(p);
+        // lane k of 16-lane group G reads V[4G + k/4][dt*16 + 4*(k%4) .. +3]
+        const char* vrow = vb + vt_row * ROW_B + vt_half;
+#pragma unroll
+        for (int dt = 0; dt < DT16; ++dt)
+          o[dt] = Mfma<DT>::pv(Mfma<DT>::tr_read(vrow + (((2 * dt + vt_pair) ^ swz(vt_row)) << 4)), pb, o[dt]);
+      }
+    }
+  };
+
+  // Ring of kRing stage buffers, kRing - 1 stages in flight while one is
+  // computed.  At iteration st the wave's loads for st are the oldest outstanding ones,
+  // so vmcnt((kRing - 2) * PER_WAVE) means st has landed; the barrier then
+  // makes every wave's part visible and guarantees every wave is done with
+  // buffer (st - 1) % kRing, which stage st + kRing - 1 overwrites.
+#pragma unroll
+  for (int i = 0; i < kRing - 1; ++i) issue(min(i, last), i);
+  // The compiler tracks the query loads but not the direct-to-LDS loads; make
+  // it wait for the queries here, once, instead of at their first use inside
+  // the loop (where its wait would also drain the stage ring every iteration).
+  // This wait covers the prologue stages too: one round trip for both.
+  if constexpr (DT == kF32) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : : "v"(qf32[ks]));
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : : "v"(qf16[ks]));
   }
+  wait_vmcnt<0>();
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st % kRing;
+    wait_vmcnt<(kRing - 2) * PER_WAVE>();
+    lds_sync();
+    if (st == last && (t1 & (kBlock - 1)) != 0) {
+      // zero the V rows past the end of the chunk's last, partly filled block
+      // (their probabilities are 0, but 0 * NaN would poison the product)
+      const int bl = (nb - 1) - st * STAGE_BLK;
+      const int first = t1 & (kBlock - 1);
+      char* vb = &smem[buf][kTensorStage + bl * BLK_B];
+      for (int i = tid; i < (kBlock - first) * GRAN; i += W * 64) {
+        const int t = first + i / GRAN;
+        *reinterpret_cast<u32x4*>(vb + t * ROW_B + ((i % GRAN) << 4)) = u32x4{0u, 0u, 0u, 0u};
+      }
+      lds_sync();
+    }
+    issue(min(st + kRing - 1, last), (st + kRing - 1) % kRing);
+    if (has_q) compute(st, buf);
+  }
+  wait_vmcnt<0>();   // the re-read stages issued by the last iterations
 
   if (!has_q) return;
-  float lt = lsum + __shfl_xor(lsum, 16);
-  lt += __shfl_xor(lt, 32);
+  float lt = sum_xor16(lsum);
+  lt = sum_xor32(lt);
   if (q_ok) {
     const size_t slot = (size_t)(rq * H + h) * a.seg + c;
     const float inv = 1.f / lt;
@@ -269,22 +376,28 @@ __global__ __launch_bounds__(512) void k_prefix(PrefixArgs a) {
 }
 
 template <int DT, int D>
-static hipError_t launch_prefix_t(const PrefixArgs& a, int waves, hipStream_t s) {
+static hipError_t launch_prefix_t(const PrefixArgs& a, int waves, hipStream_t s, hipEvent_t e0,
+                                  hipEvent_t e1) {
   const long blocks = (long)a.NG * a.seg_p * a.H * a.qtiles;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL((k_prefix<DT, D>), dim3((unsigned)blocks), dim3(64 * waves), 0, s, a);
+  if (waves == 4)
+    hipExtLaunchKernelGGL((k_prefix<DT, D, 4>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  else
+    hipExtLaunchKernelGGL((k_prefix<DT, D, 8>), dim3((unsigned)blocks), dim3(512), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 
-hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s) {
-  if (waves < 4 || waves > 8) return hipErrorInvalidValue;
+hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s,
+                         hipEvent_t e0, hipEvent_t e1) {
+  if ((waves != 4 && waves != 8) || a.cp > kMaxChunkBlocks * kBlock || a.cp % 32 != 0)
+    return hipErrorInvalidValue;
   switch (dtype * 1000 + D) {
-    case kF32 * 1000 + 64: return launch_prefix_t<kF32, 64>(a, waves, s);
-    case kF32 * 1000 + 128: return launch_prefix_t<kF32, 128>(a, waves, s);
-    case kF16 * 1000 + 64: return launch_prefix_t<kF16, 64>(a, waves, s);
-    case kF16 * 1000 + 128: return launch_prefix_t<kF16, 128>(a, waves, s);
-    case kBF16 * 1000 + 64: return launch_prefix_t<kBF16, 64>(a, waves, s);
-    case kBF16 * 1000 + 128: return launch_prefix_t<kBF16, 128>(a, waves, s);
+    case kF32 * 1000 + 64: return launch_prefix_t<kF32, 64>(a, waves, s, e0, e1);
+    case kF32 * 1000 + 128: return launch_prefix_t<kF32, 128>(a, waves, s, e0, e1);
+    case kF16 * 1000 + 64: return launch_prefix_t<kF16, 64>(a, waves, s, e0, e1);
+    case kF16 * 1000 + 128: return launch_prefix_t<kF16, 128>(a, waves, s, e0, e1);
+    case kBF16 * 1000 + 64: return launch_prefix_t<kBF16, 64>(a, waves, s, e0, e1);
+    case kBF16 * 1000 + 128: return launch_prefix_t<kBF16, 128>(a, waves, s, e0, e1);
   }
   return hipErrorInvalidValue;
 }

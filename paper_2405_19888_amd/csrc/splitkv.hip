@@ -1,98 +1,203 @@
-// Split-KV decode attention over paged K/V (the non-shared tokens of each
-// request; with the prefix slots enabled it is also the per-request baseline).
+// Split-KV decode attention over paged K/V: the non-shared tokens of every
+// request (and, on the per-request path, its group's prefix as well).
 //
-// One wavefront owns one work item (request r, head h, chunk c).  A chunk is a
-// run of whole 16-token blocks.  A token row is D*elt bytes, read as
-// D*elt/16 lanes x 16 bytes, so every load instruction of the wave covers a
-// contiguous 1 KiB of the block (fully coalesced 128-bit loads).  Each group
-// of lanes that shares a token computes its slice of q.k, the slices are summed
-// with DPP row operations, and every token group keeps its own online-softmax
-// state; the groups are combined once at the end of the chunk.  The chunk's
-// normalised output and its base-2 log-sum-exp go to the workspace.
+// Work layout.  Each request owns a row of 16-token block columns (its own
+// tokens; on the per-request path its group's prefix blocks first).  The rows
+// are laid end to end into one flat column list, which is cut into equal runs
+// of Q columns ("column groups").  Wave (g, h) reduces head h over column
+// group g, so every wave streams the same number of bytes, and the H waves of
+// a group walk the same physical blocks at the same time, reading all heads
+// of a 16-token block (one contiguous H*4 KiB region per tensor) together.
+// One workgroup of 16 waves runs per CU, so the per-CU load is even too.  A run
+// may cross request boundaries: the wave then emits one partial result
+// (normalised output and base-2 log-sum-exp) per (request, head) piece.
+//
+// Per block, a token row is D*elt bytes read as D*elt/16 lanes x 16 bytes, so
+// each load instruction covers a contiguous 1 KiB of the block (coalesced
+// 128-bit loads).  Each group of lanes that shares a token computes its slice
+// of q.k, the slices are summed with DPP row operations, and every token group
+// keeps its own online-softmax state; the groups are combined at the end of a
+// piece.  One block is reduced while the next one's loads are in flight; the
+// loop is unrolled by two with ping-pong registers and every load inside it is
+// unconditional, so the compiler's memory-wait counts stay exact.
 #include "common.h"
 
 namespace parrot {
 
+// Waves per workgroup = per CU (one workgroup per CU); the register budget is
+// capped so that they are all resident at once (4 SIMDs per CU).
+#ifndef PARROT_SPLITKV_WAVES_PER_CU
+#define PARROT_SPLITKV_WAVES_PER_CU 8
+#endif
+constexpr int kSkvWaves = PARROT_SPLITKV_WAVES_PER_CU;
+
 template <int DT, int D>
-__global__ __launch_bounds__(256) void k_splitkv(SplitKVArgs a) {
+__global__ __launch_bounds__(kSkvWaves * 64) __attribute__((amdgpu_waves_per_eu(kSkvWaves / 4)))
+void k_splitkv(SplitKVArgs a) {
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;        // bytes per token row
   constexpr int LPT = ROW_B / 16;             // lanes per token
   constexpr int TPI = kWave / LPT;            // tokens per load instruction
   constexpr int IPB = kBlock / TPI;           // load instructions per block
   constexpr int EPL = E::kPerLoad;            // elements per lane load
+  constexpr int BLK_B = kBlock * ROW_B;
   static_assert(TPI * ROW_B == 1024, "one instruction covers 1 KiB");
 
-  const int lane = threadIdx.x & 63;
-  const long wave = (long)blockIdx.x * (blockDim.x >> 6) +
-                    __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int H = a.H;
-  if (wave >= (long)a.R * a.nc * H) return;
-  const int h = (int)(wave % H);
-  const long rest = wave / H;
-  const int c = a.first_c + (int)(rest % a.nc);
-  const int r = (int)(rest / a.nc);
+  // per-request data: first flat block per head-sequence, blocks per
+  // sequence, leading prefix blocks, group, prefix and own token counts
+  __shared__ int s_excl[kMaxRequests], s_cnt[kMaxRequests], s_nbp[kMaxRequests];
+  __shared__ int s_g[kMaxRequests], s_plen[kMaxRequests], s_slen[kMaxRequests];
+  __shared__ int s_total;
 
-  // resolve the chunk to a token range of one paged sequence
-  int t0, t1, nblk;
-  const int* tbl;
-  const char* kpool;
-  const char* vpool;
-  if (c < a.seg_p) {
-    const int g = a.gid[r];
-    if (g < 0 || g >= a.NG) return;
-    const int P = clampi(a.plen[g], 0, a.max_p);
-    t0 = c * a.cp;
-    if (t0 >= P) return;
-    t1 = min(P, t0 + a.cp);
-    tbl = a.ptab + (long)g * a.pstride;
-    kpool = (const char*)a.pk; vpool = (const char*)a.pv; nblk = a.npblk;
-  } else {
-    const int S = clampi(a.slen[r], 0, a.max_s);
-    t0 = (c - a.seg_p) * a.cs;
-    if (t0 >= S) return;
-    t1 = min(S, t0 + a.cs);
-    tbl = a.stab + (long)r * a.sstride;
-    kpool = (const char*)a.sk; vpool = (const char*)a.sv; nblk = a.nsblk;
+  const int lane = threadIdx.x & 63;
+  const int wave_in_wg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int R = a.R, H = a.H;
+
+  if (wave_in_wg == 0) {
+    int carry = 0;
+    for (int base = 0; base < R; base += kWave) {
+      const int r = base + lane;
+      const bool valid = r < R;
+      const int S = valid ? clampi(a.slen[r], 0, a.max_s) : 0;
+      int g = -1, P = 0;
+      if (a.with_prefix && valid) {
+        g = a.gid[r];
+        g = (g >= 0 && g < a.NG) ? g : -1;
+        P = g >= 0 ? clampi(a.plen[g], 0, a.max_p) : 0;
+      }
+      const int nbp = (P + kBlock - 1) / kBlock;
+      const int cnt = nbp + (S + kBlock - 1) / kBlock;
+      int incl = cnt;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int t = __shfl_up(incl, off);
+        if (lane >= off) incl += t;
+      }
+      if (valid) {
+        s_excl[r] = carry + incl - cnt; s_cnt[r] = cnt; s_nbp[r] = nbp;
+        s_g[r] = g; s_plen[r] = P; s_slen[r] = S;
+      }
+      carry += __shfl(incl, kWave - 1);
+    }
+    if (lane == 0) s_total = carry;
   }
+  __syncthreads();
+  const int C = s_total;                                      // flat block columns
+  const int G = a.nwaves / H;                                 // column groups
+  const int Qg = (C + G - 1) / G;
+  const int Q = Qg > a.min_q ? Qg : a.min_q;                  // columns per group
+  if (blockIdx.x == 0) {                                      // for the merge
+    for (int r = threadIdx.x; r < R; r += blockDim.x) a.seq_info[r] = s_excl[r];
+    if (threadIdx.x == 0) a.seq_info[R] = Q;
+  }
+  const int w = blockIdx.x * kSkvWaves + wave_in_wg;
+  const int grp = w / H;
+  int h = w % H;
+  const int c0 = grp * Q;
+  if (grp >= G || c0 >= C) return;
+  const int nblk_run = (C - c0 < Q) ? (C - c0) : Q;
+
+  // the request holding column c0: the last request whose first column is <= c0
+  int r = 0;
+  for (int base = 0; base < R; base += kWave) {
+    const int rr = base + lane;
+    const unsigned long long mask = __ballot(rr < R && s_excl[rr] <= c0);
+    const int n = __popcll(mask);
+    if (n > 0) r = base + n - 1;
+    if (n < kWave) break;
+  }
+  int cnt = s_cnt[r];
+  if (cnt <= 0) return;                       // unreachable for consistent data
+  int b = c0 - s_excl[r];
 
   const int sub = lane % LPT;                 // which 16-byte slice of the row
   const int tg = lane / LPT;                  // token group
-  const u32x4 qf = ld16((const char*)a.q + ((size_t)(r * H + h) * D + sub * EPL) * E::kBytes);
-  const size_t blk_stride = (size_t)H * kBlock * ROW_B;
-  const size_t head_off = (size_t)h * kBlock * ROW_B + (size_t)lane * 16;
+  const size_t blk_stride = (size_t)H * BLK_B;
+
+  // One fetched block: K and V slices, the matching query slice, and the
+  // metadata needed to reduce it and to close its piece.
+  struct Blk {
+    u32x4 k[IPB], v[IPB], q;
+    int ntok;      // valid tokens in the block
+    int seq;       // r * H + h
+    int piece_end; // last block of its sequence
+  };
+  auto fetch = [&](Blk& B) {
+    const int nbp = s_nbp[r];
+    const char* kp;
+    const char* vp;
+    int entry, nblk, ntok;
+    if (b < nbp) {
+      entry = a.ptab[(long)s_g[r] * a.pstride + b];
+      kp = (const char*)a.pk; vp = (const char*)a.pv; nblk = a.npblk;
+      ntok = s_plen[r] - b * kBlock;
+    } else {
+      const int bs = b - nbp;
+      entry = a.stab[(long)r * a.sstride + bs];
+      kp = (const char*)a.sk; vp = (const char*)a.sv; nblk = a.nsblk;
+      ntok = s_slen[r] - bs * kBlock;
+    }
+    const int blk = clampi(entry, 0, nblk - 1);
+    const size_t off = blk * blk_stride + (size_t)h * BLK_B + (size_t)lane * 16;
+#pragma unroll
+    for (int i = 0; i < IPB; ++i) { B.k[i] = ld16(kp + off + i * 1024); B.v[i] = ld16(vp + off + i * 1024); }
+    B.q = ld16((const char*)a.q + ((size_t)(r * H + h) * D + sub * EPL) * E::kBytes);
+    B.ntok = ntok < kBlock ? ntok : kBlock;
+    B.seq = r * H + h;
+    B.piece_end = (b == cnt - 1);
+    // advance the cursor to the next column (same head)
+    if (++b == cnt) {
+      b = 0;
+      do { ++r; } while (r < R && s_cnt[r] == 0);
+      cnt = r < R ? s_cnt[r] : 1;
+    }
+  };
 
   float m = -INFINITY, l = 0.f;
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
 
-  const int b0 = t0 / kBlock, b1 = (t1 + kBlock - 1) / kBlock;
-  u32x4 kc[IPB], vc[IPB], kn[IPB], vn[IPB];
-  {
-    const int blk = clampi(tbl[b0], 0, nblk - 1);
-    const char* kb = kpool + blk * blk_stride + head_off;
-    const char* vb = vpool + blk * blk_stride + head_off;
+  // close the current piece of sequence `seq`: combine the token groups,
+  // write the normalised output and log-sum-exp, reset the state
+  auto close_piece = [&](int seq) {
 #pragma unroll
-    for (int i = 0; i < IPB; ++i) { kc[i] = ld16(kb + i * 1024); vc[i] = ld16(vb + i * 1024); }
-  }
-  for (int b = b0; b < b1; ++b) {
-    if (b + 1 < b1) {
-      const int blk = clampi(tbl[b + 1], 0, nblk - 1);
-      const char* kb = kpool + blk * blk_stride + head_off;
-      const char* vb = vpool + blk * blk_stride + head_off;
+    for (int off = LPT; off < kWave; off <<= 1) {
+      const float mo = __shfl_xor(m, off);
+      const float lo = __shfl_xor(l, off);
+      const float mn = fmaxf(m, mo);
+      const float mref = (mn == -INFINITY) ? 0.f : mn;
+      const float sa = fast_exp2(m - mref), sb = fast_exp2(mo - mref);
+      l = l * sa + lo * sb;
 #pragma unroll
-      for (int i = 0; i < IPB; ++i) { kn[i] = ld16(kb + i * 1024); vn[i] = ld16(vb + i * 1024); }
+      for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * sa + __shfl_xor(acc[e], off) * sb;
+      m = mn;
     }
+    const int piece = grp - s_excl[seq / H] / Q;
+    if (tg == 0) {
+      const size_t slot = (size_t)seq * a.seg + a.seg_p + piece;
+      const float inv = 1.f / l;
+      float* o = a.o_part + slot * D + sub * EPL;
+#pragma unroll
+      for (int e = 0; e < EPL; e += 4)
+        *reinterpret_cast<f32x4*>(o + e) = f32x4{acc[e] * inv, acc[e + 1] * inv, acc[e + 2] * inv, acc[e + 3] * inv};
+      if (lane == 0) a.lse_part[slot] = m + fast_log2(l);
+    }
+    m = -INFINITY; l = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  };
+
+  auto reduce = [&](Blk& B, bool run_end) {
     float s[IPB];
 #pragma unroll
-    for (int i = 0; i < IPB; ++i) s[i] = group_sum<LPT>(E::dot(kc[i], qf)) * a.scale_log2;
-    if (b * kBlock + kBlock > t1) {           // partly filled block: mask the tail
+    for (int i = 0; i < IPB; ++i) s[i] = group_sum<LPT>(E::dot(B.k[i], B.q)) * a.scale_log2;
+    if (B.ntok < kBlock) {                    // partly filled block: mask the tail
 #pragma unroll
       for (int i = 0; i < IPB; ++i) {
-        if (b * kBlock + i * TPI + tg >= t1) {
+        if (i * TPI + tg >= B.ntok) {
           s[i] = -INFINITY;
-          vc[i] = u32x4{0u, 0u, 0u, 0u};      // 0 * NaN would poison the sum
+          B.v[i] = u32x4{0u, 0u, 0u, 0u};     // 0 * NaN would poison the sum
         }
       }
     }
@@ -112,56 +217,44 @@ __global__ __launch_bounds__(256) void k_splitkv(SplitKVArgs a) {
 #pragma unroll
     for (int i = 0; i < IPB; ++i) {
       float v[EPL];
-      E::to_f32(vc[i], v);
+      E::to_f32(B.v[i], v);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(p[i], v[e], acc[e]);
     }
     m = mn;
-#pragma unroll
-    for (int i = 0; i < IPB; ++i) { kc[i] = kn[i]; vc[i] = vn[i]; }
-  }
+    if (B.piece_end || run_end) close_piece(B.seq);
+  };
 
-  // combine the token groups that share a row slice
-#pragma unroll
-  for (int off = LPT; off < kWave; off <<= 1) {
-    const float mo = __shfl_xor(m, off);
-    const float lo = __shfl_xor(l, off);
-    const float mn = fmaxf(m, mo);
-    const float mref = (mn == -INFINITY) ? 0.f : mn;
-    const float sa = fast_exp2(m - mref), sb = fast_exp2(mo - mref);
-    l = l * sa + lo * sb;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * sa + __shfl_xor(acc[e], off) * sb;
-    m = mn;
-  }
-  if (tg == 0) {
-    const size_t slot = (size_t)(r * H + h) * a.seg + c;
-    const float inv = 1.f / l;
-    float* o = a.o_part + slot * D + sub * EPL;
-#pragma unroll
-    for (int e = 0; e < EPL; e += 4)
-      *reinterpret_cast<f32x4*>(o + e) = f32x4{acc[e] * inv, acc[e + 1] * inv, acc[e + 2] * inv, acc[e + 3] * inv};
-    if (lane == 0) a.lse_part[slot] = m + fast_log2(l);
+  Blk A, Bb;
+  fetch(A);
+  for (int i = 0;; i += 2) {
+    if (i + 1 >= nblk_run) { reduce(A, true); break; }
+    fetch(Bb);
+    reduce(A, false);
+    if (i + 2 >= nblk_run) { reduce(Bb, true); break; }
+    fetch(A);
+    reduce(Bb, false);
   }
 }
 
 template <int DT, int D>
-static hipError_t launch_splitkv_t(const SplitKVArgs& a, hipStream_t s) {
-  const long waves = (long)a.R * a.nc * a.H;
-  if (waves <= 0) return hipSuccess;
-  const long blocks = (waves + 3) / 4;
-  hipLaunchKernelGGL((k_splitkv<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, a);
+static hipError_t launch_splitkv_t(const SplitKVArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (a.nwaves <= 0 || a.nwaves % kSkvWaves != 0 || a.nwaves / a.H < 1) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL((k_splitkv<DT, D>), dim3((unsigned)(a.nwaves / kSkvWaves)), dim3(kSkvWaves * 64), 0, s,
+                        e0, e1, 0, a);
   return hipGetLastError();
 }
 
-hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s) {
+hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+  if (a.R > kMaxRequests) return hipErrorInvalidValue;
   switch (dtype * 1000 + D) {
-    case kF32 * 1000 + 64: return launch_splitkv_t<kF32, 64>(a, s);
-    case kF32 * 1000 + 128: return launch_splitkv_t<kF32, 128>(a, s);
-    case kF16 * 1000 + 64: return launch_splitkv_t<kF16, 64>(a, s);
-    case kF16 * 1000 + 128: return launch_splitkv_t<kF16, 128>(a, s);
-    case kBF16 * 1000 + 64: return launch_splitkv_t<kBF16, 64>(a, s);
-    case kBF16 * 1000 + 128: return launch_splitkv_t<kBF16, 128>(a, s);
+    case kF32 * 1000 + 64: return launch_splitkv_t<kF32, 64>(a, s, e0, e1);
+    case kF32 * 1000 + 128: return launch_splitkv_t<kF32, 128>(a, s, e0, e1);
+    case kF16 * 1000 + 64: return launch_splitkv_t<kF16, 64>(a, s, e0, e1);
+    case kF16 * 1000 + 128: return launch_splitkv_t<kF16, 128>(a, s, e0, e1);
+    case kBF16 * 1000 + 64: return launch_splitkv_t<kBF16, 64>(a, s, e0, e1);
+    case kBF16 * 1000 + 128: return launch_splitkv_t<kBF16, 128>(a, s, e0, e1);
   }
   return hipErrorInvalidValue;
 }
