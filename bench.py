@@ -1,7 +1,8 @@
 """Benchmark: shared-prefix decode attention on one MI355X.
 
-One step is one call of parrot_shared_prefix_decode (prefix-group kernel,
-split-KV kernel, merge kernel) for one layer of a decode batch.  The default
+One step is one call of parrot_shared_prefix_decode (partial-result kernel
+with its prefix-group and split-KV roles, then the merge kernel) for one layer
+of a decode batch.  The default
 workload is the LLaMA-7B layer shape: 32 heads x 128, fp16 KV in 16-token
 blocks with permuted block tables, one prefix group of 32 requests sharing a
 2048-token prefix, own lengths U[64,512].  Steps cycle through `--layers`
@@ -10,8 +11,8 @@ still in the 256 MB Infinity Cache when it is read again.
 
 Prints one JSON line.  `value` is requests per second per layer
 (R / seconds per step).  The `roofline` object describes the dominant kernel
-(split-KV) from HIP events recorded on the launch stream around it during the
-timed steps; `cpu_baseline` times the float64 CPU oracle on a bounded sample
+(the partial-result kernel) from HIP events attached to its launches on the
+launch stream during the timed steps; `cpu_baseline` times the float64 CPU oracle on a bounded sample
 of the same workload.
 """
 from __future__ import annotations
@@ -30,8 +31,9 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16/bf16 MFMA
 ELT_BYTES = {"float32": 4, "float16": 2, "bfloat16": 2}
 DTYPE_TAG = {"float32": "f32", "float16": "f16", "bfloat16": "bf16"}
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "splitkv_counters.json")
-KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/splitkv.hip", "paper_2405_19888_amd/csrc/common.h"]
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "partials_counters.json")
+KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/partials.hip", "paper_2405_19888_amd/csrc/prefix_role.h",
+                  "paper_2405_19888_amd/csrc/splitkv_role.h", "paper_2405_19888_amd/csrc/common.h"]
 
 
 def kernel_source_hash() -> str:
@@ -97,7 +99,7 @@ def cpu_baseline(plan, layer_dev, budget_s: float):
 
 
 def traffic_from_counters(plan_key: str):
-    """HBM bytes per split-KV launch from committed rocprofv3 counter runs,
+    """HBM bytes per partial-result launch from committed rocprofv3 counter runs,
     only if they were taken on the current kernel source."""
     if not os.path.exists(COUNTERS_FILE):
         return None
@@ -155,7 +157,7 @@ def main():
     ab = algorithmic_bytes(plan)
     K, W, L = args.steps, args.warmup, args.layers
 
-    names = ("prefix", "splitkv", "merge")
+    names = ("partials", "merge")
 
     def run(shared: bool, trace: bool):
         """W untimed steps, then K timed steps; every `trace_every`-th timed step
@@ -163,7 +165,7 @@ def main():
         calls = [dec.bind(layers[l], shared=shared, stream=stream) for l in range(L)]
         every = max(1, args.trace_every)
         traced = list(range(0, K, every)) if trace else []
-        events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(6)] for i in traced}
+        events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in traced}
         for evs in events.values():       # materialise the events outside the timed region
             for e in evs:
                 e.record(stream)
@@ -181,8 +183,6 @@ def main():
         if trace:
             per = {}
             for k, name in enumerate(names):
-                if name == "prefix" and not shared:
-                    continue
                 per[name + "_us"] = sum(evs[2 * k].elapsed_time(evs[2 * k + 1])
                                         for evs in events.values()) * 1e3 / len(events)
             per["traced_steps"] = len(events)
@@ -217,23 +217,25 @@ def main():
     }
     result["hbm_frac"] = round(result["hbm_gbps"] / HBM_PEAK_GBPS, 4)
     if per is not None:
-        achieved = ab["splitkv"] / (per["splitkv_us"] * 1e-6) / 1e9
+        # dominant kernel: the partial-result kernel (prefix-group and split-KV roles)
+        part_bytes = ab["prefix_kv"] + ab["suffix_kv"] + ab["q"]
+        achieved = part_bytes / (per["partials_us"] * 1e-6) / 1e9
         traffic = traffic_from_counters(cfg.name)
         result["roofline"] = {
-            "kernel": "k_splitkv (own tokens of every request)",
+            "kernel": "k_partials (prefix-group MFMA role + split-KV role)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
-            "algorithmic_bytes": ab["splitkv"],
-            "avg_us": round(per["splitkv_us"], 3),
+            "algorithmic_bytes": part_bytes,
+            "avg_us": round(per["partials_us"], 3),
         }
-        prefix_s = per["prefix_us"] * 1e-6
         result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
         result["kernels_us"]["traced_steps"] = per["traced_steps"]
-        result["prefix_kernel"] = {
-            "hbm_gbps": round(ab["prefix_kv"] / prefix_s / 1e9, 1),
-            "mfma_tflops": round(ab["prefix_flops"] / prefix_s / 1e12, 2),
-            "mfma_util": round(ab["prefix_flops"] / prefix_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+        result["prefix_mfma"] = {
+            "flops": ab["prefix_flops"],
+            "tflops_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12, 2),
+            "util_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12
+                                               / MFMA_F16_PEAK_TFLOPS, 5),
         }
     if not args.no_baselines:
         wall_n, _ = run(shared=False, trace=False)

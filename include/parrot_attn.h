@@ -92,14 +92,13 @@ typedef struct {
 /* Optional timing hooks: hipEvent_t handles (each may be NULL), created by the
  * caller with timing enabled.  Each kernel of a call is launched with its pair
  * attached (hipExtLaunchKernel start/stop events), so the events carry that
- * kernel's own start and end time and add no marker work to the stream.  Pairs
- * of kernels a call does not run are left untouched. */
+ * kernel's own start and end time instead of adding marker work to the
+ * stream.  Attaching events still costs a few microseconds of stream time per
+ * kernel, so time throughput on calls without them. */
 typedef struct {
-  void* prefix_start;    /* prefix-group (MFMA) kernel */
-  void* prefix_stop;
-  void* splitkv_start;   /* split-KV (non-shared tokens) kernel */
-  void* splitkv_stop;
-  void* merge_start;     /* log-sum-exp merge kernel */
+  void* partials_start;  /* the partial-result kernel (split-KV + prefix-group roles) */
+  void* partials_stop;
+  void* merge_start;     /* the log-sum-exp merge kernel */
   void* merge_stop;
 } parrot_trace;
 
@@ -110,14 +109,16 @@ size_t parrot_workspace_bytes(const parrot_problem* p);
 
 /*
  * Shared-prefix decode attention (Section 5.3; Section 6, "Kernel
- * Optimization").  Three kernels run on `stream` in order:
- *   1. prefix-group kernel: for each (group, head, prefix chunk) the chunk's
- *      K/V tiles are staged in LDS once and all members' queries are computed
- *      against them on MFMA with an online softmax; one partial result per
- *      member is written to the workspace;
- *   2. split-KV kernel: each request's own tokens, in chunks, with 128-bit
- *      coalesced loads; one partial per chunk;
- *   3. merge kernel: log-sum-exp combination of all partials of (r, h).
+ * Optimization").  Two kernels run on `stream` in order:
+ *   1. the partial-result kernel, with two kinds of workgroups side by side:
+ *      - prefix-group: for each (group, head, prefix chunk) the chunk's K/V
+ *        tiles are staged in LDS once and all members' queries are computed
+ *        against them on MFMA with an online softmax; one partial result per
+ *        member is written to the workspace;
+ *      - split-KV: each request's own tokens, split into equal runs of
+ *        16-token blocks over a fixed grid, with 128-bit coalesced loads; one
+ *        partial per (request, head) piece;
+ *   2. the merge kernel: log-sum-exp combination of all partials of (r, h).
  *
  *   q                    [R][H][D] dtype, 16-byte aligned
  *   prefix_k, prefix_v   [num_prefix_blocks][H][B][D] dtype, 16-byte aligned
@@ -152,7 +153,8 @@ parrot_status parrot_shared_prefix_decode(
  * Per-request decode attention over the same inputs without sharing: every
  * request reads its group's prefix blocks itself, as a paged-attention
  * decode kernel does (the baseline the paper compares against in Section 8.3).
- * Same arguments, same results up to rounding; the prefix kernel is skipped.
+ * Same arguments, same results up to rounding; the partial-result kernel runs
+ * its split-KV role only, over prefix and own tokens.
  */
 parrot_status parrot_per_request_decode(
     const parrot_problem* p,

@@ -52,10 +52,8 @@ class ParrotProblem(ctypes.Structure):
 
 class ParrotTrace(ctypes.Structure):
     _fields_ = [
-        ("prefix_start", ctypes.c_void_p),
-        ("prefix_stop", ctypes.c_void_p),
-        ("splitkv_start", ctypes.c_void_p),
-        ("splitkv_stop", ctypes.c_void_p),
+        ("partials_start", ctypes.c_void_p),
+        ("partials_stop", ctypes.c_void_p),
         ("merge_start", ctypes.c_void_p),
         ("merge_stop", ctypes.c_void_p),
     ]

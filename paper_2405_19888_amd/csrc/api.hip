@@ -35,14 +35,14 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 #ifndef PARROT_PREFIX_CHUNK
 #define PARROT_PREFIX_CHUNK 256
 #endif
-#ifndef PARROT_SPLITKV_WAVES_PER_CU
-#define PARROT_SPLITKV_WAVES_PER_CU 8   // must match the split-KV kernel's setting
+#ifndef PARROT_SPLITKV_WGS_PER_CU
+#define PARROT_SPLITKV_WGS_PER_CU 2     // split-KV workgroups (4 waves each) per CU
 #endif
 #ifndef PARROT_SPLITKV_MIN_BLOCKS
 #define PARROT_SPLITKV_MIN_BLOCKS 2
 #endif
 constexpr int kPrefixChunk = PARROT_PREFIX_CHUNK;
-constexpr int kSplitkvWavesPerCu = PARROT_SPLITKV_WAVES_PER_CU;
+constexpr int kSplitkvWgsPerCu = PARROT_SPLITKV_WGS_PER_CU;
 constexpr int kSplitkvMinBlocks = PARROT_SPLITKV_MIN_BLOCKS;
 
 // Compute units of the current device (cached per device; no device sync).
@@ -106,9 +106,8 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   const long seg = std::max<long>(pl->seg_p + pieces_shared, pieces_naive);
   pl->seg = (int)seg;
   const long mg = p->num_groups > 0 ? p->max_group_size : 1;
-  const long waves = ceil_div(mg, 16) <= 4 ? 4 : 8;
-  pl->prefix_waves = (int)waves;
-  pl->prefix_qtiles = (int)ceil_div(mg, 16 * waves);
+  pl->prefix_waves = 4;
+  pl->prefix_qtiles = (int)ceil_div(mg, 16 * pl->prefix_waves);
   pl->skv_waves = 0;   // set at launch from the device's CU count
 
   const double slots = (double)p->num_requests * p->num_heads * seg;
@@ -127,6 +126,11 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
 
 hipEvent_t ev(void* p) { return reinterpret_cast<hipEvent_t>(p); }
 
+parrot_status hip_ok(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return PARROT_OK;
+}
+
 parrot_status launched(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(PARROT_ERR_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
   return PARROT_OK;
@@ -143,7 +147,7 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr};
   const parrot_trace& tr = trace ? *trace : none;
   if (p->num_requests == 0) {
     g_err.clear();
@@ -175,19 +179,10 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
   const float scale_log2 = p->sm_scale * parrot::kLog2e;
   const int D = p->head_dim, dt = (int)p->dtype;
 
-  if (shared && p->num_groups > 0 && pl.seg_p > 0) {
-    parrot::PrefixArgs a{};
-    a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.ptab = ptab; a.plen = plen; a.gid = gid;
-    a.o_part = o_part; a.lse_part = lse_part;
-    a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
-    a.pstride = p->prefix_table_stride; a.max_p = p->max_prefix_len; a.npblk = p->num_prefix_blocks;
-    a.seg = pl.seg; a.seg_p = pl.seg_p; a.cp = pl.cp; a.qtiles = pl.prefix_qtiles;
-    a.scale_log2 = scale_log2;
-    PARROT_TRY(launched(parrot::launch_prefix(a, dt, D, pl.prefix_waves, s, ev(tr.prefix_start),
-                                              ev(tr.prefix_stop)), "prefix-group kernel"));
-  }
+  const bool run_prefix = shared && p->num_groups > 0 && pl.seg_p > 0;
   {
-    parrot::SplitKVArgs a{};
+    parrot::PartialsArgs pa{};
+    parrot::SplitKVArgs& a = pa.skv;
     a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
     a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
     a.o_part = o_part; a.lse_part = lse_part; a.seq_info = seq_info;
@@ -197,13 +192,24 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
     a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0;
     a.with_prefix = shared ? 0 : 1;
-    // one workgroup per CU; a multiple of H waves so every column group has all heads
-    a.nwaves = num_cus() * kSplitkvWavesPerCu;
-    if (a.nwaves < a.H) a.nwaves = (int)ceil_div(a.H, kSplitkvWavesPerCu) * kSplitkvWavesPerCu;
+    // a fixed grid of split-KV workgroups per CU, at least one wave per head
+    pa.n_skv = num_cus() * kSplitkvWgsPerCu;
+    if (pa.n_skv * 4 < a.H) pa.n_skv = (int)ceil_div(a.H, 4);
+    a.nwaves = pa.n_skv * 4;
     a.min_q = pl.skv_min_q;
     a.scale_log2 = scale_log2;
-    PARROT_TRY(launched(parrot::launch_splitkv(a, dt, D, s, ev(tr.splitkv_start), ev(tr.splitkv_stop)),
-                        "split-KV kernel"));
+    if (run_prefix) {
+      parrot::PrefixArgs& b = pa.pre;
+      b.q = q; b.pk = prefix_k; b.pv = prefix_v; b.ptab = ptab; b.plen = plen; b.gid = gid;
+      b.o_part = o_part; b.lse_part = lse_part;
+      b.R = p->num_requests; b.H = p->num_heads; b.NG = p->num_groups;
+      b.pstride = p->prefix_table_stride; b.max_p = p->max_prefix_len; b.npblk = p->num_prefix_blocks;
+      b.seg = pl.seg; b.seg_p = pl.seg_p; b.cp = pl.cp; b.qtiles = pl.prefix_qtiles;
+      b.scale_log2 = scale_log2;
+      pa.n_pre = p->num_groups * pl.seg_p * p->num_heads * pl.prefix_qtiles;
+    }
+    PARROT_TRY(launched(parrot::launch_partials(pa, dt, D, s, ev(tr.partials_start), ev(tr.partials_stop)),
+                        "partials kernel"));
   }
   {
     parrot::MergeArgs a{};

@@ -90,10 +90,16 @@ struct ValidateArgs {
 // dtype codes follow parrot_dtype
 enum Dtype { kF32 = 0, kF16 = 1, kBF16 = 2 };
 
+// Both producers of partial results in one launch: n_skv split-KV workgroups
+// followed by n_pre prefix-group workgroups (none on the per-request path).
+struct PartialsArgs {
+  SplitKVArgs skv;
+  PrefixArgs pre;
+  int n_skv, n_pre;
+};
+
 // Each launcher attaches the optional (start, stop) timing events to its kernel.
-hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s, hipEvent_t e0,
-                         hipEvent_t e1);
+hipError_t launch_partials(const PartialsArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
 

@@ -1,0 +1,57 @@
+// The partial-result kernel: one launch that runs both producers of partial
+// attention results side by side.
+//
+//   workgroups [0, n_skv)            split-KV role: every request's own tokens
+//                                    (on the per-request path, prefix as well)
+//   workgroups [n_skv, n_skv + n_pre) prefix-group role: each group's shared
+//                                    prefix, read once for all of its members
+//
+// The split-KV workgroups come first so that they are all dispatched at once
+// (two per CU) and stream at full rate from the start; the prefix-group
+// workgroups take the third slot of every CU as it frees up.  Both roles fit
+// one launch shape: 256 threads, the LDS union of both roles (about 48 KiB,
+// three workgroups per CU) and a register budget of three waves per SIMD.
+#include "prefix_role.h"
+#include "splitkv_role.h"
+
+namespace parrot {
+
+constexpr int kPartialsLds = kPrefixLds > kSplitkvLds ? kPrefixLds : kSplitkvLds;
+
+template <int DT, int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+void k_partials(PartialsArgs a) {
+  __shared__ __attribute__((aligned(1024))) char lds[kPartialsLds];
+  if ((int)blockIdx.x < a.n_skv)
+    splitkv_role<DT, D>(a.skv, lds, blockIdx.x);
+  else
+    prefix_role<DT, D>(a.pre, lds, blockIdx.x - a.n_skv);
+}
+
+template <int DT, int D>
+static hipError_t launch_partials_t(const PartialsArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const long blocks = (long)a.n_skv + a.n_pre;
+  if (blocks <= 0) return hipSuccess;
+  hipExtLaunchKernelGGL((k_partials<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_partials(const PartialsArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0,
+                           hipEvent_t e1) {
+  if (a.skv.R > kMaxRequests || a.n_skv < 1 || a.skv.nwaves != a.n_skv * kSkvWaves ||
+      a.skv.nwaves / a.skv.H < 1)
+    return hipErrorInvalidValue;
+  if (a.n_pre > 0 && (a.pre.cp > prefix_detail::kMaxChunkBlocks * kBlock || a.pre.cp % 32 != 0))
+    return hipErrorInvalidValue;
+  switch (dtype * 1000 + D) {
+    case kF32 * 1000 + 64: return launch_partials_t<kF32, 64>(a, s, e0, e1);
+    case kF32 * 1000 + 128: return launch_partials_t<kF32, 128>(a, s, e0, e1);
+    case kF16 * 1000 + 64: return launch_partials_t<kF16, 64>(a, s, e0, e1);
+    case kF16 * 1000 + 128: return launch_partials_t<kF16, 128>(a, s, e0, e1);
+    case kBF16 * 1000 + 64: return launch_partials_t<kBF16, 64>(a, s, e0, e1);
+    case kBF16 * 1000 + 128: return launch_partials_t<kBF16, 128>(a, s, e0, e1);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace parrot

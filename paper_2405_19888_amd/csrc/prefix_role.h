@@ -26,16 +26,18 @@
 // (conflict-free transposed V reads).  The swizzle is applied on the global
 // side: each lane of a direct-to-LDS load fetches the granule that belongs at
 // its fixed LDS slot.
+#pragma once
+
 #include "common.h"
 
 namespace parrot {
 
-namespace {
+namespace prefix_detail {
 
 constexpr int kTensorStage = 8192;   // bytes of K (and of V) per stage
 constexpr int kStageBytes = 2 * kTensorStage;
 constexpr int kStageChunks = kStageBytes / 1024;  // 1 KiB per direct-to-LDS instruction
-constexpr int kRing = 4;             // stage buffers in LDS (kRing - 1 stages in flight)
+constexpr int kRing = 3;             // stage buffers in LDS (kRing - 1 stages in flight)
 constexpr int kMaxChunkBlocks = 64;  // prefix chunk <= 1024 tokens
 
 
@@ -95,10 +97,18 @@ template <> struct Mfma<kBF16> {
   }
 };
 
-}  // namespace
+}  // namespace prefix_detail
 
-template <int DT, int D, int W>
-__global__ __launch_bounds__(W * 64) void k_prefix(PrefixArgs a) {
+constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
+// LDS bytes the prefix role needs: the stage ring, members, block ids, count.
+constexpr int kPrefixLds = prefix_detail::kRing * prefix_detail::kStageBytes +
+                           (kPrefixWaves * 16 + prefix_detail::kMaxChunkBlocks + 4) * 4;
+
+// One workgroup of the prefix role; `wg` is the role-local workgroup index.
+template <int DT, int D>
+__device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int wg) {
+  using namespace prefix_detail;
+  constexpr int W = kPrefixWaves;
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;
   constexpr int GRAN = ROW_B / 16;                    // 16-byte granules per row
@@ -110,16 +120,15 @@ __global__ __launch_bounds__(W * 64) void k_prefix(PrefixArgs a) {
   static_assert(STAGE_BLK >= 1 && GRAN >= 8, "stage holds a block; swizzle fits a row");
   static_assert(kStageChunks % W == 0, "stage chunks split evenly over waves");
 
-  __shared__ __attribute__((aligned(1024))) char smem[kRing][kStageBytes];
-  __shared__ int members[W * 16];
-  __shared__ int s_tbl[kMaxChunkBlocks];
-  __shared__ int s_count;
+  auto smem = reinterpret_cast<char (*)[kStageBytes]>(lds);                 // [kRing][kStageBytes]
+  int* members = reinterpret_cast<int*>(lds + kRing * kStageBytes);        // [W * 16]
+  int* s_tbl = members + W * 16;                                           // [kMaxChunkBlocks]
+  int& s_count = s_tbl[kMaxChunkBlocks];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  int wg = blockIdx.x;
   const int H = a.H;
   const int h = wg % H; wg /= H;
   const int c = wg % a.seg_p; wg /= a.seg_p;
@@ -373,33 +382,6 @@ __global__ __launch_bounds__(W * 64) void k_prefix(PrefixArgs a) {
     for (int dt = 0; dt < DT16; ++dt) *reinterpret_cast<f32x4*>(dst + dt * 16) = o[dt] * inv;
     if (lane < 16) a.lse_part[slot] = m + fast_log2(lt);
   }
-}
-
-template <int DT, int D>
-static hipError_t launch_prefix_t(const PrefixArgs& a, int waves, hipStream_t s, hipEvent_t e0,
-                                  hipEvent_t e1) {
-  const long blocks = (long)a.NG * a.seg_p * a.H * a.qtiles;
-  if (blocks <= 0) return hipSuccess;
-  if (waves == 4)
-    hipExtLaunchKernelGGL((k_prefix<DT, D, 4>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
-  else
-    hipExtLaunchKernelGGL((k_prefix<DT, D, 8>), dim3((unsigned)blocks), dim3(512), 0, s, e0, e1, 0, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_prefix(const PrefixArgs& a, int dtype, int D, int waves, hipStream_t s,
-                         hipEvent_t e0, hipEvent_t e1) {
-  if ((waves != 4 && waves != 8) || a.cp > kMaxChunkBlocks * kBlock || a.cp % 32 != 0)
-    return hipErrorInvalidValue;
-  switch (dtype * 1000 + D) {
-    case kF32 * 1000 + 64: return launch_prefix_t<kF32, 64>(a, waves, s, e0, e1);
-    case kF32 * 1000 + 128: return launch_prefix_t<kF32, 128>(a, waves, s, e0, e1);
-    case kF16 * 1000 + 64: return launch_prefix_t<kF16, 64>(a, waves, s, e0, e1);
-    case kF16 * 1000 + 128: return launch_prefix_t<kF16, 128>(a, waves, s, e0, e1);
-    case kBF16 * 1000 + 64: return launch_prefix_t<kBF16, 64>(a, waves, s, e0, e1);
-    case kBF16 * 1000 + 128: return launch_prefix_t<kBF16, 128>(a, waves, s, e0, e1);
-  }
-  return hipErrorInvalidValue;
 }
 
 }  // namespace parrot

@@ -20,20 +20,20 @@
 // piece.  One block is reduced while the next one's loads are in flight; the
 // loop is unrolled by two with ping-pong registers and every load inside it is
 // unconditional, so the compiler's memory-wait counts stay exact.
+#pragma once
+
 #include "common.h"
 
 namespace parrot {
 
-// Waves per workgroup = per CU (one workgroup per CU); the register budget is
-// capped so that they are all resident at once (4 SIMDs per CU).
-#ifndef PARROT_SPLITKV_WAVES_PER_CU
-#define PARROT_SPLITKV_WAVES_PER_CU 8
-#endif
-constexpr int kSkvWaves = PARROT_SPLITKV_WAVES_PER_CU;
+constexpr int kSkvWaves = 4;   // waves per split-KV workgroup
+// LDS bytes the split-KV role needs: six per-request arrays and a total.
+constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 
+// One workgroup of the split-KV role; `wg` is the role-local workgroup index
+// and a.nwaves = 4 x (number of split-KV workgroups).
 template <int DT, int D>
-__global__ __launch_bounds__(kSkvWaves * 64) __attribute__((amdgpu_waves_per_eu(kSkvWaves / 4)))
-void k_splitkv(SplitKVArgs a) {
+__device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, int wg) {
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;        // bytes per token row
   constexpr int LPT = ROW_B / 16;             // lanes per token
@@ -45,9 +45,13 @@ void k_splitkv(SplitKVArgs a) {
 
   // per-request data: first flat block per head-sequence, blocks per
   // sequence, leading prefix blocks, group, prefix and own token counts
-  __shared__ int s_excl[kMaxRequests], s_cnt[kMaxRequests], s_nbp[kMaxRequests];
-  __shared__ int s_g[kMaxRequests], s_plen[kMaxRequests], s_slen[kMaxRequests];
-  __shared__ int s_total;
+  int* s_excl = reinterpret_cast<int*>(lds);
+  int* s_cnt = s_excl + kMaxRequests;
+  int* s_nbp = s_cnt + kMaxRequests;
+  int* s_g = s_nbp + kMaxRequests;
+  int* s_plen = s_g + kMaxRequests;
+  int* s_slen = s_plen + kMaxRequests;
+  int& s_total = s_slen[kMaxRequests];
 
   const int lane = threadIdx.x & 63;
   const int wave_in_wg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -86,11 +90,11 @@ void k_splitkv(SplitKVArgs a) {
   const int G = a.nwaves / H;                                 // column groups
   const int Qg = (C + G - 1) / G;
   const int Q = Qg > a.min_q ? Qg : a.min_q;                  // columns per group
-  if (blockIdx.x == 0) {                                      // for the merge
+  if (wg == 0) {                                              // for the merge
     for (int r = threadIdx.x; r < R; r += blockDim.x) a.seq_info[r] = s_excl[r];
     if (threadIdx.x == 0) a.seq_info[R] = Q;
   }
-  const int w = blockIdx.x * kSkvWaves + wave_in_wg;
+  const int w = wg * kSkvWaves + wave_in_wg;
   const int grp = w / H;
   int h = w % H;
   const int c0 = grp * Q;
@@ -235,28 +239,6 @@ void k_splitkv(SplitKVArgs a) {
     fetch(A);
     reduce(Bb, false);
   }
-}
-
-template <int DT, int D>
-static hipError_t launch_splitkv_t(const SplitKVArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (a.nwaves <= 0 || a.nwaves % kSkvWaves != 0 || a.nwaves / a.H < 1) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL((k_splitkv<DT, D>), dim3((unsigned)(a.nwaves / kSkvWaves)), dim3(kSkvWaves * 64), 0, s,
-                        e0, e1, 0, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_splitkv(const SplitKVArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0,
-                          hipEvent_t e1) {
-  if (a.R > kMaxRequests) return hipErrorInvalidValue;
-  switch (dtype * 1000 + D) {
-    case kF32 * 1000 + 64: return launch_splitkv_t<kF32, 64>(a, s, e0, e1);
-    case kF32 * 1000 + 128: return launch_splitkv_t<kF32, 128>(a, s, e0, e1);
-    case kF16 * 1000 + 64: return launch_splitkv_t<kF16, 64>(a, s, e0, e1);
-    case kF16 * 1000 + 128: return launch_splitkv_t<kF16, 128>(a, s, e0, e1);
-    case kBF16 * 1000 + 64: return launch_splitkv_t<kBF16, 64>(a, s, e0, e1);
-    case kBF16 * 1000 + 128: return launch_splitkv_t<kBF16, 128>(a, s, e0, e1);
-  }
-  return hipErrorInvalidValue;
 }
 
 }  // namespace parrot

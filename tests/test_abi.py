@@ -42,7 +42,7 @@ def base_problem(**over):
 
 def test_struct_layout_matches_header():
     assert ctypes.sizeof(B.ParrotProblem) == 14 * 4
-    assert ctypes.sizeof(B.ParrotTrace) == 6 * ctypes.sizeof(ctypes.c_void_p)
+    assert ctypes.sizeof(B.ParrotTrace) == 4 * ctypes.sizeof(ctypes.c_void_p)
 
 
 def test_workspace_sizes(parrot_lib):

@@ -281,14 +281,13 @@ def test_trace_events_time_each_kernel():
     plan = make_plan(get_config("c2"))
     dev = make_batch(plan).to("cuda")
     dec = Decoder(problem_for(plan))
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     for e in evs:
         e.record()
     torch.cuda.synchronize()
     tr = ParrotTrace(*[e.cuda_event for e in evs])
     dec(dev, shared=True, trace=tr)
     torch.cuda.synchronize()
-    times = [evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(3)]
+    times = [evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(2)]
     assert all(t > 0 for t in times), times
-    # the kernels run in order on one stream
-    assert evs[1].elapsed_time(evs[2]) >= 0 and evs[3].elapsed_time(evs[4]) >= 0
+    assert evs[1].elapsed_time(evs[2]) >= 0        # the merge runs after the partials
