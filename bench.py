@@ -120,6 +120,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle timing")
     ap.add_argument("--no-baselines", action="store_true", help="skip the per-request and CPU legs")
     ap.add_argument("--no-trace", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="first run three plain device copies of this many MiB (a known-size "
+                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     ap.add_argument("--trace-every", type=int, default=16,
                     help="attach per-kernel HIP events to every N-th timed step (each traced "
                          "launch costs a few microseconds of stream time)")
@@ -135,6 +138,14 @@ def main():
     from workloads import get_config, make_device_layer, make_plan
     from workloads.gen import TORCH_DTYPES
 
+    if args.copy_mib > 0:
+        n = args.copy_mib << 19                      # fp16 elements in that many MiB
+        src = torch.ones(n, dtype=torch.float16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = get_config(args.config)
     if cfg.layers != 1:
         raise SystemExit(f"{cfg.name} has {cfg.layers} layers; bench one-layer workloads")

@@ -128,6 +128,9 @@ ALIASES = {
 
 
 def get_config(name: str, **overrides) -> ConfigSpec:
+    if name.startswith("sweep_p"):
+        cfg = prefix_sweep(int(name[len("sweep_p"):]))
+        return cfg.with_(**overrides) if overrides else cfg
     cfg = CONFIGS[ALIASES.get(name, name)]
     return cfg.with_(**overrides) if overrides else cfg
 
