@@ -3,13 +3,13 @@
  *
  * One decode iteration of one attention layer for a batch of requests, where
  * requests forked from a common parent context share that context's prompt
- * prefix (Section 5.3, "Sharing Prompt Prefix"; Section 6, the engine's
+ * prefix (Section 5.3, "Sharing Prompt Prefix"; Section 7, the engine's
  * Fill/Generate with parent_context_id).  The shared prefix's keys and values
  * are read once per group, not once per request: a prefix stage computes
  * interim results (running max and exp-sum, here kept as an output vector and
  * a log-sum-exp) for every member of the group, a non-shared stage does the
  * same for each request's own tokens, and a merge joins them into the final
- * attention output (Section 6, "Kernel Optimization").
+ * attention output (Section 7, "Kernel Optimization").
  *
  * Result (per request r and head h; the paper defers the formula to the
  * FlashAttention and PagedAttention work it builds on):
@@ -19,7 +19,7 @@
  *   s_j = sm_scale * <q[r,h,:], K_j>,  lse[r,h] = ln sum_j exp(s_j),
  *   out[r,h,:] = sum_j exp(s_j - lse[r,h]) * V_j.
  *
- * Paged KV layout (Section 6: KV cache in non-contiguous blocks located
+ * Paged KV layout (Section 7: KV cache in non-contiguous blocks located
  * through a per-request page table): a K or V pool is
  *   [num_blocks][H][B][D] elements of `dtype`, row-major,
  * and token t of a sequence with block-table row `tbl` is
@@ -108,7 +108,7 @@ typedef struct {
 size_t parrot_workspace_bytes(const parrot_problem* p);
 
 /*
- * Shared-prefix decode attention (Section 5.3; Section 6, "Kernel
+ * Shared-prefix decode attention (Section 5.3; Section 7, "Kernel
  * Optimization").  Two kernels run on `stream` in order:
  *   1. the partial-result kernel, with two kinds of workgroups side by side:
  *      - prefix-group: for each (group, head, prefix chunk) the chunk's K/V

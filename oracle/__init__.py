@@ -4,7 +4,7 @@ This package is the checker, not the product.  Only the test suite, the smoke
 check of the entry module and the CPU-baseline leg of the benchmark may import
 it; the library path never calls it and has no CPU fallback.
 
-What it computes (Section 5.3, "Sharing Prompt Prefix", and Section 6,
+What it computes (Section 5.3, "Sharing Prompt Prefix", and Section 7,
 "Kernel Optimization"): decode-phase softmax attention of one query per request
 over that request's whole context, i.e. the shared prefix of its group followed
 by its own non-shared tokens, with keys and values read from a paged KV cache

@@ -1,6 +1,6 @@
 """Plain float64 decode attention over a paged KV cache (test infrastructure).
 
-Definitions (Section 5.3 and the "Kernel Optimization" paragraph of Section 6;
+Definitions (Section 5.3 and the "Kernel Optimization" paragraph of Section 7;
 the paper builds on the softmax attention of FlashAttention and PagedAttention
 and does not restate it, so the standard definition is written out here):
 
@@ -15,7 +15,7 @@ and does not restate it, so the standard definition is written out here):
       w_j    = exp(s_j - lse)
       out[d] = sum_j w_j * V_j[d]
 
-  Paged storage (Section 6, the per-request page table kept from
+  Paged storage (Section 7, the per-request page table kept from
   PagedAttention): token t of a sequence with block table row ``tbl`` lives at
   pool[tbl[t // B], h, t % B, :] of a [num_blocks, H, B, D] pool.
 
@@ -50,7 +50,7 @@ def _ints(x) -> np.ndarray:
 def gather_sequence(pool, table_row: Sequence[int], length: int) -> np.ndarray:
     """Tokens 0..length-1 of one paged sequence as float64 [length, H, D].
 
-    Token t is pool[table_row[t // B], :, t % B, :] (Section 6, paged KV with a
+    Token t is pool[table_row[t // B], :, t % B, :] (Section 7, paged KV with a
     per-request page table).
     """
     B = int(pool.shape[2])
@@ -97,7 +97,7 @@ def merge_segments(parts: Iterable[tuple]) -> tuple:
     segment alone, attention over their union is
         l = ln sum_i exp(l_i),   o = sum_i exp(l_i - l) * o_i,
     which is how the paper's kernel joins the prefix's interim results with
-    the non-shared tokens (Section 6, "Kernel Optimization").  Empty segments
+    the non-shared tokens (Section 7, "Kernel Optimization").  Empty segments
     (l_i = -inf) carry weight zero.
     """
     parts = list(parts)

@@ -29,11 +29,16 @@ long ceil_div(long a, long b) { return (a + b - 1) / b; }
 
 bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
 
-// Chunk sizes and slot counts.  Chunks are whole 16-token blocks.  The prefix
-// chunk bounds both the per-workgroup LDS pipeline depth and the number of
-// partials written per member; the non-shared chunk is one wavefront's work.
+// Chunk sizes and slot counts.  Chunks are whole 16-token blocks.  A prefix
+// chunk is one prefix-group workgroup's work; every chunk costs each member one
+// partial result written and merged, so the chunk starts at PARROT_PREFIX_CHUNK
+// tokens and doubles (up to 1024) while the prefix work would still give more
+// than PARROT_PREFIX_TARGET_WGS workgroups.
 #ifndef PARROT_PREFIX_CHUNK
 #define PARROT_PREFIX_CHUNK 256
+#endif
+#ifndef PARROT_PREFIX_TARGET_WGS
+#define PARROT_PREFIX_TARGET_WGS 512
 #endif
 #ifndef PARROT_SPLITKV_WGS_PER_CU
 #define PARROT_SPLITKV_WGS_PER_CU 2     // split-KV workgroups (4 waves each) per CU
@@ -42,6 +47,8 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 #define PARROT_SPLITKV_MIN_BLOCKS 2
 #endif
 constexpr int kPrefixChunk = PARROT_PREFIX_CHUNK;
+constexpr int kPrefixChunkMax = 1024;   // the prefix role's table stage holds 64 blocks
+constexpr long kPrefixTargetWgs = PARROT_PREFIX_TARGET_WGS;
 constexpr int kSplitkvWgsPerCu = PARROT_SPLITKV_WGS_PER_CU;
 constexpr int kSplitkvMinBlocks = PARROT_SPLITKV_MIN_BLOCKS;
 
@@ -92,7 +99,14 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
 
   if (p->num_requests > parrot::kMaxRequests)
     return fail(PARROT_ERR_UNSUPPORTED, "num_requests %d > %d per call", p->num_requests, parrot::kMaxRequests);
+  const long mg = p->num_groups > 0 ? p->max_group_size : 1;
+  pl->prefix_waves = 4;
+  pl->prefix_qtiles = (int)ceil_div(mg, 16 * pl->prefix_waves);
   pl->cp = kPrefixChunk;
+  if (p->num_groups > 0) {
+    const double work = (double)p->max_prefix_len * p->num_groups * p->num_heads * pl->prefix_qtiles;
+    while (pl->cp < kPrefixChunkMax && work / pl->cp > (double)kPrefixTargetWgs) pl->cp *= 2;
+  }
   pl->skv_min_q = kSplitkvMinBlocks;
   // slots: shared path = prefix chunks + split-KV pieces of the own tokens;
   // per-request path = split-KV pieces of prefix + own tokens.  One stride
@@ -105,9 +119,6 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   pl->seg_s = (int)pieces_shared;
   const long seg = std::max<long>(pl->seg_p + pieces_shared, pieces_naive);
   pl->seg = (int)seg;
-  const long mg = p->num_groups > 0 ? p->max_group_size : 1;
-  pl->prefix_waves = 4;
-  pl->prefix_qtiles = (int)ceil_div(mg, 16 * pl->prefix_waves);
   pl->skv_waves = 0;   // set at launch from the device's CU count
 
   const double slots = (double)p->num_requests * p->num_heads * seg;
@@ -119,7 +130,7 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
   pl->lse_bytes = align256(n_slots * sizeof(float));
-  pl->info_bytes = align256(((size_t)p->num_requests + 1) * sizeof(int32_t));
+  pl->info_bytes = align256((size_t)p->num_requests * 2 * sizeof(int32_t));
   pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes + pl->info_bytes : 0;
   return PARROT_OK;
 }
@@ -175,7 +186,7 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
 
   float* o_part = reinterpret_cast<float*>(workspace);
   float* lse_part = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + pl.o_bytes);
-  int* seq_info = reinterpret_cast<int*>(reinterpret_cast<char*>(workspace) + pl.o_bytes + pl.lse_bytes);
+  int* merge_meta = reinterpret_cast<int*>(reinterpret_cast<char*>(workspace) + pl.o_bytes + pl.lse_bytes);
   const float scale_log2 = p->sm_scale * parrot::kLog2e;
   const int D = p->head_dim, dt = (int)p->dtype;
 
@@ -185,12 +196,12 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     parrot::SplitKVArgs& a = pa.skv;
     a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
     a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
-    a.o_part = o_part; a.lse_part = lse_part; a.seq_info = seq_info;
+    a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
     a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
     a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
     a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
-    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0;
+    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0; a.cp = pl.cp;
     a.with_prefix = shared ? 0 : 1;
     // a fixed grid of split-KV workgroups per CU, at least one wave per head
     pa.n_skv = num_cus() * kSplitkvWgsPerCu;
@@ -213,13 +224,10 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
   }
   {
     parrot::MergeArgs a{};
-    a.o_part = o_part; a.lse_part = lse_part; a.seq_info = seq_info;
-    a.plen = plen; a.slen = slen; a.gid = gid;
+    a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.out = out; a.lse = lse;
-    a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
-    a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
-    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0; a.cp = pl.cp;
-    a.with_prefix = shared ? 0 : 1;
+    a.R = p->num_requests; a.H = p->num_heads;
+    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0;
     PARROT_TRY(launched(parrot::launch_merge(a, dt, D, s, ev(tr.merge_start), ev(tr.merge_stop)),
                         "merge kernel"));
   }

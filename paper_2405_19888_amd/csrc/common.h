@@ -17,8 +17,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 // Partial results live in the workspace as
 //   o_part  [R][H][seg][D] float32   (normalised partial output of one piece)
 //   lse_part[R][H][seg]    float32   (base-2 log-sum-exp of the piece's scaled logits)
-//   seq_info[R + 1]        int32     (split-KV: first flat block of each request,
-//                                     then the blocks-per-wave of the launch)
+//   merge_meta[R][2]       int32     (per request: prefix-chunk slots, split-KV pieces)
 // Slots [0, seg_p) hold the prefix-group kernel's chunks (chunk c covers prefix
 // tokens [c*cp, (c+1)*cp)); slots [seg_p, seg) hold split-KV pieces.  The
 // split-KV kernel sees every request's blocks (own tokens, preceded by its
@@ -45,12 +44,12 @@ struct SplitKVArgs {
   const int* stab; const int* slen;
   const int* gid;
   float* o_part; float* lse_part;
-  int* seq_info;
+  int* merge_meta;       // written by split-KV workgroup 0 for the merge
   int R, H, NG;
   int pstride, sstride;
   int max_p, max_s;
   int npblk, nsblk;
-  int seg, seg_p;
+  int seg, seg_p, cp;
   int with_prefix;       // 1: each sequence is the group prefix, then the own tokens
   int nwaves;            // waves launched
   int min_q;             // blocks per wave >= min_q
@@ -71,13 +70,10 @@ struct PrefixArgs {
 
 struct MergeArgs {
   const float* o_part; const float* lse_part;
-  const int* seq_info;
-  const int* plen; const int* slen; const int* gid;
+  const int* merge_meta;
   void* out; float* lse;
-  int R, H, NG;
-  int max_p, max_s;
-  int seg, seg_p, cp;
-  int with_prefix;       // split-KV sequences include the group prefix (per-request path)
+  int R, H;
+  int seg, seg_p;
 };
 
 struct ValidateArgs {

@@ -3,7 +3,7 @@
 //
 // Partials of disjoint key sets combine exactly: with base-2 log-sum-exps
 // l_i and normalised outputs o_i, the union has l = log2 sum_i 2^{l_i} and
-// o = sum_i 2^{l_i - l} o_i (Section 6, "Kernel Optimization": the prefix's
+// o = sum_i 2^{l_i - l} o_i (Section 7, "Kernel Optimization": the prefix's
 // interim results are amalgamated with the non-shared part).
 #include "common.h"
 
@@ -20,34 +20,25 @@ PARROT_DEV float group_max(float x) {
   return x;
 }
 
-// One wave per (request, head); each lane owns D/64 output elements.  Lane i
-// reads the log-sum-exp of slot i, so one round of loads gives every weight;
-// the weights are then broadcast with readlane while the partial outputs of
-// up to kUnroll slots are loaded together.
+// One wave per (request, head); each lane owns D/64 output elements.  The
+// request's slot counts come from the descriptor the split-KV workgroup 0
+// wrote, so the only dependent load before the data is that descriptor.  Lane
+// i then reads the log-sum-exp of slot i while the partial outputs of the
+// first kBatch slots are loaded in the same round; later slots (long prefixes
+// or long runs) are read batch by batch with their weights.
 template <int DT, int D>
 __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   using E = Elem<DT>;
   constexpr int EPL = D / kWave;
-  constexpr int kUnroll = 8;
+  constexpr int kBatch = 64 / EPL;          // 32 slots for D = 128
   const int lane = threadIdx.x & 63;
   const long w = (long)blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (w >= (long)a.R * a.H) return;
   const int r = (int)(w / a.H);
   const int h = (int)(w % a.H);
-  const int g = a.gid[r];
-  const int P = (g >= 0 && g < a.NG) ? clampi(a.plen[g], 0, a.max_p) : 0;
-  const int S = clampi(a.slen[r], 0, a.max_s);
-  // prefix-group kernel chunks (shared path) occupy slots [0, np)
-  const int np = a.with_prefix ? 0 : (P + a.cp - 1) / a.cp;
-  // split-KV pieces: the waves whose runs cover this sequence
-  const int cnt = (a.with_prefix ? (P + kBlock - 1) / kBlock : 0) + (S + kBlock - 1) / kBlock;
-  int ns = 0;
-  if (cnt > 0) {
-    const int Q = a.seq_info[a.R];
-    const int first = a.seq_info[r];
-    ns = (first + cnt - 1) / Q - first / Q + 1;
-  }
-  const int n = np + ns;
+  const int2 meta = *reinterpret_cast<const int2*>(a.merge_meta + 2 * r);
+  const int np = meta.x;                    // prefix-chunk slots [0, np)
+  const int n = np + meta.y;                // then split-KV pieces from seg_p on
   const size_t base = (size_t)(r * a.H + h) * a.seg;
   char* outp = (char*)a.out + ((size_t)(r * a.H + h) * D + lane * EPL) * E::kBytes;
   if (n == 0) {  // empty context: defined as out = 0, lse = -inf
@@ -57,33 +48,56 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     return;
   }
   auto slot_of = [&](int i) { return i < np ? i : a.seg_p + (i - np); };
-  float mx = -INFINITY;
-  for (int i = lane; i < n; i += kWave) mx = fmaxf(mx, a.lse_part[base + slot_of(i)]);
+  auto load_o = [&](int i, float* v) {
+    const float* src = a.o_part + (base + slot_of(i)) * D + lane * EPL;
+    if constexpr (EPL == 2) {
+      const float2 x = *reinterpret_cast<const float2*>(src);
+      v[0] = x.x; v[1] = x.y;
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) v[e] = src[e];
+    }
+  };
+
+  // round 1: every lane's lse slot and the first batch of outputs together
+  const float l_lane = lane < n ? a.lse_part[base + slot_of(lane)] : -INFINITY;
+  float v[kBatch][EPL];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) load_o(min(u, n - 1), v[u]);
+
+  float mx = l_lane;
+  for (int i = lane + kWave; i < n; i += kWave) mx = fmaxf(mx, a.lse_part[base + slot_of(i)]);
   mx = group_max<64>(mx);
-  float tot = 0.f;
+  const float w_lane = lane < n ? fast_exp2(l_lane - mx) : 0.f;
+  float tot = w_lane;
+  for (int i = lane + kWave; i < n; i += kWave) tot += fast_exp2(a.lse_part[base + slot_of(i)] - mx);
+  tot = group_sum<64>(tot);
+
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
-  for (int i0 = 0; i0 < n; i0 += kWave) {
-    const int cnt = min(kWave, n - i0);
-    const float wl = lane < cnt ? fast_exp2(a.lse_part[base + slot_of(i0 + lane)] - mx) : 0.f;
-    tot += group_sum<64>(wl);
-    for (int j0 = 0; j0 < cnt; j0 += kUnroll) {
-      float v[kUnroll][EPL];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int j = min(j0 + u, cnt - 1);
-        const float* src = a.o_part + (base + slot_of(i0 + j)) * D + lane * EPL;
+  for (int u = 0; u < kBatch; ++u) {
+    if (u < n) {
+      const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w_lane), u));
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) v[u][e] = src[e];
-      }
+      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wu, v[u][e], acc[e]);
+    }
+  }
+  for (int j0 = kBatch; j0 < n; j0 += kBatch) {
+    float wv[kBatch];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        if (j0 + u < cnt) {
-          const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), j0 + u));
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = min(j0 + u, n - 1);
+      load_o(j, v[u]);
+      wv[u] = a.lse_part[base + slot_of(j)];
+    }
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wu, v[u][e], acc[e]);
-        }
+    for (int u = 0; u < kBatch; ++u) {
+      if (j0 + u < n) {
+        const float wu = fast_exp2(wv[u] - mx);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wu, v[u][e], acc[e]);
       }
     }
   }

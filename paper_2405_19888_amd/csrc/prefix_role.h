@@ -2,7 +2,7 @@
 //
 // One workgroup owns (group g, head h, prefix chunk c, query tile qt).  The
 // chunk's K and V blocks pass through LDS in 16 KiB stages (K and V together),
-// so the shared prefix is read from HBM once per group (Section 6, "Kernel
+// so the shared prefix is read from HBM once per group (Section 7, "Kernel
 // Optimization": prefix KV tiles are loaded to on-chip memory once and reused
 // by every request of the group).  Stages are fetched with direct-to-LDS loads
 // (global_load_lds_dwordx4) into a ring of three stage buffers, two stages

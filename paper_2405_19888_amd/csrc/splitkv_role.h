@@ -8,7 +8,8 @@
 // group g, so every wave streams the same number of bytes, and the H waves of
 // a group walk the same physical blocks at the same time, reading all heads
 // of a 16-token block (one contiguous H*4 KiB region per tensor) together.
-// One workgroup of 16 waves runs per CU, so the per-CU load is even too.  A run
+// The role's grid is a fixed number of 4-wave workgroups per CU, so the
+// per-CU load is even too.  A run
 // may cross request boundaries: the wave then emits one partial result
 // (normalised output and base-2 log-sum-exp) per (request, head) piece.
 //
@@ -27,6 +28,9 @@
 namespace parrot {
 
 constexpr int kSkvWaves = 4;   // waves per split-KV workgroup
+#ifndef PARROT_SKV_DEPTH
+#define PARROT_SKV_DEPTH 2         // register buffers per wave (blocks in flight + 1)
+#endif
 // LDS bytes the split-KV role needs: six per-request arrays and a total.
 constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 
@@ -90,9 +94,20 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
   const int G = a.nwaves / H;                                 // column groups
   const int Qg = (C + G - 1) / G;
   const int Q = Qg > a.min_q ? Qg : a.min_q;                  // columns per group
-  if (wg == 0) {                                              // for the merge
-    for (int r = threadIdx.x; r < R; r += blockDim.x) a.seq_info[r] = s_excl[r];
-    if (threadIdx.x == 0) a.seq_info[R] = Q;
+  if (wg == 0) {
+    // Merge descriptor of each request: how many prefix-chunk slots (shared
+    // path: chunks of its group's prefix) and how many split-KV pieces (the
+    // column groups its run of columns touches) hold its partial results.
+    for (int rr = threadIdx.x; rr < R; rr += blockDim.x) {
+      int np = 0;
+      if (!a.with_prefix) {
+        const int g = a.gid[rr];
+        if (g >= 0 && g < a.NG) np = (clampi(a.plen[g], 0, a.max_p) + a.cp - 1) / a.cp;
+      }
+      const int first = s_excl[rr], n = s_cnt[rr];
+      const int ns = n > 0 ? (first + n - 1) / Q - first / Q + 1 : 0;
+      *reinterpret_cast<int2*>(a.merge_meta + 2 * rr) = make_int2(np, ns);
+    }
   }
   const int w = wg * kSkvWaves + wave_in_wg;
   const int grp = w / H;
@@ -229,6 +244,24 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     if (B.piece_end || run_end) close_piece(B.seq);
   };
 
+#if PARROT_SKV_DEPTH == 3
+  // two blocks in flight while one is reduced (three register buffers)
+  Blk A, Bb, Cc;
+  fetch(A);
+  if (nblk_run == 1) { reduce(A, true); return; }
+  fetch(Bb);
+  for (int i = 0;; i += 3) {
+    if (i + 2 >= nblk_run) { reduce(A, false); reduce(Bb, true); break; }
+    fetch(Cc);
+    reduce(A, false);
+    if (i + 3 >= nblk_run) { reduce(Bb, false); reduce(Cc, true); break; }
+    fetch(A);
+    reduce(Bb, false);
+    if (i + 4 >= nblk_run) { reduce(Cc, false); reduce(A, true); break; }
+    fetch(Bb);
+    reduce(Cc, false);
+  }
+#else
   Blk A, Bb;
   fetch(A);
   for (int i = 0;; i += 2) {
@@ -239,6 +272,7 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     fetch(A);
     reduce(Bb, false);
   }
+#endif
 }
 
 }  // namespace parrot
