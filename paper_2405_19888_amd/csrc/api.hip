@@ -30,15 +30,9 @@ long ceil_div(long a, long b) { return (a + b - 1) / b; }
 bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
 
 // Chunk sizes and slot counts.  Chunks are whole 16-token blocks.  A prefix
-// chunk is one prefix-group workgroup's work; every chunk costs each member one
-// partial result written and merged, so the chunk starts at PARROT_PREFIX_CHUNK
-// tokens and doubles (up to 1024) while the prefix work would still give more
-// than PARROT_PREFIX_TARGET_WGS workgroups.
+// chunk is one prefix-group workgroup's work (see prefix_chunk below).
 #ifndef PARROT_PREFIX_CHUNK
 #define PARROT_PREFIX_CHUNK 256
-#endif
-#ifndef PARROT_PREFIX_TARGET_WGS
-#define PARROT_PREFIX_TARGET_WGS 512
 #endif
 #ifndef PARROT_SPLITKV_WGS_PER_CU
 #define PARROT_SPLITKV_WGS_PER_CU 2     // split-KV workgroups (4 waves each) per CU
@@ -48,7 +42,6 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 #endif
 constexpr int kPrefixChunk = PARROT_PREFIX_CHUNK;
 constexpr int kPrefixChunkMax = 1024;   // the prefix role's table stage holds 64 blocks
-constexpr long kPrefixTargetWgs = PARROT_PREFIX_TARGET_WGS;
 constexpr int kSplitkvWgsPerCu = PARROT_SPLITKV_WGS_PER_CU;
 constexpr int kSplitkvMinBlocks = PARROT_SPLITKV_MIN_BLOCKS;
 
@@ -63,6 +56,32 @@ int num_cus() {
     cache[dev].store(v, std::memory_order_relaxed);
   }
   return v;
+}
+
+// Prefix chunk length.  One prefix-group workgroup streams one chunk of one
+// head for up to 64 members, about two 16 KiB stages in flight, so its run time
+// grows with the chunk; every chunk also costs each member one partial result
+// written and merged.  With n(c) = max_prefix_len * groups * heads * query
+// tiles / c workgroups for chunk c (an upper bound: the host only knows the
+// maximum prefix length), measured on MI355X:
+//  * n(1024) <= CUs: the smallest c in {256, 512, 1024} with n(c) <= CUs; all
+//    prefix workgroups then run alongside the own-token stream from the start;
+//  * CUs < n(1024) <= 2 CUs: c = 512, so that the workgroups that start late
+//    (once the own-token stream drains) are short;
+//  * otherwise c = 1024 (many rounds anyway; fewest partial results).
+int prefix_chunk(const parrot_problem* p, int qtiles) {
+  if (p->num_groups <= 0) return kPrefixChunk;
+  const double work = (double)p->max_prefix_len * p->num_groups * p->num_heads * qtiles;
+  const double cus = num_cus();
+  int cp = kPrefixChunk;
+  if (work / kPrefixChunkMax <= cus) {
+    while (cp < kPrefixChunkMax && work / cp > cus) cp *= 2;
+  } else if (work / kPrefixChunkMax <= 2 * cus) {
+    cp = std::max(cp, kPrefixChunkMax / 2);
+  } else {
+    cp = std::max(cp, kPrefixChunkMax);
+  }
+  return cp;
 }
 
 parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
@@ -102,11 +121,7 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   const long mg = p->num_groups > 0 ? p->max_group_size : 1;
   pl->prefix_waves = 4;
   pl->prefix_qtiles = (int)ceil_div(mg, 16 * pl->prefix_waves);
-  pl->cp = kPrefixChunk;
-  if (p->num_groups > 0) {
-    const double work = (double)p->max_prefix_len * p->num_groups * p->num_heads * pl->prefix_qtiles;
-    while (pl->cp < kPrefixChunkMax && work / pl->cp > (double)kPrefixTargetWgs) pl->cp *= 2;
-  }
+  pl->cp = prefix_chunk(p, pl->prefix_qtiles);
   pl->skv_min_q = kSplitkvMinBlocks;
   // slots: shared path = prefix chunks + split-KV pieces of the own tokens;
   // per-request path = split-KV pieces of prefix + own tokens.  One stride

@@ -221,6 +221,19 @@ PARROT_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 // 16-byte global load (kept as a plain vector load so the compiler emits
 // global_load_dwordx4).
 PARROT_DEV u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+// Wave-uniform read of a read-only int through the constant address space,
+// which the compiler turns into a scalar load.  Scalar loads are counted by
+// lgkmcnt, so waiting for such a value (a block-table entry that the next KV
+// addresses depend on) does not also wait for the vector loads in flight.
+PARROT_DEV int ld_uniform(const int* p) {
+  typedef __attribute__((address_space(4))) const int const_int;
+  return *reinterpret_cast<const_int*>(reinterpret_cast<uintptr_t>(p));
+}
+// Streaming 16-byte load (nontemporal hint) for KV data read once per call:
+// on this GPU it sustains about 10 % more read bandwidth than a cached load.
+PARROT_DEV u32x4 ld16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 // Reinterpret one 32-bit word as a pair of 16-bit floats.  The word is taken
 // by value on purpose: this compiler's __builtin_bit_cast applied directly to an

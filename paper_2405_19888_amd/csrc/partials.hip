@@ -6,11 +6,13 @@
 //   workgroups [n_skv, n_skv + n_pre) prefix-group role: each group's shared
 //                                    prefix, read once for all of its members
 //
-// The split-KV workgroups come first so that they are all dispatched at once
-// (two per CU) and stream at full rate from the start; the prefix-group
-// workgroups take the third slot of every CU as it frees up.  Both roles fit
-// one launch shape: 256 threads, the LDS union of both roles (about 48 KiB,
-// three workgroups per CU) and a register budget of three waves per SIMD.
+// The split-KV grid is two workgroups per CU and the prefix-group work of the
+// benchmark workloads is about one more per CU, so every workgroup is resident
+// from the start (measured: each CU holds eight split-KV waves and four
+// prefix-group waves) and the prefix work overlaps the own-token stream.  Both
+// roles fit one launch shape: 256 threads, the LDS union of both roles (about
+// 48 KiB, three workgroups per CU) and a register budget of three waves per
+// SIMD.
 #include "prefix_role.h"
 #include "splitkv_role.h"
 
@@ -19,11 +21,19 @@ namespace parrot {
 constexpr int kPartialsLds = kPrefixLds > kSplitkvLds ? kPrefixLds : kSplitkvLds;
 
 template <int DT, int D>
+__device__ __forceinline__ void run_splitkv(const SplitKVArgs& a, char* lds, int wg) {
+  if (a.with_prefix)
+    splitkv_role<DT, D, false>(a, lds, wg);   // per-request path: cached loads
+  else
+    splitkv_role<DT, D, true>(a, lds, wg);    // shared path: streaming loads
+}
+
+template <int DT, int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
 void k_partials(PartialsArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds[kPartialsLds];
   if ((int)blockIdx.x < a.n_skv)
-    splitkv_role<DT, D>(a.skv, lds, blockIdx.x);
+    run_splitkv<DT, D>(a.skv, lds, blockIdx.x);
   else
     prefix_role<DT, D>(a.pre, lds, blockIdx.x - a.n_skv);
 }

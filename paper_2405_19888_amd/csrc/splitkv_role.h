@@ -28,15 +28,22 @@
 namespace parrot {
 
 constexpr int kSkvWaves = 4;   // waves per split-KV workgroup
-#ifndef PARROT_SKV_DEPTH
-#define PARROT_SKV_DEPTH 2         // register buffers per wave (blocks in flight + 1)
-#endif
 // LDS bytes the split-KV role needs: six per-request arrays and a total.
 constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 
 // One workgroup of the split-KV role; `wg` is the role-local workgroup index
 // and a.nwaves = 4 x (number of split-KV workgroups).
-template <int DT, int D>
+//
+// Load policy, chosen per path by measurement on MI355X:
+//  * STREAM (the shared path: every KV block is read once per call): K/V use
+//    a nontemporal hint, and a block's table entry is an ordinary vector
+//    load.  Waiting for that entry also waits for the previous block, so
+//    about one block per wave is in flight; with the HBM already saturated
+//    this runs slightly faster than keeping two blocks in flight.
+//  * per-request path (each member re-reads its group's prefix, mostly from
+//    the caches): cached K/V loads, and table entries as scalar loads so the
+//    next block's K/V loads can issue while the current block is in flight.
+template <int DT, int D, bool STREAM>
 __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, int wg) {
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;        // bytes per token row
@@ -147,19 +154,23 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     const char* vp;
     int entry, nblk, ntok;
     if (b < nbp) {
-      entry = a.ptab[(long)s_g[r] * a.pstride + b];
+      entry = STREAM ? a.ptab[(long)s_g[r] * a.pstride + b]
+                     : ld_uniform(a.ptab + (long)s_g[r] * a.pstride + b);
       kp = (const char*)a.pk; vp = (const char*)a.pv; nblk = a.npblk;
       ntok = s_plen[r] - b * kBlock;
     } else {
       const int bs = b - nbp;
-      entry = a.stab[(long)r * a.sstride + bs];
+      entry = STREAM ? a.stab[(long)r * a.sstride + bs] : ld_uniform(a.stab + (long)r * a.sstride + bs);
       kp = (const char*)a.sk; vp = (const char*)a.sv; nblk = a.nsblk;
       ntok = s_slen[r] - bs * kBlock;
     }
     const int blk = clampi(entry, 0, nblk - 1);
     const size_t off = blk * blk_stride + (size_t)h * BLK_B + (size_t)lane * 16;
 #pragma unroll
-    for (int i = 0; i < IPB; ++i) { B.k[i] = ld16(kp + off + i * 1024); B.v[i] = ld16(vp + off + i * 1024); }
+    for (int i = 0; i < IPB; ++i) {
+      B.k[i] = STREAM ? ld16_stream(kp + off + i * 1024) : ld16(kp + off + i * 1024);
+      B.v[i] = STREAM ? ld16_stream(vp + off + i * 1024) : ld16(vp + off + i * 1024);
+    }
     B.q = ld16((const char*)a.q + ((size_t)(r * H + h) * D + sub * EPL) * E::kBytes);
     B.ntok = ntok < kBlock ? ntok : kBlock;
     B.seq = r * H + h;
@@ -244,24 +255,6 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     if (B.piece_end || run_end) close_piece(B.seq);
   };
 
-#if PARROT_SKV_DEPTH == 3
-  // two blocks in flight while one is reduced (three register buffers)
-  Blk A, Bb, Cc;
-  fetch(A);
-  if (nblk_run == 1) { reduce(A, true); return; }
-  fetch(Bb);
-  for (int i = 0;; i += 3) {
-    if (i + 2 >= nblk_run) { reduce(A, false); reduce(Bb, true); break; }
-    fetch(Cc);
-    reduce(A, false);
-    if (i + 3 >= nblk_run) { reduce(Bb, false); reduce(Cc, true); break; }
-    fetch(A);
-    reduce(Bb, false);
-    if (i + 4 >= nblk_run) { reduce(Cc, false); reduce(A, true); break; }
-    fetch(Bb);
-    reduce(Cc, false);
-  }
-#else
   Blk A, Bb;
   fetch(A);
   for (int i = 0;; i += 2) {
@@ -272,7 +265,6 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     fetch(A);
     reduce(Bb, false);
   }
-#endif
 }
 
 }  // namespace parrot

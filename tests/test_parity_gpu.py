@@ -123,16 +123,16 @@ def edge_plan(kind, dtype, D, seed=0):
         return build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype,
                           group_of_request=[0, 0, 1, 1, 1], prefix_lens=[256, 512],
                           suffix_lens=[128, 256, 0, 384, 16], sm_scale=scale, shuffle=True, rng=rng)
-    if kind == "chunk512":
-        # enough prefix work that the prefix chunk grows to 512 tokens
-        # (max prefix x groups x heads = 5000 x 4 x 8)
+    if kind == "long_prefix_4g":
+        # enough prefix work (max prefix x groups x heads = 5000 x 4 x 8) that
+        # the prefix chunk grows past 256 tokens (1024 on a 256-CU device)
         gor = [0, 0, 1, 2, 2, 3, -1]
         return build_plan(heads=8, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
                           prefix_lens=[5000, 511, 513, 1537],
                           suffix_lens=rng.integers(0, 90, size=len(gor)).tolist(), sm_scale=scale,
                           shuffle=True, rng=rng)
-    if kind == "chunk1024":
-        # ... and to 1024 tokens (4200 x 8 x 8)
+    if kind == "long_prefix_8g":
+        # 4200 x 8 x 8: a 512-token prefix chunk on a 256-CU device
         gor = [g for g in range(8) for _ in range(2)]
         return build_plan(heads=8, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
                           prefix_lens=[4200, 1025, 1023, 3000, 17, 2049, 4096, 700],
@@ -141,8 +141,8 @@ def edge_plan(kind, dtype, D, seed=0):
     raise ValueError(kind)
 
 
-EDGE_KINDS = ["boundaries", "big_group", "ungrouped", "single_key", "chunk_multiples", "chunk512",
-              "chunk1024"]
+EDGE_KINDS = ["boundaries", "big_group", "ungrouped", "single_key", "chunk_multiples",
+              "long_prefix_4g", "long_prefix_8g"]
 
 
 @pytest.mark.parametrize("D", [64, 128])
