@@ -7,13 +7,16 @@ workload is the LLaMA-7B layer shape: 32 heads x 128, fp16 KV in 16-token
 blocks with permuted block tables, one prefix group of 32 requests sharing a
 2048-token prefix, own lengths U[64,512].  Steps cycle through `--layers`
 layers with distinct KV values, all resident in HBM, so a layer's KV is not
-still in the 256 MB Infinity Cache when it is read again.
+still in the 256 MB Infinity Cache when it is read again.  A multi-layer
+workload (`--config c5`: 32 LLaMA-7B layers) cycles through all of its own
+layers instead, and a step is one layer of it.
 
 Prints one JSON line.  `value` is requests per second per layer
 (R / seconds per step).  The `roofline` object describes the dominant kernel
 (the partial-result kernel) from HIP events attached to its launches on the
-launch stream during the timed steps; `cpu_baseline` times the float64 CPU oracle on a bounded sample
-of the same workload.
+launch stream during the timed steps, and `ceilings` holds a plain device copy
+measured in the same process; `cpu_baseline` times the float64 CPU oracle on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -104,6 +107,24 @@ def cpu_baseline(plan, layer_dev, budget_s: float):
     }
 
 
+def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
+    """Read + write GB/s of a plain device-to-device copy (a ceiling for
+    bandwidth-bound kernels on this device, measured in the same process)."""
+    src = torch.ones(mib << 19, dtype=torch.float16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    gbps = 2 * reps * src.numel() * 2 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
 def traffic_from_counters(plan_key: str):
     """HBM bytes per partial-result launch from committed rocprofv3 counter runs,
     only if they were taken on the current kernel source."""
@@ -153,11 +174,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     cfg = get_config(args.config)
-    if cfg.layers != 1:
-        raise SystemExit(f"{cfg.name} has {cfg.layers} layers; bench one-layer workloads")
     plan = make_plan(cfg)
     dev = "cuda"
-    layers = [make_device_layer(plan, l, dev, seed=cfg.seed) for l in range(args.layers)]
+    # A multi-layer workload cycles through all of its layers (each with its
+    # own KV, all resident); a one-layer workload cycles --layers distinct-KV
+    # copies so that every call reads cold HBM.
+    n_layers = cfg.layers if cfg.layers > 1 else args.layers
+    layers = [make_device_layer(plan, l, dev, seed=cfg.seed) for l in range(n_layers)]
+    copy_gbps = copy_ceiling(torch)
     prob = problem_from_host(
         num_heads=plan.heads, head_dim=plan.head_dim, block_size=plan.block_size,
         dtype=TORCH_DTYPES[plan.dtype], sm_scale=plan.sm_scale, group_ids=plan.group_ids,
@@ -172,7 +196,7 @@ def main():
     dec = Decoder(prob, device=dev)
     stream = torch.cuda.current_stream()
     ab = algorithmic_bytes(plan)
-    K, W, L = args.steps, args.warmup, args.layers
+    K, W, L = args.steps, args.warmup, n_layers
 
     names = ("partials", "merge")
 
@@ -228,7 +252,8 @@ def main():
             "prefix_lens": [int(x) for x in plan.prefix_lens],
             "suffix_len_mean": round(float(plan.suffix_lens.mean()), 1),
             "kv_block": plan.block_size, "kv_dtype": DTYPE_TAG[plan.dtype],
-            "layers_cycled": L, "timing": "HBM-resident inputs, distinct KV per cycled layer",
+            "layers": cfg.layers, "layers_cycled": L,
+            "timing": "HBM-resident inputs, distinct KV per cycled layer",
         },
         "hbm_gbps": round(ab["shared_total"] / (wall / K) / 1e9, 1),
     }
@@ -248,12 +273,22 @@ def main():
         }
         result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
         result["kernels_us"]["traced_steps"] = per["traced_steps"]
-        result["prefix_mfma"] = {
-            "flops": ab["prefix_flops"],
-            "tflops_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12, 2),
-            "util_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12
-                                               / MFMA_F16_PEAK_TFLOPS, 5),
+        result["ceilings"] = {
+            "copy_gbps": round(copy_gbps, 1),
+            "note": "device-to-device copy of 1 GiB in this process, read + write bytes per second",
+            "partials_frac_of_copy": round(achieved / copy_gbps, 4),
         }
+        if ab["prefix_flops"] > 0:
+            intensity = ab["prefix_flops"] / ab["prefix_kv"]
+            result["prefix_mfma"] = {
+                "flops": ab["prefix_flops"],
+                "flop_per_byte": round(intensity, 2),
+                "tflops_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12, 2),
+                "util_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12
+                                                   / MFMA_F16_PEAK_TFLOPS, 5),
+                "util_ceiling_at_hbm_peak": round(min(1.0, intensity * HBM_PEAK_GBPS / 1e3
+                                                      / MFMA_F16_PEAK_TFLOPS), 5),
+            }
     if not args.no_baselines:
         wall_n, _ = run(shared=False, trace=False)
         result["per_request_baseline"] = {
