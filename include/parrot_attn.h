@@ -103,8 +103,11 @@ typedef struct {
 } parrot_trace;
 
 /* Bytes of device workspace either decode entry point needs for `p`
- * (0 when R = 0).  Returns (size_t)-1 if `p` is invalid; the reason is then
- * in parrot_last_error(). */
+ * (0 when R = 0).  The prefix chunk, and with it the workspace size, depends
+ * on the compute-unit count of the current HIP device, so ask with the device
+ * current that the calls will run on (a call with a smaller workspace fails
+ * with PARROT_ERR_WORKSPACE_TOO_SMALL).  Returns (size_t)-1 if `p` is invalid;
+ * the reason is then in parrot_last_error(). */
 size_t parrot_workspace_bytes(const parrot_problem* p);
 
 /*
@@ -116,8 +119,8 @@ size_t parrot_workspace_bytes(const parrot_problem* p);
  *        against them on MFMA with an online softmax; one partial result per
  *        member is written to the workspace;
  *      - split-KV: each request's own tokens, split into equal runs of
- *        16-token blocks over a fixed grid, with 128-bit coalesced loads; one
- *        partial per (request, head) piece;
+ *        16-token blocks over a fixed grid, with 128-bit coalesced streaming
+ *        loads; one partial per (request, head) piece;
  *   2. the merge kernel: log-sum-exp combination of all partials of (r, h).
  *
  *   q                    [R][H][D] dtype, 16-byte aligned
