@@ -7,7 +7,8 @@ it; the library path never calls it and has no CPU fallback.
 What it computes (Section 5.3, "Sharing Prompt Prefix", and Section 7,
 "Kernel Optimization"): decode-phase softmax attention of one query per request
 over that request's whole context, i.e. the shared prefix of its group followed
-by its own non-shared tokens, with keys and values read from a paged KV cache
+by its own non-shared tokens (or, with nested groups, the prefixes of the
+group's ancestors first), with keys and values read from a paged KV cache
 through block tables.  The paper's two-stage kernel reaches exactly this result
 (up to rounding order), so the oracle is the plain definition written out, in
 float64, per request and per head, with no blocking, splitting or fusion.
@@ -25,11 +26,12 @@ from .attention import (
     attend,
     merge_segments,
     softmax_weights,
+    group_chain,
     request_kv,
     shared_prefix_decode,
 )
 
 __all__ = [
     "to_f64", "gather_sequence", "attend", "merge_segments", "softmax_weights",
-    "request_kv", "shared_prefix_decode",
+    "group_chain", "request_kv", "shared_prefix_decode",
 ]

@@ -19,6 +19,14 @@ and does not restate it, so the standard definition is written out here):
   PagedAttention): token t of a sequence with block table row ``tbl`` lives at
   pool[tbl[t // B], h, t % B, :] of a [num_blocks, H, B, D] pool.
 
+  Nested prefixes: a prompt can share prefixes at several depths (a prefix
+  hash is taken after every semantic variable, Section 5.3, and a context can
+  be forked from a forked context through parent_context_id, Section 7).  With
+  prefix_parents[g] naming the group whose prefix precedes group g's (-1 for
+  none), a request of group g reads the prefixes of g's ancestors, outermost
+  first, then g's own prefix, then its own tokens.  Without prefix_parents
+  every group stands alone.
+
 All inputs are upcast exactly to float64 before any arithmetic.
 """
 from __future__ import annotations
@@ -112,27 +120,45 @@ def merge_segments(parts: Iterable[tuple]) -> tuple:
     return o, l
 
 
+def group_chain(g: int, prefix_parents=None) -> list:
+    """The groups whose prefixes a request of group g reads, outermost first."""
+    if g < 0:
+        return []
+    if prefix_parents is None:
+        return [g]
+    parents = _ints(prefix_parents)
+    chain = [g]
+    while parents[chain[-1]] >= 0:
+        if len(chain) > len(parents):
+            raise ValueError("prefix_parents contains a cycle")
+        chain.append(int(parents[chain[-1]]))
+    return chain[::-1]
+
+
 def request_kv(r: int, *, prefix_k, prefix_v, suffix_k, suffix_v,
-               prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids):
-    """Keys and values of request r: its group's prefix, then its own suffix."""
+               prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids,
+               prefix_parents=None):
+    """Keys and values of request r: the prefixes of its group's chain, then
+    its own suffix."""
     g = int(_ints(group_ids)[r])
     S = int(_ints(suffix_lens)[r])
     stab = _ints(suffix_tables)[r]
-    Ks = gather_sequence(suffix_k, stab, S)
-    Vs = gather_sequence(suffix_v, stab, S)
-    if g < 0:
-        return Ks, Vs
-    P = int(_ints(prefix_lens)[g])
-    ptab = _ints(prefix_tables)[g]
-    Kp = gather_sequence(prefix_k, ptab, P)
-    Vp = gather_sequence(prefix_v, ptab, P)
-    return np.concatenate([Kp, Ks]), np.concatenate([Vp, Vs])
+    Ks = [gather_sequence(suffix_k, stab, S)]
+    Vs = [gather_sequence(suffix_v, stab, S)]
+    Kp, Vp = [], []
+    for a in group_chain(g, prefix_parents):
+        P = int(_ints(prefix_lens)[a])
+        ptab = _ints(prefix_tables)[a]
+        Kp.append(gather_sequence(prefix_k, ptab, P))
+        Vp.append(gather_sequence(prefix_v, ptab, P))
+    return np.concatenate(Kp + Ks), np.concatenate(Vp + Vs)
 
 
 def shared_prefix_decode(q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_tables,
                          prefix_lens, suffix_tables, suffix_lens, group_ids,
-                         sm_scale: float, requests: Optional[Sequence[int]] = None):
-    """Naive per-request decode attention over concat(prefix, suffix).
+                         sm_scale: float, requests: Optional[Sequence[int]] = None,
+                         prefix_parents=None):
+    """Naive per-request decode attention over concat(prefixes, suffix).
 
     Returns (out [n, H, D], lse [n, H]) in float64 for the requests listed in
     ``requests`` (all requests, in order, by default).
@@ -148,7 +174,8 @@ def shared_prefix_decode(q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_table
         K, V = request_kv(r, prefix_k=prefix_k, prefix_v=prefix_v, suffix_k=suffix_k,
                           suffix_v=suffix_v, prefix_tables=prefix_tables,
                           prefix_lens=prefix_lens, suffix_tables=suffix_tables,
-                          suffix_lens=suffix_lens, group_ids=group_ids)
+                          suffix_lens=suffix_lens, group_ids=group_ids,
+                          prefix_parents=prefix_parents)
         if K.shape[0] == 0:
             raise ValueError(f"request {r} has an empty context")
         out[i], lse[i] = attend(qf[r], K, V, sm_scale)

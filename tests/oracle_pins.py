@@ -28,6 +28,8 @@ def decode_args(batch, **over):
                 prefix_tables=p.prefix_tables, prefix_lens=p.prefix_lens,
                 suffix_tables=p.suffix_tables, suffix_lens=p.suffix_lens,
                 group_ids=p.group_ids, sm_scale=p.sm_scale)
+    if p.nested:
+        args["prefix_parents"] = p.prefix_parents
     args.update(over)
     return args
 
@@ -46,6 +48,29 @@ def c1_batch():
     return make_batch(make_plan(get_config("tiny")))
 
 
+def tiny_nested_batch(seed=4, dtype="float32", block_size=4, aligned=False):
+    """Three levels of groups (0; 1 and 2 under 0; 3 under 1) with requests at
+    every level, one ungrouped request, paged and shuffled.  With `aligned`,
+    the prefixes that have descendants fill whole blocks."""
+    rng = np.random.default_rng(seed)
+    lens = [8, 4, 9, 3] if aligned else [7, 5, 9, 3]
+    plan = build_plan(heads=2, head_dim=8, block_size=block_size, dtype=dtype,
+                      group_of_request=[3, 3, 1, 2, 0, -1, 2, 3],
+                      prefix_lens=lens, prefix_parents=[-1, 0, 0, 1],
+                      suffix_lens=[2, 0, 5, 1, 4, 6, 0, 9],
+                      sm_scale=1.0 / math.sqrt(8.0), paged=True, shuffle=True, rng=rng)
+    return make_batch(plan, seed=seed)
+
+
+def _walk_up(parents, g):
+    """Brute-force chain: the groups from the outermost ancestor down to g."""
+    out = []
+    while g >= 0:
+        out.insert(0, int(g))
+        g = int(parents[g])
+    return out
+
+
 # ---------------------------------------------------------------- brute force
 def brute_force(batch):
     """Pure-Python loops, math.exp without max shift, own index arithmetic."""
@@ -57,9 +82,8 @@ def brute_force(batch):
     R, H, D = len(q), p.heads, p.head_dim
     outs, lses = [], []
     for r in range(R):
-        keys = []   # (block, slot) of every key, prefix first
-        g = int(p.group_ids[r])
-        if g >= 0:
+        keys = []   # (block, slot) of every key, prefixes first
+        for g in _walk_up(p.prefix_parents, int(p.group_ids[r])):
             for t in range(int(p.prefix_lens[g])):
                 keys.append((int(p.prefix_tables[g][t // B]), t % B))
         for t in range(int(p.suffix_lens[r])):
@@ -273,6 +297,72 @@ def pin_decomposition(decode, merge):
         _close(l, whole[1][r], 1e-13, 1e-13, f"decomposition lse {r}")
 
 
+def pin_nested_brute_force(decode):
+    for batch in (tiny_nested_batch(), tiny_nested_batch(seed=6, block_size=16)):
+        out, lse = decode(**decode_args(batch))
+        bo, bl = brute_force(batch)
+        _close(out, bo, 1e-12, 1e-13, "nested brute force out")
+        _close(lse, bl, 1e-12, 1e-13, "nested brute force lse")
+
+
+def pin_nested_zero_query(decode):
+    """q = 0: lse = ln N with N the chain's prefix tokens plus the own tokens."""
+    batch = tiny_nested_batch()
+    p = batch.plan
+    out, lse = decode(**decode_args(batch, q=torch.zeros_like(batch.q)))
+    B = p.block_size
+    v = batch.v_pool.double()
+    for r in range(p.num_requests):
+        acc = torch.zeros(p.heads, p.head_dim, dtype=torch.float64)
+        n = 0
+        for g in _walk_up(p.prefix_parents, int(p.group_ids[r])):
+            for t in range(int(p.prefix_lens[g])):
+                acc += v[int(p.prefix_tables[g][t // B]), :, t % B, :]
+                n += 1
+        for t in range(int(p.suffix_lens[r])):
+            acc += v[int(p.suffix_tables[r][t // B]), :, t % B, :]
+            n += 1
+        _close(lse[r], np.full(p.heads, math.log(n)), 0, 1e-13, f"nested zero-query lse {r}")
+        _close(out[r], (acc / n).numpy(), 1e-12, 1e-13, f"nested zero-query out {r}")
+
+
+def pin_nested_flatten(decode):
+    """Nested groups with whole-block ancestor prefixes equal flat groups whose
+    tables are the chains' tables laid end to end."""
+    from workloads.gen import flatten_nested
+    batch = tiny_nested_batch(aligned=True)
+    flat = flatten_nested(batch.plan)
+    a = decode(**decode_args(batch))
+    fb = type(batch)(plan=flat, q=batch.q, k_pool=batch.k_pool, v_pool=batch.v_pool)
+    b = decode(**decode_args(fb))
+    _close(a[0], b[0], 1e-13, 1e-14, "nested vs flattened out")
+    _close(a[1], b[1], 1e-14, 1e-14, "nested vs flattened lse")
+
+
+def pin_nested_spike(decode):
+    """A dominant key at every level boundary of the chain."""
+    batch = tiny_nested_batch()
+    p = batch.plan
+    B = p.block_size
+    for r in range(p.num_requests):
+        locs = []
+        for g in _walk_up(p.prefix_parents, int(p.group_ids[r])):
+            P = int(p.prefix_lens[g])
+            for t in sorted({0, P - 1}):
+                locs.append((int(p.prefix_tables[g][t // B]), t % B))
+        S = int(p.suffix_lens[r])
+        for t in sorted({0, S - 1} if S else set()):
+            locs.append((int(p.suffix_tables[r][t // B]), t % B))
+        for blk, slot in locs:
+            h = 1
+            k = batch.k_pool.clone()
+            qv = batch.q[r, h].double()
+            k[blk, h, slot, :] = (40.0 / (p.sm_scale * float(qv @ qv)) * qv).to(k.dtype)
+            out, lse = decode(**decode_args(batch, prefix_k=k, suffix_k=k), requests=[r])
+            _close(out[0, h], batch.v_pool[blk, h, slot].double().numpy(), 0, 1e-9,
+                   f"nested spike r={r} block={blk} slot={slot}")
+
+
 ALL_PINS = {
     "worked_example": pin_worked_example,
     "brute_force": pin_brute_force,
@@ -282,4 +372,8 @@ ALL_PINS = {
     "single_identical": pin_single_and_identical_keys,
     "scale": pin_scale,
     "layout_invariance": pin_layout_invariance,
+    "nested_brute_force": pin_nested_brute_force,
+    "nested_zero_query": pin_nested_zero_query,
+    "nested_flatten": pin_nested_flatten,
+    "nested_spike": pin_nested_spike,
 }

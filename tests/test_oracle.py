@@ -12,12 +12,35 @@ import pytest
 
 import oracle
 import oracle.attention as oa
+import oracle_pins as pins
 from oracle_pins import ALL_PINS, GOLDEN, pin_decomposition, tiny_paged_batch, decode_args
 
 
 @pytest.mark.parametrize("name", sorted(ALL_PINS))
 def test_oracle_pin(name):
     ALL_PINS[name](oracle.shared_prefix_decode)
+
+
+def test_oracle_nested_decomposition():
+    """Each chain level alone and the own tokens alone, merged, equal the
+    whole nested context."""
+    b = pins.tiny_nested_batch()
+    p = b.plan
+    whole = oracle.shared_prefix_decode(**pins.decode_args(b))
+    for r in range(p.num_requests):
+        parts = []
+        for g in pins._walk_up(p.prefix_parents, int(p.group_ids[r])):
+            gid = np.full_like(p.group_ids, -1)
+            gid[r] = g
+            parts.append(oracle.shared_prefix_decode(
+                **pins.decode_args(b, group_ids=gid, suffix_lens=np.zeros_like(p.suffix_lens),
+                                   prefix_parents=None), requests=[r]))
+        if p.suffix_lens[r] > 0:
+            parts.append(oracle.shared_prefix_decode(
+                **pins.decode_args(b, group_ids=np.full_like(p.group_ids, -1)), requests=[r]))
+        o, l = oracle.merge_segments([(x[0][0], x[1][0]) for x in parts])
+        np.testing.assert_allclose(o, whole[0][r], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(l, whole[1][r], rtol=1e-13, atol=1e-13)
 
 
 def test_oracle_decomposition_invariant():
@@ -157,7 +180,7 @@ def _mut_wrong_group(monkeypatch):
 def _mut_suffix_from_offset(monkeypatch):
     """Suffix read as if it continued the prefix's token numbering."""
     def f(r, *, prefix_k, prefix_v, suffix_k, suffix_v, prefix_tables, prefix_lens,
-          suffix_tables, suffix_lens, group_ids):
+          suffix_tables, suffix_lens, group_ids, prefix_parents=None):
         g = int(np.asarray(group_ids)[r])
         S = int(np.asarray(suffix_lens)[r])
         P = int(np.asarray(prefix_lens)[g]) if g >= 0 else 0
@@ -195,6 +218,33 @@ def _mut_prefix_ignored(monkeypatch):
     monkeypatch.setattr(oa, "request_kv", f)
 
 
+def _mut_chain_leaf_only(monkeypatch):
+    monkeypatch.setattr(oa, "group_chain", lambda g, parents=None: [g] if g >= 0 else [])
+
+
+def _mut_chain_root_only(monkeypatch):
+    real = oa.group_chain
+    monkeypatch.setattr(oa, "group_chain", lambda g, parents=None: real(g, parents)[:1])
+
+
+def _mut_chain_leaf_twice(monkeypatch):
+    real = oa.group_chain
+
+    def f(g, parents=None):
+        c = real(g, parents)
+        return c + c[-1:] if len(c) > 1 else c
+    monkeypatch.setattr(oa, "group_chain", f)
+
+
+def _mut_chain_skips_middle(monkeypatch):
+    real = oa.group_chain
+
+    def f(g, parents=None):
+        c = real(g, parents)
+        return [c[0], c[-1]] if len(c) > 2 else c
+    monkeypatch.setattr(oa, "group_chain", f)
+
+
 MUTANTS = {
     "drop_last_key": _mut_drop_last,
     "gather_slot_shift": _mut_gather_slot_shift,
@@ -208,6 +258,10 @@ MUTANTS = {
     "suffix_from_offset": _mut_suffix_from_offset,
     "head_shift": _mut_head_shift,
     "prefix_ignored": _mut_prefix_ignored,
+    "chain_leaf_only": _mut_chain_leaf_only,
+    "chain_root_only": _mut_chain_root_only,
+    "chain_leaf_twice": _mut_chain_leaf_twice,
+    "chain_skips_middle": _mut_chain_skips_middle,
 }
 
 

@@ -93,4 +93,32 @@ def test_dtype_cast_is_round_to_nearest_even():
 
 def test_aliases_cover_all_configs():
     assert sorted(ALIASES.values()) == sorted(["tiny", "llama7b_g32_p2048", "sysprompt_g64_p6000",
-                                               "mapreduce_13b_4x32", "mixed_7b_32layer"])
+                                               "mapreduce_13b_4x32", "mixed_7b_32layer",
+                                               "nested_sys6000_8x8_fs256"])
+
+
+def test_nested_plan_chains_and_flattening():
+    from workloads.gen import flatten_nested
+    plan = make_plan(get_config("nested"))
+    assert plan.depth() == 2 and plan.nested
+    assert plan.reader_counts() == [64] + [8] * 8
+    for r in range(plan.num_requests):
+        g = int(plan.group_ids[r])
+        assert plan.chain(g) == [0, g] and g >= 1
+        assert plan.context_lens()[r] == 6000 + 256 + plan.suffix_lens[r]
+    flat = flatten_nested(plan)
+    assert not flat.nested and flat.num_groups == 8
+    assert np.array_equal(flat.context_lens(), plan.context_lens())
+    # the flat prefix of a request's group is its chain's blocks in order
+    B = plan.block_size
+    for r in range(plan.num_requests):
+        g, fg = int(plan.group_ids[r]), int(flat.group_ids[r])
+        want = list(plan.prefix_tables[0][:6000 // B]) + list(plan.prefix_tables[g][:256 // B])
+        assert list(flat.prefix_tables[fg][:len(want)]) == want
+
+
+def test_parents_must_point_to_lower_groups():
+    with pytest.raises(ValueError):
+        build_plan(heads=1, head_dim=64, block_size=16, dtype="float32", group_of_request=[0, 1],
+                   prefix_lens=[16, 16], suffix_lens=[1, 1], sm_scale=1.0,
+                   prefix_parents=[1, -1])

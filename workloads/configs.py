@@ -50,9 +50,10 @@ class ConfigSpec:
     head_dim: int
     block_size: int
     dtype: str                      # "float32" | "float16" | "bfloat16"
-    group_sizes: tuple              # members per prefix group
+    group_sizes: tuple              # requests whose own group is g
     prefix_len: tuple               # length recipe, one draw per group
     suffix_len: tuple               # length recipe, one draw per grouped request
+    prefix_parents: tuple = ()      # parent group per group (-1 = none); () = flat
     ungrouped: int = 0              # requests with no shared prefix
     ungrouped_len: tuple = ("fixed", 0)   # whole-context length recipe for them
     q_scale: float = 1.0            # q is drawn N(0,1) * q_scale
@@ -118,12 +119,23 @@ CONFIGS: dict[str, ConfigSpec] = {
         prefix_len=("uniform", 512, 4096), suffix_len=("uniform", 32, 1024),
         ungrouped=32, ungrouped_len=("sum_uniform", (512, 4096), (32, 1024)),
         sm_scale=_INV_SQRT128),
+    "nested_sys6000_8x8_fs256": ConfigSpec(
+        name="nested_sys6000_8x8_fs256",
+        description="two-level sharing, LLaMA-7B layer: 32 heads x 128, fp16 "
+                    "paged; a 6000-token system prompt (group 0) shared by 8 "
+                    "sub-groups, each adding a 256-token few-shot block and "
+                    "holding 8 requests; own tokens U[64,512]",
+        layers=1, heads=32, head_dim=128, block_size=16, dtype="float16",
+        group_sizes=(0,) + (8,) * 8, prefix_parents=(-1,) + (0,) * 8,
+        prefix_len=("list", [6000] + [256] * 8),
+        suffix_len=("uniform", 64, 512), sm_scale=_INV_SQRT128),
 }
 
 # Short aliases in the order the workloads are listed (C1..C5).
 ALIASES = {
     "c1": "tiny", "c2": "llama7b_g32_p2048", "c3": "sysprompt_g64_p6000",
     "c4": "mapreduce_13b_4x32", "c5": "mixed_7b_32layer",
+    "nested": "nested_sys6000_8x8_fs256",
 }
 
 

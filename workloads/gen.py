@@ -9,6 +9,10 @@ Layout of a batch (the paged KV block layout of the library it feeds):
     S_r >= 0; its group id is g, or -1 when it shares no prefix (then the whole
     context is its suffix).  A request's keys are its group's P_g prefix tokens
     followed by its own S_r suffix tokens.
+  * Groups may nest: prefix_parents[g] is the group whose prefix precedes g's
+    (-1 for none), always a lower group number.  A request of group g then
+    reads the prefixes of g's ancestors, outermost first, then g's, then its
+    own tokens.  Flat workloads have every parent -1.
   * Unused token slots of a partly filled block are NaN, and unused block
     table entries point at one all-NaN "poison" block, so any read past a
     length shows up as NaN instead of a plausible number.
@@ -32,7 +36,7 @@ gigabytes would be too slow, and its values differ from the host recipe.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass
+from dataclasses import dataclass, replace
 from typing import Optional, Sequence
 
 import numpy as np
@@ -89,6 +93,33 @@ class LayoutPlan:
     suffix_tables: np.ndarray    # int32 [R, suffix_stride]
     block_fill: np.ndarray       # int32 [NB] valid token slots per physical block
     poison_block: int            # physical id of the all-NaN block
+    prefix_parents: Optional[np.ndarray] = None   # int32 [NG], -1 = outermost
+
+    def __post_init__(self):
+        if self.prefix_parents is None:
+            self.prefix_parents = np.full(self.num_groups, -1, dtype=np.int32)
+        par = np.asarray(self.prefix_parents, dtype=np.int32)
+        if par.shape != (self.num_groups,):
+            raise ValueError("one parent per group is required")
+        if np.any((par >= np.arange(self.num_groups)) | (par < -1)):
+            raise ValueError("a group's parent must be -1 or a lower group number")
+        self.prefix_parents = par
+
+    @property
+    def nested(self) -> bool:
+        return bool(np.any(self.prefix_parents >= 0))
+
+    def chain(self, g: int) -> list[int]:
+        """Groups whose prefixes a request of group g reads, outermost first."""
+        out = []
+        while g >= 0:
+            out.append(int(g))
+            g = int(self.prefix_parents[g])
+        return out[::-1]
+
+    def depth(self) -> int:
+        """Longest chain of groups (1 for flat groups, 0 without groups)."""
+        return max([0] + [len(self.chain(g)) for g in range(self.num_groups)])
 
     @property
     def num_requests(self) -> int:
@@ -103,13 +134,23 @@ class LayoutPlan:
         return int(self.block_fill.shape[0])
 
     def group_sizes(self) -> list[int]:
+        """Requests whose own group is g."""
         return [int((self.group_ids == g).sum()) for g in range(self.num_groups)]
 
+    def reader_counts(self) -> list[int]:
+        """Requests that read group g's prefix (g's members and its descendants')."""
+        n = [0] * self.num_groups
+        for g in self.group_ids:
+            for a in self.chain(int(g)):
+                n[a] += 1
+        return n
+
+    def chain_prefix_len(self, g: int) -> int:
+        return int(sum(int(self.prefix_lens[a]) for a in self.chain(g)))
+
     def context_lens(self) -> np.ndarray:
-        """P_{g(r)} + S_r for every request."""
-        p = np.where(self.group_ids >= 0,
-                     self.prefix_lens[np.maximum(self.group_ids, 0)] if self.num_groups
-                     else 0, 0)
+        """Prefix tokens along the request's chain plus S_r, for every request."""
+        p = np.array([self.chain_prefix_len(int(g)) for g in self.group_ids], dtype=np.int64)
         return (p + self.suffix_lens).astype(np.int64)
 
 
@@ -117,10 +158,12 @@ def build_plan(*, heads: int, head_dim: int, block_size: int, dtype: str,
                group_of_request: Sequence[int], prefix_lens: Sequence[int],
                suffix_lens: Sequence[int], sm_scale: float, q_scale: float = 1.0,
                paged: bool = True, shuffle: bool = False,
-               rng: Optional[np.random.Generator] = None) -> LayoutPlan:
+               rng: Optional[np.random.Generator] = None,
+               prefix_parents: Optional[Sequence[int]] = None) -> LayoutPlan:
     """Allocate blocks and tables for explicit lengths.
 
-    ``group_of_request``, ``suffix_lens`` are in pre-shuffle request order.
+    ``group_of_request``, ``suffix_lens`` are in pre-shuffle request order;
+    ``prefix_parents`` (default: all -1) nests groups.
     """
     B = int(block_size)
     gor = np.asarray(group_of_request, dtype=np.int64)
@@ -175,7 +218,8 @@ def build_plan(*, heads: int, head_dim: int, block_size: int, dtype: str,
         prefix_lens=plen.astype(np.int32),
         suffix_lens=slen[order].astype(np.int32),
         prefix_tables=ptab, suffix_tables=stab[order].copy(),
-        block_fill=block_fill, poison_block=poison)
+        block_fill=block_fill, poison_block=poison,
+        prefix_parents=None if prefix_parents is None else np.asarray(prefix_parents, np.int32))
 
 
 def make_plan(cfg: ConfigSpec) -> LayoutPlan:
@@ -190,7 +234,42 @@ def make_plan(cfg: ConfigSpec) -> LayoutPlan:
     return build_plan(heads=cfg.heads, head_dim=cfg.head_dim, block_size=cfg.block_size,
                       dtype=cfg.dtype, group_of_request=gor, prefix_lens=plen,
                       suffix_lens=slen, sm_scale=cfg.sm_scale, q_scale=cfg.q_scale,
-                      paged=cfg.paged, shuffle=cfg.shuffle_requests, rng=rng)
+                      paged=cfg.paged, shuffle=cfg.shuffle_requests, rng=rng,
+                      prefix_parents=cfg.prefix_parents or None)
+
+
+def flatten_nested(plan: LayoutPlan) -> LayoutPlan:
+    """The same batch with one flat group per group that has members: its
+    prefix is the concatenation of its chain's prefixes (same physical blocks).
+
+    Only defined when every ancestor prefix fills whole blocks (otherwise the
+    concatenated token numbering would not match the block tables).  Used to
+    run the flat entry points on a nested workload, as baselines.
+    """
+    B = plan.block_size
+    leaders = [g for g in range(plan.num_groups) if np.any(plan.group_ids == g)]
+    for g in leaders:
+        for a in plan.chain(g)[:-1]:
+            if int(plan.prefix_lens[a]) % B:
+                raise ValueError(f"group {a}: prefix length {int(plan.prefix_lens[a])} "
+                                 f"is not a multiple of the block size {B}")
+    rows, lens = [], []
+    for g in leaders:
+        row = []
+        for a in plan.chain(g):
+            n = -(-int(plan.prefix_lens[a]) // B)
+            row += [int(x) for x in plan.prefix_tables[a][:n]]
+        rows.append(row)
+        lens.append(plan.chain_prefix_len(g))
+    stride = max([1] + [len(r) for r in rows])
+    ptab = np.full((len(leaders), stride), plan.poison_block, dtype=np.int32)
+    for i, row in enumerate(rows):
+        ptab[i, :len(row)] = row
+    remap = {g: i for i, g in enumerate(leaders)}
+    gid = np.array([remap.get(int(g), -1) if g >= 0 else -1 for g in plan.group_ids],
+                   dtype=np.int32)
+    return replace(plan, group_ids=gid, prefix_lens=np.asarray(lens, dtype=np.int32),
+                   prefix_tables=ptab, prefix_parents=None)
 
 
 @dataclass
@@ -209,7 +288,7 @@ class DecodeBatch:
         p = self.plan
         return dict(prefix_tables=p.prefix_tables, prefix_lens=p.prefix_lens,
                     suffix_tables=p.suffix_tables, suffix_lens=p.suffix_lens,
-                    group_ids=p.group_ids)
+                    group_ids=p.group_ids, prefix_parents=p.prefix_parents)
 
     def to(self, device) -> dict:
         """Tensors of this batch on ``device`` (int arrays as int32 tensors)."""
