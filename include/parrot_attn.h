@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 1
+#define PARROT_ABI_VERSION 2
 
 typedef enum {
   PARROT_OK = 0,
@@ -87,6 +87,11 @@ typedef struct {
   int32_t num_suffix_blocks;   /* blocks in the suffix pools (>= 1) */
   parrot_dtype dtype;          /* element type of q, the KV pools and out */
   float sm_scale;              /* logits are sm_scale * q.k; finite */
+  int32_t max_prefix_depth;    /* nested groups: >= the longest chain of groups,
+                                  in [0, 4] (0 and 1 mean flat groups); sizes the
+                                  workspace.  With nested groups, max_group_size
+                                  bounds the requests that read any one group's
+                                  prefix (its members and its descendants'). */
 } parrot_problem;
 
 /* Optional timing hooks: hipEvent_t handles (each may be NULL), created by the
@@ -172,6 +177,35 @@ parrot_status parrot_per_request_decode(
     void* stream, const parrot_trace* trace);
 
 /*
+ * Nested shared-prefix decode attention: several levels of shared prefixes
+ * (Section 5.3: a prompt's prefix hash is taken after every semantic variable,
+ * so one prompt can share a system prompt with many requests and a longer
+ * prefix with fewer; Section 7: contexts fork from forked contexts through
+ * parent_context_id).  Groups form a forest given by
+ *   prefix_parents       int32 [NG]: the group whose prefix precedes group g's,
+ *                        or -1; always lower than g, so chains end; a chain
+ *                        holds at most max_prefix_depth groups.
+ * A request of group g attends to the prefixes of g's ancestors, outermost
+ * first, then g's prefix, then its own tokens.  Every group's prefix is read
+ * once per call, for all requests below it.  Other arguments as
+ * parrot_shared_prefix_decode (requests may belong to any group of a chain,
+ * or to none); with every parent -1 the result is that of
+ * parrot_shared_prefix_decode.
+ */
+parrot_status parrot_nested_prefix_decode(
+    const parrot_problem* p,
+    const void* q,
+    const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* prefix_parents,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
+    void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/*
  * Checks the device-side contents against `p` (a debugging aid; it
  * synchronises `stream`): group ids in [-1, NG), prefix lengths in
  * [1, max_prefix_len], suffix lengths in [0, max_suffix_len], P + S >= 1,
@@ -182,6 +216,15 @@ parrot_status parrot_per_request_decode(
 parrot_status parrot_validate_inputs(
     const parrot_problem* p,
     const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, int32_t* scratch, void* stream);
+
+/* parrot_validate_inputs for nested groups: also checks that every parent is
+ * in [-1, g) and that no chain holds more than max_prefix_depth groups. */
+parrot_status parrot_validate_nested_inputs(
+    const parrot_problem* p,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* prefix_parents,
     const int32_t* suffix_block_tables, const int32_t* suffix_lens,
     const int32_t* group_ids, int32_t* scratch, void* stream);
 

@@ -13,9 +13,11 @@ from .binding import (  # noqa: F401
     make_problem,
     parrot_abi_version,
     parrot_last_error,
+    parrot_nested_prefix_decode,
     parrot_per_request_decode,
     parrot_shared_prefix_decode,
     parrot_validate_inputs,
+    parrot_validate_nested_inputs,
     parrot_workspace_bytes,
     problem_from_host,
 )

@@ -47,6 +47,7 @@ class ParrotProblem(ctypes.Structure):
         ("num_suffix_blocks", ctypes.c_int32),
         ("dtype", ctypes.c_int),
         ("sm_scale", ctypes.c_float),
+        ("max_prefix_depth", ctypes.c_int32),
     ]
 
 
@@ -61,7 +62,8 @@ class ParrotTrace(ctypes.Structure):
 
 EXPORTED = (
     "parrot_workspace_bytes", "parrot_shared_prefix_decode", "parrot_per_request_decode",
-    "parrot_validate_inputs", "parrot_last_error", "parrot_abi_version",
+    "parrot_nested_prefix_decode", "parrot_validate_inputs", "parrot_validate_nested_inputs",
+    "parrot_last_error", "parrot_abi_version",
 )
 
 _lib: Optional[ctypes.CDLL] = None
@@ -86,8 +88,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = dec_args
         f.restype = ctypes.c_int
+    lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
+    lib.parrot_nested_prefix_decode.restype = ctypes.c_int
     lib.parrot_validate_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, vp, vp]
     lib.parrot_validate_inputs.restype = ctypes.c_int
+    lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p, vp, vp]
+    lib.parrot_validate_nested_inputs.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []
@@ -106,12 +112,14 @@ def parrot_abi_version() -> int:
 
 def make_problem(*, num_requests, num_heads, head_dim, block_size, num_groups, max_group_size,
                  max_prefix_len, max_suffix_len, prefix_table_stride, suffix_table_stride,
-                 num_prefix_blocks, num_suffix_blocks, dtype, sm_scale) -> ParrotProblem:
+                 num_prefix_blocks, num_suffix_blocks, dtype, sm_scale,
+                 max_prefix_depth=0) -> ParrotProblem:
     code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
     return ParrotProblem(int(num_requests), int(num_heads), int(head_dim), int(block_size),
                          int(num_groups), int(max_group_size), int(max_prefix_len),
                          int(max_suffix_len), int(prefix_table_stride), int(suffix_table_stride),
-                         int(num_prefix_blocks), int(num_suffix_blocks), code, float(sm_scale))
+                         int(num_prefix_blocks), int(num_suffix_blocks), code, float(sm_scale),
+                         int(max_prefix_depth))
 
 
 def parrot_workspace_bytes(problem: ParrotProblem) -> int:
@@ -142,14 +150,16 @@ def _stream_handle(stream) -> Optional[int]:
 
 def _decode(fn_name, problem, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
             prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
-            stream=None, trace: Optional[ParrotTrace] = None):
+            stream=None, trace: Optional[ParrotTrace] = None, prefix_parents=None):
     lib = load_library()
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    parents = (_ptr(prefix_parents),) if fn_name == "parrot_nested_prefix_decode" else ()
     status = getattr(lib, fn_name)(
         ctypes.byref(problem), _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(suffix_k),
-        _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(suffix_block_tables),
-        _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes,
-        _stream_handle(stream), ctypes.byref(trace) if trace is not None else None)
+        _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), *parents,
+        _ptr(suffix_block_tables), _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse),
+        _ptr(workspace), ws_bytes, _stream_handle(stream),
+        ctypes.byref(trace) if trace is not None else None)
     _check(status)
 
 
@@ -173,6 +183,27 @@ def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v
             out, lse, workspace, stream, trace)
 
 
+def parrot_nested_prefix_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+                                prefix_block_tables, prefix_lens, prefix_parents,
+                                suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+                                stream=None, trace=None):
+    """Shared-prefix decode attention with nested groups (see the C header)."""
+    _decode("parrot_nested_prefix_decode", problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+            prefix_block_tables, prefix_lens, suffix_block_tables, suffix_lens, group_ids,
+            out, lse, workspace, stream, trace, prefix_parents=prefix_parents)
+
+
+def parrot_validate_nested_inputs(problem, prefix_block_tables, prefix_lens, prefix_parents,
+                                  suffix_block_tables, suffix_lens, group_ids, scratch,
+                                  stream=None):
+    """Device-side content check including the group parents (synchronises)."""
+    lib = load_library()
+    _check(lib.parrot_validate_nested_inputs(
+        ctypes.byref(problem), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(prefix_parents),
+        _ptr(suffix_block_tables), _ptr(suffix_lens), _ptr(group_ids), _ptr(scratch),
+        _stream_handle(stream)))
+
+
 def parrot_validate_inputs(problem, prefix_block_tables, prefix_lens, suffix_block_tables,
                            suffix_lens, group_ids, scratch, stream=None):
     """Device-side content check (synchronises the stream)."""
@@ -185,26 +216,36 @@ def parrot_validate_inputs(problem, prefix_block_tables, prefix_lens, suffix_blo
 
 def problem_from_host(*, num_heads, head_dim, block_size, dtype, sm_scale, group_ids, prefix_lens,
                       suffix_lens, prefix_table_stride, suffix_table_stride, num_prefix_blocks,
-                      num_suffix_blocks) -> ParrotProblem:
+                      num_suffix_blocks, prefix_parents=None) -> ParrotProblem:
     """Fill a ParrotProblem from host copies of the batch metadata.
 
-    ``group_ids``, ``prefix_lens`` and ``suffix_lens`` are host sequences; only
-    their sizes and maxima are used (the serving engine knows them on the host).
+    ``group_ids``, ``prefix_lens``, ``suffix_lens`` (and, for nested groups,
+    ``prefix_parents``) are host sequences; only their sizes, maxima and the
+    group chains are used (the serving engine knows them on the host).
     """
     import numpy as np
     gid = np.asarray(group_ids)
     plen = np.asarray(prefix_lens)
     slen = np.asarray(suffix_lens)
     ng = int(plen.shape[0])
-    sizes = np.bincount(gid[gid >= 0], minlength=max(ng, 1)) if gid.size else np.zeros(1, int)
+    readers = np.zeros(max(ng, 1), dtype=np.int64)
+    depth = 1 if ng else 0
+    par = None if prefix_parents is None else np.asarray(prefix_parents)
+    for g in gid:
+        n, x = 0, int(g)
+        while x >= 0:
+            readers[x] += 1
+            n += 1
+            x = int(par[x]) if par is not None else -1
+        depth = max(depth, n)
     return make_problem(
         num_requests=gid.shape[0], num_heads=num_heads, head_dim=head_dim,
-        block_size=block_size, num_groups=ng, max_group_size=int(sizes.max()) if ng else 0,
+        block_size=block_size, num_groups=ng, max_group_size=int(readers.max()) if ng else 0,
         max_prefix_len=int(plen.max()) if ng else 0,
         max_suffix_len=int(slen.max()) if slen.size else 0,
         prefix_table_stride=prefix_table_stride, suffix_table_stride=suffix_table_stride,
         num_prefix_blocks=num_prefix_blocks, num_suffix_blocks=num_suffix_blocks,
-        dtype=dtype, sm_scale=sm_scale)
+        dtype=dtype, sm_scale=sm_scale, max_prefix_depth=depth if par is not None else 0)
 
 
 class Decoder:
@@ -221,27 +262,40 @@ class Decoder:
         nbytes = parrot_workspace_bytes(problem)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
 
-    def bind(self, t: dict, shared: bool = True, stream=None):
+    @staticmethod
+    def _entry(shared: bool, nested: bool) -> str:
+        if nested:
+            if not shared:
+                raise ValueError("nested groups have no per-request entry point")
+            return "parrot_nested_prefix_decode"
+        return "parrot_shared_prefix_decode" if shared else "parrot_per_request_decode"
+
+    def bind(self, t: dict, shared: bool = True, stream=None, nested: bool = False):
         """Marshal the arguments once; the returned callable re-issues the same
-        call (same tensors, stream and buffers) with only the optional trace."""
+        call (same tensors, stream and buffers) with only the optional trace.
+        ``nested`` calls the nested-group entry point with t["prefix_parents"]."""
         lib = load_library()
-        fn = getattr(lib, "parrot_shared_prefix_decode" if shared else "parrot_per_request_decode")
+        name = self._entry(shared, nested)
+        fn = getattr(lib, name)
         pk = t.get("prefix_k", t.get("k_pool")); pv = t.get("prefix_v", t.get("v_pool"))
         sk = t.get("suffix_k", t.get("k_pool")); sv = t.get("suffix_v", t.get("v_pool"))
         ws = self.workspace
+        parents = (_ptr(t["prefix_parents"]),) if nested else ()
         args = (ctypes.byref(self.problem), _ptr(t["q"]), _ptr(pk), _ptr(pv), _ptr(sk), _ptr(sv),
-                _ptr(t["prefix_tables"]), _ptr(t["prefix_lens"]), _ptr(t["suffix_tables"]),
-                _ptr(t["suffix_lens"]), _ptr(t["group_ids"]), _ptr(self.out), _ptr(self.lse),
-                _ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream))
+                _ptr(t["prefix_tables"]), _ptr(t["prefix_lens"]), *parents,
+                _ptr(t["suffix_tables"]), _ptr(t["suffix_lens"]), _ptr(t["group_ids"]),
+                _ptr(self.out), _ptr(self.lse), _ptr(ws), ws.numel() * ws.element_size(),
+                _stream_handle(stream))
 
         def call(trace: Optional[ParrotTrace] = None):
             _check(fn(*args, ctypes.byref(trace) if trace is not None else None))
         return call
 
-    def __call__(self, t: dict, shared: bool = True, stream=None, trace=None):
-        fn = parrot_shared_prefix_decode if shared else parrot_per_request_decode
-        fn(self.problem, t["q"], t.get("prefix_k", t.get("k_pool")), t.get("prefix_v", t.get("v_pool")),
-           t.get("suffix_k", t.get("k_pool")), t.get("suffix_v", t.get("v_pool")),
-           t["prefix_tables"], t["prefix_lens"], t["suffix_tables"], t["suffix_lens"],
-           t["group_ids"], self.out, self.lse, self.workspace, stream=stream, trace=trace)
+    def __call__(self, t: dict, shared: bool = True, stream=None, trace=None, nested: bool = False):
+        _decode(self._entry(shared, nested), self.problem, t["q"],
+                t.get("prefix_k", t.get("k_pool")), t.get("prefix_v", t.get("v_pool")),
+                t.get("suffix_k", t.get("k_pool")), t.get("suffix_v", t.get("v_pool")),
+                t["prefix_tables"], t["prefix_lens"], t["suffix_tables"], t["suffix_lens"],
+                t["group_ids"], self.out, self.lse, self.workspace, stream=stream, trace=trace,
+                prefix_parents=t.get("prefix_parents") if nested else None)
         return self.out, self.lse

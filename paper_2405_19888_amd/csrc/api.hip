@@ -118,6 +118,10 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
 
   if (p->num_requests > parrot::kMaxRequests)
     return fail(PARROT_ERR_UNSUPPORTED, "num_requests %d > %d per call", p->num_requests, parrot::kMaxRequests);
+  if (p->max_prefix_depth < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_prefix_depth %d < 0", p->max_prefix_depth);
+  if (p->max_prefix_depth > parrot::kMaxDepth)
+    return fail(PARROT_ERR_UNSUPPORTED, "max_prefix_depth %d > %d", p->max_prefix_depth, parrot::kMaxDepth);
+  pl->depth = p->num_groups > 0 ? std::max(1, (int)p->max_prefix_depth) : 0;
   const long mg = p->num_groups > 0 ? p->max_group_size : 1;
   pl->prefix_waves = 4;
   pl->prefix_qtiles = (int)ceil_div(mg, 16 * pl->prefix_waves);
@@ -131,8 +135,12 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   const long pieces_shared = nbs_max > 0 ? ceil_div(nbs_max, pl->skv_min_q) + 1 : 0;
   const long pieces_naive = ceil_div(nbp_max + nbs_max, pl->skv_min_q) + 1;
   pl->seg_p = p->num_groups > 0 ? (int)ceil_div(p->max_prefix_len, pl->cp) : 0;
+  if (pl->seg_p > 0xFFFF)
+    return fail(PARROT_ERR_UNSUPPORTED, "max_prefix_len %d needs %d prefix chunks (at most 65535)",
+                p->max_prefix_len, pl->seg_p);
+  pl->seg_pre = pl->depth * pl->seg_p;
   pl->seg_s = (int)pieces_shared;
-  const long seg = std::max<long>(pl->seg_p + pieces_shared, pieces_naive);
+  const long seg = std::max<long>(pl->seg_pre + pieces_shared, pieces_naive);
   pl->seg = (int)seg;
   pl->skv_waves = 0;   // set at launch from the device's CU count
 
@@ -145,7 +153,7 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
   pl->lse_bytes = align256(n_slots * sizeof(float));
-  pl->info_bytes = align256((size_t)p->num_requests * 2 * sizeof(int32_t));
+  pl->info_bytes = align256((size_t)p->num_requests * parrot::kMetaInts * sizeof(int32_t));
   pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes + pl->info_bytes : 0;
   return PARROT_OK;
 }
@@ -164,11 +172,13 @@ parrot_status launched(hipError_t e, const char* what) {
 
 #define PARROT_TRY(x) do { parrot_status _s = (x); if (_s != PARROT_OK) return _s; } while (0)
 
+// shared: prefix-group role for the prefixes (else the split-KV role reads
+// them per request); parents: nested groups (shared path only; NULL = flat).
 parrot_status decode(bool shared, const parrot_problem* p, const void* q, const void* prefix_k,
                      const void* prefix_v, const void* suffix_k, const void* suffix_v,
-                     const int32_t* ptab, const int32_t* plen, const int32_t* stab,
-                     const int32_t* slen, const int32_t* gid, void* out, float* lse,
-                     void* workspace, size_t workspace_bytes, void* stream,
+                     const int32_t* ptab, const int32_t* plen, const int32_t* parents,
+                     const int32_t* stab, const int32_t* slen, const int32_t* gid, void* out,
+                     float* lse, void* workspace, size_t workspace_bytes, void* stream,
                      const parrot_trace* trace) {
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
@@ -211,12 +221,14 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     parrot::SplitKVArgs& a = pa.skv;
     a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
     a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
+    a.parents = shared ? parents : nullptr;
+    a.depth = parents ? pl.depth : 1;
     a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
     a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
     a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
     a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
-    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0; a.cp = pl.cp;
+    a.seg = pl.seg; a.seg_pre = shared ? pl.seg_pre : 0; a.cp = pl.cp;
     a.with_prefix = shared ? 0 : 1;
     // a fixed grid of split-KV workgroups per CU, at least one wave per head
     pa.n_skv = num_cus() * kSplitkvWgsPerCu;
@@ -227,6 +239,8 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     if (run_prefix) {
       parrot::PrefixArgs& b = pa.pre;
       b.q = q; b.pk = prefix_k; b.pv = prefix_v; b.ptab = ptab; b.plen = plen; b.gid = gid;
+      b.parents = parents;
+      b.depth = parents ? pl.depth : 1;
       b.o_part = o_part; b.lse_part = lse_part;
       b.R = p->num_requests; b.H = p->num_heads; b.NG = p->num_groups;
       b.pstride = p->prefix_table_stride; b.max_p = p->max_prefix_len; b.npblk = p->num_prefix_blocks;
@@ -242,7 +256,7 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.out = out; a.lse = lse;
     a.R = p->num_requests; a.H = p->num_heads;
-    a.seg = pl.seg; a.seg_p = shared ? pl.seg_p : 0;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.seg_pre = shared ? pl.seg_pre : 0;
     PARROT_TRY(launched(parrot::launch_merge(a, dt, D, s, ev(tr.merge_start), ev(tr.merge_stop)),
                         "merge kernel"));
   }
@@ -268,8 +282,8 @@ parrot_status parrot_shared_prefix_decode(
     const int32_t* group_ids, void* out, float* lse, void* workspace, size_t workspace_bytes,
     void* stream, const parrot_trace* trace) {
   return decode(true, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
-                prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
-                workspace_bytes, stream, trace);
+                prefix_lens, nullptr, suffix_block_tables, suffix_lens, group_ids, out, lse,
+                workspace, workspace_bytes, stream, trace);
 }
 
 parrot_status parrot_per_request_decode(
@@ -279,14 +293,34 @@ parrot_status parrot_per_request_decode(
     const int32_t* group_ids, void* out, float* lse, void* workspace, size_t workspace_bytes,
     void* stream, const parrot_trace* trace) {
   return decode(false, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
-                prefix_lens, suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+                prefix_lens, nullptr, suffix_block_tables, suffix_lens, group_ids, out, lse,
+                workspace, workspace_bytes, stream, trace);
+}
+
+parrot_status parrot_nested_prefix_decode(
+    const parrot_problem* p, const void* q, const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v, const int32_t* prefix_block_tables,
+    const int32_t* prefix_lens, const int32_t* prefix_parents, const int32_t* suffix_block_tables,
+    const int32_t* suffix_lens, const int32_t* group_ids, void* out, float* lse, void* workspace,
+    size_t workspace_bytes, void* stream, const parrot_trace* trace) {
+  if (p && p->num_requests > 0 && p->num_groups > 0) {
+    if (!prefix_parents) return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_parents is NULL");
+    if (!aligned(prefix_parents, 4)) return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_parents is not 4-byte aligned");
+  }
+  return decode(true, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+                prefix_lens, p && p->num_groups > 0 ? prefix_parents : nullptr,
+                suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
                 workspace_bytes, stream, trace);
 }
 
-parrot_status parrot_validate_inputs(const parrot_problem* p, const int32_t* prefix_block_tables,
-                                     const int32_t* prefix_lens, const int32_t* suffix_block_tables,
-                                     const int32_t* suffix_lens, const int32_t* group_ids,
-                                     int32_t* scratch, void* stream) {
+}  // extern "C"
+
+namespace {
+
+parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tables,
+                       const int32_t* prefix_lens, const int32_t* prefix_parents,
+                       const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+                       const int32_t* group_ids, int32_t* scratch, void* stream) {
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
   if (p->num_requests == 0) { g_err.clear(); return PARROT_OK; }
@@ -301,6 +335,8 @@ parrot_status parrot_validate_inputs(const parrot_problem* p, const int32_t* pre
   parrot::ValidateArgs a{};
   a.ptab = prefix_block_tables; a.plen = prefix_lens; a.stab = suffix_block_tables;
   a.slen = suffix_lens; a.gid = group_ids; a.result = scratch;
+  a.parents = p->num_groups > 0 ? prefix_parents : nullptr;
+  a.depth = std::max(1, (int)p->max_prefix_depth);
   a.R = p->num_requests; a.NG = p->num_groups; a.B = p->block_size;
   a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
   a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
@@ -313,12 +349,37 @@ parrot_status parrot_validate_inputs(const parrot_problem* p, const int32_t* pre
   static const char* what[] = {"", "group id out of [-1, num_groups)", "prefix length out of [1, max_prefix_len]",
                                "suffix length out of [0, max_suffix_len]", "empty context (prefix + suffix = 0)",
                                "prefix block id out of [0, num_prefix_blocks)",
-                               "suffix block id out of [0, num_suffix_blocks)"};
+                               "suffix block id out of [0, num_suffix_blocks)",
+                               "prefix parent not in [-1, group)",
+                               "prefix chain deeper than max_prefix_depth"};
   if (res[0] != 0)
     return fail(PARROT_ERR_INVALID_ARGUMENT, "%s at entry %d (value %d)",
-                (res[0] > 0 && res[0] <= 6) ? what[res[0]] : "unknown", res[1], res[2]);
+                (res[0] > 0 && res[0] <= 8) ? what[res[0]] : "unknown", res[1], res[2]);
   g_err.clear();
   return PARROT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+parrot_status parrot_validate_inputs(const parrot_problem* p, const int32_t* prefix_block_tables,
+                                     const int32_t* prefix_lens, const int32_t* suffix_block_tables,
+                                     const int32_t* suffix_lens, const int32_t* group_ids,
+                                     int32_t* scratch, void* stream) {
+  return validate(p, prefix_block_tables, prefix_lens, nullptr, suffix_block_tables, suffix_lens,
+                  group_ids, scratch, stream);
+}
+
+parrot_status parrot_validate_nested_inputs(const parrot_problem* p, const int32_t* prefix_block_tables,
+                                            const int32_t* prefix_lens, const int32_t* prefix_parents,
+                                            const int32_t* suffix_block_tables,
+                                            const int32_t* suffix_lens, const int32_t* group_ids,
+                                            int32_t* scratch, void* stream) {
+  if (p && p->num_requests > 0 && p->num_groups > 0 && !prefix_parents)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_parents is NULL");
+  return validate(p, prefix_block_tables, prefix_lens, prefix_parents, suffix_block_tables,
+                  suffix_lens, group_ids, scratch, stream);
 }
 
 const char* parrot_last_error(void) { return g_err.c_str(); }

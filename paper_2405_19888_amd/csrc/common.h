@@ -17,16 +17,20 @@ constexpr float kLn2 = 0.6931471805599453f;
 // Partial results live in the workspace as
 //   o_part  [R][H][seg][D] float32   (normalised partial output of one piece)
 //   lse_part[R][H][seg]    float32   (base-2 log-sum-exp of the piece's scaled logits)
-//   merge_meta[R][2]       int32     (per request: prefix-chunk slots, split-KV pieces)
-// Slots [0, seg_p) hold the prefix-group kernel's chunks (chunk c covers prefix
-// tokens [c*cp, (c+1)*cp)); slots [seg_p, seg) hold split-KV pieces.  The
+//   merge_meta[R][4]       int32     (per request: split-KV pieces, prefix levels,
+//                                     prefix-chunk slots per level, 16 bits each)
+// Slots [l*seg_p, l*seg_p + seg_p) hold the prefix-group chunks of the group
+// at level l of the request's chain (chunk c covers that prefix's tokens
+// [c*cp, (c+1)*cp); level 0 is the outermost group, and flat groups use level
+// 0 only); slots [seg_pre, seg) hold split-KV pieces, seg_pre = depth * seg_p.  The
 // split-KV kernel sees every request's blocks (own tokens, preceded by its
 // group's prefix on the per-request path) as one flat list ordered by
 // (request, head, block) and gives each wave an equal run of it; piece p of
 // sequence (r, h) is the part that the p-th wave touching that sequence owns.
 struct Plan {
   int cp;                // prefix chunk tokens (prefix-group kernel)
-  int seg_p, seg_s, seg; // slots per (request, head)
+  int depth;             // prefix levels (1 for flat groups)
+  int seg_p, seg_pre, seg_s, seg; // slots per (request, head)
   int prefix_waves;      // waves per prefix-kernel workgroup (16 queries each)
   int prefix_qtiles;     // query tiles per group
   int skv_waves;         // split-KV grid, in waves
@@ -35,6 +39,8 @@ struct Plan {
 };
 
 constexpr int kMaxRequests = 1024;   // per call (split-KV keeps per-request data in LDS)
+constexpr int kMaxDepth = 4;         // prefix levels of nested groups
+constexpr int kMetaInts = 4;         // merge_meta ints per request
 
 struct SplitKVArgs {
   const void* q;
@@ -43,13 +49,15 @@ struct SplitKVArgs {
   const int* ptab; const int* plen;
   const int* stab; const int* slen;
   const int* gid;
+  const int* parents;    // nested groups (NULL: flat)
   float* o_part; float* lse_part;
   int* merge_meta;       // written by split-KV workgroup 0 for the merge
   int R, H, NG;
   int pstride, sstride;
   int max_p, max_s;
   int npblk, nsblk;
-  int seg, seg_p, cp;
+  int seg, seg_pre, cp;
+  int depth;             // prefix levels walked for the merge descriptor
   int with_prefix;       // 1: each sequence is the group prefix, then the own tokens
   int nwaves;            // waves launched
   int min_q;             // blocks per wave >= min_q
@@ -60,6 +68,8 @@ struct PrefixArgs {
   const void* q;
   const void* pk; const void* pv;
   const int* ptab; const int* plen; const int* gid;
+  const int* parents;    // nested groups (NULL: flat)
+  int depth;             // prefix levels (1: flat)
   float* o_part; float* lse_part;
   int R, H, NG;
   int pstride, max_p, npblk;
@@ -73,11 +83,13 @@ struct MergeArgs {
   const int* merge_meta;
   void* out; float* lse;
   int R, H;
-  int seg, seg_p;
+  int seg, seg_p, seg_pre;   // slots per sequence, per prefix level, before the pieces
 };
 
 struct ValidateArgs {
   const int* ptab; const int* plen; const int* stab; const int* slen; const int* gid;
+  const int* parents;    // nested groups (NULL: flat)
+  int depth;             // prefix levels allowed (nested)
   int* result;           // [0] = error code, [1] = index, [2] = value
   int R, NG, B;
   int pstride, sstride, max_p, max_s, npblk, nsblk;

@@ -36,9 +36,14 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   if (w >= (long)a.R * a.H) return;
   const int r = (int)(w / a.H);
   const int h = (int)(w % a.H);
-  const int2 meta = *reinterpret_cast<const int2*>(a.merge_meta + 2 * r);
-  const int np = meta.x;                    // prefix-chunk slots [0, np)
-  const int n = np + meta.y;                // then split-KV pieces from seg_p on
+  const int4 meta = *reinterpret_cast<const int4*>(a.merge_meta + kMetaInts * r);
+  const int nlev = meta.y;                  // prefix levels of the request's chain
+  const unsigned lo = (unsigned)meta.z, hi = (unsigned)meta.w;
+  int np[kMaxDepth] = {(int)(lo & 0xFFFFu), (int)(lo >> 16), (int)(hi & 0xFFFFu), (int)(hi >> 16)};
+#pragma unroll
+  for (int l = 0; l < kMaxDepth; ++l) np[l] = l < nlev ? np[l] : 0;
+  const int npre = np[0] + np[1] + np[2] + np[3];
+  const int n = npre + meta.x;              // prefix-chunk slots, then split-KV pieces
   const size_t base = (size_t)(r * a.H + h) * a.seg;
   char* outp = (char*)a.out + ((size_t)(r * a.H + h) * D + lane * EPL) * E::kBytes;
   if (n == 0) {  // empty context: defined as out = 0, lse = -inf
@@ -47,7 +52,16 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     if (lane == 0) a.lse[r * a.H + h] = -INFINITY;
     return;
   }
-  auto slot_of = [&](int i) { return i < np ? i : a.seg_p + (i - np); };
+  // i-th partial: the chunks of levels 0, 1, ... in turn, then the pieces
+  auto slot_of = [&](int i) {
+    int j = i;
+#pragma unroll
+    for (int l = 0; l < kMaxDepth; ++l) {
+      if (j < np[l]) return l * a.seg_p + j;
+      j -= np[l];
+    }
+    return a.seg_pre + j;
+  };
   auto load_o = [&](int i, float* v) {
     const float* src = a.o_part + (base + slot_of(i)) * D + lane * EPL;
     if constexpr (EPL == 2) {
@@ -138,6 +152,15 @@ PARROT_DEV void report(int* res, int code, int idx, int val) {
 
 __global__ __launch_bounds__(256) void k_validate(ValidateArgs a) {
   for (int g = threadIdx.x; g < a.NG; g += blockDim.x) {
+    if (a.parents) {
+      // parent in [-1, g): chains end; a chain of at most depth groups
+      const int par = a.parents[g];
+      if (par < -1 || par >= g) { report(a.result, 7, g, par); continue; }
+      // walk at most depth steps (another group's parent may be invalid too)
+      int n = 1;
+      for (int x = par; x >= 0 && x < a.NG && n <= a.depth; x = a.parents[x]) ++n;
+      if (n > a.depth) { report(a.result, 8, g, n); continue; }
+    }
     const int P = a.plen[g];
     if (P < 1 || P > a.max_p) { report(a.result, 2, g, P); continue; }
     for (int b = 0; b < (P + a.B - 1) / a.B; ++b) {

@@ -136,6 +136,15 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   const int g = wg / a.qtiles;
   if (g >= a.NG) return;
   const int P = clampi(a.plen[g], 0, a.max_p);
+  // level of g: its number of ancestors (at most depth - 1)
+  int lvl = 0;
+  if (a.parents) {
+    int x = a.parents[g];
+    while (x >= 0 && x < a.NG && lvl < a.depth - 1) {
+      ++lvl;
+      x = a.parents[x];
+    }
+  }
   const int t0 = c * a.cp;
   if (t0 >= P) return;
   const int t1 = min(P, t0 + a.cp);
@@ -150,7 +159,15 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
     int count = 0;
     for (int base = 0; base < a.R; base += kWave) {
       const int r = base + lane;
-      const bool is = r < a.R && a.gid[r] == g;
+      // r reads g's prefix when g is r's group or one of its ancestors
+      bool is = false;
+      if (r < a.R) {
+        int x = a.gid[r];
+        for (int d = 0; d < a.depth && x >= 0 && x < a.NG; ++d) {
+          if (x == g) { is = true; break; }
+          x = a.parents ? a.parents[x] : -1;
+        }
+      }
       const unsigned long long mask = __ballot(is);
       const int pos = count + __popcll(mask & ((1ull << lane) - 1ull));
       if (is && pos >= qbase && pos < qbase + W * 16) members[pos - qbase] = r;
@@ -375,7 +392,7 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   float lt = sum_xor16(lsum);
   lt = sum_xor32(lt);
   if (q_ok) {
-    const size_t slot = (size_t)(rq * H + h) * a.seg + c;
+    const size_t slot = (size_t)(rq * H + h) * a.seg + lvl * a.seg_p + c;
     const float inv = 1.f / lt;
     float* dst = a.o_part + slot * D + 4 * (lane >> 4);
 #pragma unroll

@@ -105,15 +105,27 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     // Merge descriptor of each request: how many prefix-chunk slots (shared
     // path: chunks of its group's prefix) and how many split-KV pieces (the
     // column groups its run of columns touches) hold its partial results.
+    // With nested groups, the request's chain is walked from its own group
+    // outwards (at most depth groups); level l counts from the outermost.
     for (int rr = threadIdx.x; rr < R; rr += blockDim.x) {
-      int np = 0;
+      int np[kMaxDepth] = {0, 0, 0, 0};
+      int nlev = 0;
       if (!a.with_prefix) {
-        const int g = a.gid[rr];
-        if (g >= 0 && g < a.NG) np = (clampi(a.plen[g], 0, a.max_p) + a.cp - 1) / a.cp;
+        int chain[kMaxDepth];
+        int x = a.gid[rr];
+        while (x >= 0 && x < a.NG && nlev < a.depth) {
+          chain[nlev++] = x;
+          x = a.parents ? a.parents[x] : -1;
+        }
+#pragma unroll
+        for (int i = 0; i < kMaxDepth; ++i)
+          if (i < nlev) np[nlev - 1 - i] = (clampi(a.plen[chain[i]], 0, a.max_p) + a.cp - 1) / a.cp;
       }
       const int first = s_excl[rr], n = s_cnt[rr];
       const int ns = n > 0 ? (first + n - 1) / Q - first / Q + 1 : 0;
-      *reinterpret_cast<int2*>(a.merge_meta + 2 * rr) = make_int2(np, ns);
+      *reinterpret_cast<int4*>(a.merge_meta + kMetaInts * rr) =
+          make_int4(ns, nlev, (int)((unsigned)np[0] | ((unsigned)np[1] << 16)),
+                    (int)((unsigned)np[2] | ((unsigned)np[3] << 16)));
     }
   }
   const int w = wg * kSkvWaves + wave_in_wg;
@@ -205,7 +217,7 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     }
     const int piece = grp - s_excl[seq / H] / Q;
     if (tg == 0) {
-      const size_t slot = (size_t)seq * a.seg + a.seg_p + piece;
+      const size_t slot = (size_t)seq * a.seg + a.seg_pre + piece;
       const float inv = 1.f / l;
       float* o = a.o_part + slot * D + sub * EPL;
 #pragma unroll

@@ -6,7 +6,8 @@ import numpy as np
 import torch
 
 import oracle
-from paper_2405_19888_amd import Decoder, parrot_validate_inputs, problem_from_host
+from paper_2405_19888_amd import (Decoder, parrot_validate_inputs, parrot_validate_nested_inputs,
+                                  problem_from_host)
 from workloads.gen import TORCH_DTYPES
 
 # Tolerances: max |out_gpu - out_ref| over all elements (fp32-accumulated
@@ -25,22 +26,31 @@ def problem_for(plan, num_prefix_blocks=None, num_suffix_blocks=None):
         prefix_table_stride=plan.prefix_tables.shape[1],
         suffix_table_stride=plan.suffix_tables.shape[1],
         num_prefix_blocks=num_prefix_blocks or plan.num_blocks,
-        num_suffix_blocks=num_suffix_blocks or plan.num_blocks)
+        num_suffix_blocks=num_suffix_blocks or plan.num_blocks,
+        prefix_parents=plan.prefix_parents if plan.nested else None)
 
 
 def run_gpu(plan, dev: dict, shared: bool = True, problem=None, poison: bool = True,
-            decoder: Decoder = None):
-    """Validate inputs on the device, poison outputs and workspace, run, sync."""
+            decoder: Decoder = None, nested: bool = None):
+    """Validate inputs on the device, poison outputs and workspace, run, sync.
+    Nested plans go through the nested-group entry point (unless `nested` is
+    False: then the groups are taken as flat)."""
+    nested = plan.nested if nested is None else nested
     prob = problem or problem_for(plan)
     dec = decoder or Decoder(prob)
     scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
-    parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
-                           dev["suffix_lens"], dev["group_ids"], scratch)
+    if nested:
+        parrot_validate_nested_inputs(prob, dev["prefix_tables"], dev["prefix_lens"],
+                                      dev["prefix_parents"], dev["suffix_tables"],
+                                      dev["suffix_lens"], dev["group_ids"], scratch)
+    else:
+        parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"],
+                               dev["suffix_tables"], dev["suffix_lens"], dev["group_ids"], scratch)
     if poison:
         dec.out.fill_(float("nan"))
         dec.lse.fill_(float("nan"))
         dec.workspace.fill_(0xFF)          # every float slot reads as NaN
-    out, lse = dec(dev, shared=shared)
+    out, lse = dec(dev, shared=shared, nested=nested)
     torch.cuda.synchronize()
     return out, lse
 
@@ -57,7 +67,7 @@ def oracle_for(batch_like, plan, requests=None, pools=None):
     return oracle.shared_prefix_decode(
         q.cpu() if isinstance(q, torch.Tensor) else q, kp, vp, kp, vp, plan.prefix_tables,
         plan.prefix_lens, plan.suffix_tables, plan.suffix_lens, plan.group_ids, plan.sm_scale,
-        requests=requests)
+        requests=requests, prefix_parents=plan.prefix_parents if plan.nested else None)
 
 
 def assert_close(out, lse, ref_out, ref_lse, dtype: str, what: str = ""):

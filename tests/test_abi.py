@@ -28,7 +28,7 @@ def test_exports_every_declared_symbol(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 1
+    assert B.parrot_abi_version() == 2
 
 
 def base_problem(**over):
@@ -41,7 +41,7 @@ def base_problem(**over):
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(B.ParrotProblem) == 14 * 4
+    assert ctypes.sizeof(B.ParrotProblem) == 15 * 4
     assert ctypes.sizeof(B.ParrotTrace) == 4 * ctypes.sizeof(ctypes.c_void_p)
 
 
@@ -74,6 +74,8 @@ def test_workspace_sizes(parrot_lib):
     (dict(sm_scale=float("nan")), B.PARROT_ERR_INVALID_ARGUMENT, "sm_scale"),
     (dict(num_groups=0, max_suffix_len=0, suffix_table_stride=0), B.PARROT_ERR_INVALID_ARGUMENT,
      "non-empty"),
+    (dict(max_prefix_depth=5), B.PARROT_ERR_UNSUPPORTED, "max_prefix_depth"),
+    (dict(max_prefix_depth=-1), B.PARROT_ERR_INVALID_ARGUMENT, "max_prefix_depth"),
 ])
 def test_bad_problem_rejected(parrot_lib, over, status, msg):
     with pytest.raises(B.ParrotError) as e:
@@ -90,6 +92,8 @@ FAKE = 1 << 20          # aligned fake device addresses: never dereferenced here
 
 def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
     names = ["q", "pk", "pv", "sk", "sv", "ptab", "plen", "stab", "slen", "gid", "out", "lse", "ws"]
+    if fn == "parrot_nested_prefix_decode":
+        names.insert(7, "parents")
     vals = {n: FAKE + 4096 * i for i, n in enumerate(names)}
     vals.update(ptrs)
     ws_bytes = ptrs.get("ws_bytes", 1 << 40)
@@ -97,11 +101,14 @@ def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
     return getattr(lib, fn)(ctypes.byref(prob), *[vals[n] for n in names], ws_bytes, None, None)
 
 
-@pytest.mark.parametrize("fn", ["parrot_shared_prefix_decode", "parrot_per_request_decode"])
+@pytest.mark.parametrize("fn", ["parrot_shared_prefix_decode", "parrot_per_request_decode",
+                                "parrot_nested_prefix_decode"])
 @pytest.mark.parametrize("field", ["q", "sk", "sv", "stab", "slen", "gid", "out", "lse", "ws",
-                                   "pk", "pv", "ptab", "plen"])
+                                   "pk", "pv", "ptab", "plen", "parents"])
 def test_null_pointer_rejected(parrot_lib, fn, field):
-    st = call(parrot_lib, base_problem(), fn, **{field: None})
+    if field == "parents" and fn != "parrot_nested_prefix_decode":
+        pytest.skip("only the nested entry point takes prefix_parents")
+    st = call(parrot_lib, base_problem(max_prefix_depth=2), fn, **{field: None})
     assert st == B.PARROT_ERR_INVALID_ARGUMENT
     assert "NULL" in B.parrot_last_error()
 
@@ -112,6 +119,25 @@ def test_misaligned_pointer_rejected(parrot_lib, field, off):
     st = call(parrot_lib, base_problem(), **{field: FAKE + off})
     assert st == B.PARROT_ERR_INVALID_ARGUMENT
     assert "aligned" in B.parrot_last_error()
+
+
+def test_nested_workspace_grows_with_depth(parrot_lib):
+    w1 = B.parrot_workspace_bytes(base_problem())
+    assert B.parrot_workspace_bytes(base_problem(max_prefix_depth=1)) == w1
+    w2 = B.parrot_workspace_bytes(base_problem(max_prefix_depth=2))
+    w4 = B.parrot_workspace_bytes(base_problem(max_prefix_depth=4))
+    # one slot stride serves both paths: the per-request path's pieces often
+    # dominate, so deeper nesting never shrinks the workspace
+    assert w1 <= w2 <= w4
+
+
+def test_nested_entry_checks_like_the_flat_one(parrot_lib):
+    prob = base_problem(max_prefix_depth=2)
+    need = B.parrot_workspace_bytes(prob)
+    st = call(parrot_lib, prob, "parrot_nested_prefix_decode", ws_bytes=need - 1)
+    assert st == B.PARROT_ERR_WORKSPACE_TOO_SMALL
+    st = call(parrot_lib, prob, "parrot_nested_prefix_decode", parents=FAKE + 2)
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT and "aligned" in B.parrot_last_error()
 
 
 def test_workspace_too_small(parrot_lib):
