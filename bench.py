@@ -64,7 +64,7 @@ def algorithmic_bytes(plan):
     prefix_kv = int(plan.prefix_lens.sum()) * kv_tok
     suffix_kv = int(plan.suffix_lens.sum()) * kv_tok
     naive_kv = int(plan.context_lens().sum()) * kv_tok
-    sizes = plan.group_sizes()
+    sizes = plan.reader_counts()      # requests that read each group's prefix
     prefix_flops = sum(4 * plan.head_dim * plan.heads * sizes[g] * int(plan.prefix_lens[g])
                        for g in range(plan.num_groups))
     return dict(prefix_kv=prefix_kv, suffix_kv=suffix_kv, q=q, out=out, lse=lse,
@@ -90,7 +90,8 @@ def cpu_baseline(plan, layer_dev, budget_s: float):
         r = int(order[done % plan.num_requests])
         oracle.shared_prefix_decode(q, kp, vp, kp, vp, plan.prefix_tables, plan.prefix_lens,
                                     plan.suffix_tables, plan.suffix_lens, plan.group_ids,
-                                    plan.sm_scale, requests=[r])
+                                    plan.sm_scale, requests=[r],
+                                    prefix_parents=plan.prefix_parents if plan.nested else None)
         done += 1
         wall = time.perf_counter() - t_wall0
         if wall >= budget_s:
@@ -160,8 +161,10 @@ def main():
                                    "(no multi-GPU path exists)"}))
         sys.exit(2)
 
+    import numpy as np
     import torch
-    from paper_2405_19888_amd import Decoder, ParrotTrace, parrot_validate_inputs, problem_from_host
+    from paper_2405_19888_amd import (Decoder, ParrotTrace, parrot_validate_inputs,
+                                      parrot_validate_nested_inputs, problem_from_host)
     from workloads import get_config, make_device_layer, make_plan
     from workloads.gen import TORCH_DTYPES
 
@@ -188,11 +191,17 @@ def main():
         prefix_lens=plan.prefix_lens, suffix_lens=plan.suffix_lens,
         prefix_table_stride=plan.prefix_tables.shape[1],
         suffix_table_stride=plan.suffix_tables.shape[1],
-        num_prefix_blocks=plan.num_blocks, num_suffix_blocks=plan.num_blocks)
+        num_prefix_blocks=plan.num_blocks, num_suffix_blocks=plan.num_blocks,
+        prefix_parents=plan.prefix_parents if plan.nested else None)
     scratch = torch.zeros(16, dtype=torch.int32, device=dev)
-    parrot_validate_inputs(prob, layers[0]["prefix_tables"], layers[0]["prefix_lens"],
-                           layers[0]["suffix_tables"], layers[0]["suffix_lens"],
-                           layers[0]["group_ids"], scratch)
+    t0 = layers[0]
+    if plan.nested:
+        parrot_validate_nested_inputs(prob, t0["prefix_tables"], t0["prefix_lens"],
+                                      t0["prefix_parents"], t0["suffix_tables"], t0["suffix_lens"],
+                                      t0["group_ids"], scratch)
+    else:
+        parrot_validate_inputs(prob, t0["prefix_tables"], t0["prefix_lens"], t0["suffix_tables"],
+                               t0["suffix_lens"], t0["group_ids"], scratch)
     dec = Decoder(prob, device=dev)
     stream = torch.cuda.current_stream()
     ab = algorithmic_bytes(plan)
@@ -200,10 +209,35 @@ def main():
 
     names = ("partials", "merge")
 
-    def run(shared: bool, trace: bool):
+    nested = plan.nested
+    flat_layers = flat_dec = None
+    if nested:
+        # baselines for nested groups: the flat entry points on the same blocks,
+        # each group's chain of prefixes laid end to end as one flat prefix
+        from workloads.gen import flatten_nested
+        flat = flatten_nested(plan)
+        ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+                for k, v in (("prefix_tables", flat.prefix_tables), ("prefix_lens", flat.prefix_lens),
+                             ("group_ids", flat.group_ids))}
+        flat_layers = [dict(t, **ints) for t in layers]
+        flat_dec = Decoder(problem_from_host(
+            num_heads=flat.heads, head_dim=flat.head_dim, block_size=flat.block_size,
+            dtype=TORCH_DTYPES[flat.dtype], sm_scale=flat.sm_scale, group_ids=flat.group_ids,
+            prefix_lens=flat.prefix_lens, suffix_lens=flat.suffix_lens,
+            prefix_table_stride=flat.prefix_tables.shape[1],
+            suffix_table_stride=flat.suffix_tables.shape[1],
+            num_prefix_blocks=flat.num_blocks, num_suffix_blocks=flat.num_blocks), device=dev)
+
+    def run(shared: bool, trace: bool, flat_baseline: bool = False):
         """W untimed steps, then K timed steps; every `trace_every`-th timed step
-        carries per-kernel (start, stop) event pairs when `trace` is set."""
-        calls = [dec.bind(layers[l], shared=shared, stream=stream) for l in range(L)]
+        carries per-kernel (start, stop) event pairs when `trace` is set.  For
+        nested groups, `flat_baseline` runs the flat entry points on the
+        flattened groups."""
+        if nested and (flat_baseline or not shared):
+            calls = [flat_dec.bind(flat_layers[l], shared=shared, stream=stream) for l in range(L)]
+        else:
+            calls = [dec.bind(layers[l], shared=shared, stream=stream, nested=nested)
+                     for l in range(L)]
         every = max(1, args.trace_every)
         traced = list(range(0, K, every)) if trace else []
         events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in traced}
@@ -249,6 +283,7 @@ def main():
         "config": {
             "workload": cfg.name, "requests": R, "heads": plan.heads, "head_dim": plan.head_dim,
             "prefix_groups": plan.num_groups, "group_sizes": plan.group_sizes(),
+            **({"prefix_parents": [int(x) for x in plan.prefix_parents]} if nested else {}),
             "prefix_lens": [int(x) for x in plan.prefix_lens],
             "suffix_len_mean": round(float(plan.suffix_lens.mean()), 1),
             "kv_block": plan.block_size, "kv_dtype": DTYPE_TAG[plan.dtype],
@@ -290,6 +325,17 @@ def main():
                                                       / MFMA_F16_PEAK_TFLOPS), 5),
             }
     if not args.no_baselines:
+        if nested:
+            wall_f, _ = run(shared=True, trace=False, flat_baseline=True)
+            flat_bytes = (int(flat.prefix_lens.sum()) * 2 * plan.heads * plan.head_dim
+                          * ELT_BYTES[plan.dtype] + ab["shared_total"] - ab["prefix_kv"])
+            result["flat_sharing_baseline"] = {
+                "value": round(R / (wall_f / K), 1), "unit": "req/s",
+                "ms_per_step": round(wall_f / K * 1e3, 5),
+                "speedup_of_nested": round(wall_f / wall, 3),
+                "hbm_gbps": round(flat_bytes / (wall_f / K) / 1e9, 1),
+                "note": "parrot_shared_prefix_decode with each group's prefix chain as one flat prefix",
+            }
         wall_n, _ = run(shared=False, trace=False)
         result["per_request_baseline"] = {
             "value": round(R / (wall_n / K), 1), "unit": "req/s",

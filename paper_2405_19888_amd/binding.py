@@ -88,12 +88,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = dec_args
         f.restype = ctypes.c_int
-    lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
-    lib.parrot_nested_prefix_decode.restype = ctypes.c_int
+    if hasattr(lib, "parrot_nested_prefix_decode"):      # absent from ABI 1 builds
+        lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
+        lib.parrot_nested_prefix_decode.restype = ctypes.c_int
     lib.parrot_validate_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, vp, vp]
     lib.parrot_validate_inputs.restype = ctypes.c_int
-    lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p, vp, vp]
-    lib.parrot_validate_nested_inputs.restype = ctypes.c_int
+    if hasattr(lib, "parrot_validate_nested_inputs"):
+        lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p,
+                                                      vp, vp]
+        lib.parrot_validate_nested_inputs.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []

@@ -42,8 +42,9 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   int np[kMaxDepth] = {(int)(lo & 0xFFFFu), (int)(lo >> 16), (int)(hi & 0xFFFFu), (int)(hi >> 16)};
 #pragma unroll
   for (int l = 0; l < kMaxDepth; ++l) np[l] = l < nlev ? np[l] : 0;
-  const int npre = np[0] + np[1] + np[2] + np[3];
-  const int n = npre + meta.x;              // prefix-chunk slots, then split-KV pieces
+  // partial i of the request: level 0's chunks, level 1's, ..., then the pieces
+  const int b1 = np[0], b2 = b1 + np[1], b3 = b2 + np[2], b4 = b3 + np[3];
+  const int n = b4 + meta.x;
   const size_t base = (size_t)(r * a.H + h) * a.seg;
   char* outp = (char*)a.out + ((size_t)(r * a.H + h) * D + lane * EPL) * E::kBytes;
   if (n == 0) {  // empty context: defined as out = 0, lse = -inf
@@ -52,18 +53,18 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     if (lane == 0) a.lse[r * a.H + h] = -INFINITY;
     return;
   }
-  // i-th partial: the chunks of levels 0, 1, ... in turn, then the pieces
-  auto slot_of = [&](int i) {
-    int j = i;
-#pragma unroll
-    for (int l = 0; l < kMaxDepth; ++l) {
-      if (j < np[l]) return l * a.seg_p + j;
-      j -= np[l];
-    }
-    return a.seg_pre + j;
+  auto slot_of = [&](int i) {               // selects only, so loads unroll freely
+    int sl = a.seg_pre + (i - b4);
+    sl = i < b4 ? 3 * a.seg_p + (i - b3) : sl;
+    sl = i < b3 ? 2 * a.seg_p + (i - b2) : sl;
+    sl = i < b2 ? a.seg_p + (i - b1) : sl;
+    return i < b1 ? i : sl;
   };
+  // lane i holds the slot of partial i; the first 64 are broadcast by readlane
+  const int slot_lane = slot_of(lane);
+  auto slot_bcast = [&](int i) { return i < kWave ? __builtin_amdgcn_readlane(slot_lane, i) : slot_of(i); };
   auto load_o = [&](int i, float* v) {
-    const float* src = a.o_part + (base + slot_of(i)) * D + lane * EPL;
+    const float* src = a.o_part + (base + slot_bcast(i)) * D + lane * EPL;
     if constexpr (EPL == 2) {
       const float2 x = *reinterpret_cast<const float2*>(src);
       v[0] = x.x; v[1] = x.y;
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   };
 
   // round 1: every lane's lse slot and the first batch of outputs together
-  const float l_lane = lane < n ? a.lse_part[base + slot_of(lane)] : -INFINITY;
+  const float l_lane = lane < n ? a.lse_part[base + slot_lane] : -INFINITY;
   float v[kBatch][EPL];
 #pragma unroll
   for (int u = 0; u < kBatch; ++u) load_o(min(u, n - 1), v[u]);
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     for (int u = 0; u < kBatch; ++u) {
       const int j = min(j0 + u, n - 1);
       load_o(j, v[u]);
-      wv[u] = a.lse_part[base + slot_of(j)];
+      wv[u] = a.lse_part[base + slot_bcast(j)];
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
