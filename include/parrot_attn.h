@@ -177,6 +177,34 @@ parrot_status parrot_per_request_decode(
     void* stream, const parrot_trace* trace);
 
 /*
+ * Shared-prefix decode attention that first appends this step's token (the
+ * engine's Generate step, Section 7: each iteration fills one more token into
+ * every request's context).  For every request with suffix_lens[r] >= 1, the
+ * token at own position S_r - 1 is the new one: its keys and values are read
+ * from
+ *   k_new, v_new         [R][H][D] dtype, 16-byte aligned
+ * and written into the suffix pools at slot
+ * suffix_block_tables[r][(S_r - 1) / B], offset (S_r - 1) % B (whatever that
+ * slot held before is ignored).  Requests with S_r = 0 append nothing.  The
+ * result equals writing the new tokens first and then calling
+ * parrot_shared_prefix_decode.  The written slot must belong to the request
+ * alone: not to another request's blocks nor to any group's prefix (the pools
+ * themselves may be the same tensors).  Other arguments as
+ * parrot_shared_prefix_decode.
+ */
+parrot_status parrot_shared_prefix_decode_append(
+    const parrot_problem* p,
+    const void* q, const void* k_new, const void* v_new,
+    const void* prefix_k, const void* prefix_v,
+    void* suffix_k, void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
+    void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/*
  * Nested shared-prefix decode attention: several levels of shared prefixes
  * (Section 5.3: a prompt's prefix hash is taken after every semantic variable,
  * so one prompt can share a system prompt with many requests and a longer

@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     parrot_nested_prefix_decode,
     parrot_per_request_decode,
     parrot_shared_prefix_decode,
+    parrot_shared_prefix_decode_append,
     parrot_validate_inputs,
     parrot_validate_nested_inputs,
     parrot_workspace_bytes,

@@ -62,8 +62,9 @@ class ParrotTrace(ctypes.Structure):
 
 EXPORTED = (
     "parrot_workspace_bytes", "parrot_shared_prefix_decode", "parrot_per_request_decode",
-    "parrot_nested_prefix_decode", "parrot_validate_inputs", "parrot_validate_nested_inputs",
-    "parrot_last_error", "parrot_abi_version",
+    "parrot_nested_prefix_decode", "parrot_shared_prefix_decode_append",
+    "parrot_validate_inputs", "parrot_validate_nested_inputs", "parrot_last_error",
+    "parrot_abi_version",
 )
 
 _lib: Optional[ctypes.CDLL] = None
@@ -88,6 +89,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = dec_args
         f.restype = ctypes.c_int
+    if hasattr(lib, "parrot_shared_prefix_decode_append"):   # absent from ABI 1 builds
+        lib.parrot_shared_prefix_decode_append.argtypes = dec_args[:2] + [vp, vp] + dec_args[2:]
+        lib.parrot_shared_prefix_decode_append.restype = ctypes.c_int
     if hasattr(lib, "parrot_nested_prefix_decode"):      # absent from ABI 1 builds
         lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
         lib.parrot_nested_prefix_decode.restype = ctypes.c_int
@@ -186,6 +190,22 @@ def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v
             out, lse, workspace, stream, trace)
 
 
+def parrot_shared_prefix_decode_append(problem, q, k_new, v_new, prefix_k, prefix_v, suffix_k,
+                                       suffix_v, prefix_block_tables, prefix_lens,
+                                       suffix_block_tables, suffix_lens, group_ids, out, lse,
+                                       workspace, stream=None, trace=None):
+    """Append this step's K/V (k_new, v_new) into the suffix pools, then
+    shared-prefix decode attention (see the C header)."""
+    lib = load_library()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.parrot_shared_prefix_decode_append(
+        ctypes.byref(problem), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(prefix_k), _ptr(prefix_v),
+        _ptr(suffix_k), _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens),
+        _ptr(suffix_block_tables), _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse),
+        _ptr(workspace), ws_bytes, _stream_handle(stream),
+        ctypes.byref(trace) if trace is not None else None))
+
+
 def parrot_nested_prefix_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
                                 prefix_block_tables, prefix_lens, prefix_parents,
                                 suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
@@ -266,26 +286,29 @@ class Decoder:
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
 
     @staticmethod
-    def _entry(shared: bool, nested: bool) -> str:
-        if nested:
-            if not shared:
-                raise ValueError("nested groups have no per-request entry point")
-            return "parrot_nested_prefix_decode"
+    def _entry(shared: bool, nested: bool, append: bool = False) -> str:
+        if nested or append:
+            if not shared or (nested and append):
+                raise ValueError("nested groups and appending have shared-path entry points only")
+            return "parrot_nested_prefix_decode" if nested else "parrot_shared_prefix_decode_append"
         return "parrot_shared_prefix_decode" if shared else "parrot_per_request_decode"
 
-    def bind(self, t: dict, shared: bool = True, stream=None, nested: bool = False):
+    def bind(self, t: dict, shared: bool = True, stream=None, nested: bool = False,
+             append: bool = False):
         """Marshal the arguments once; the returned callable re-issues the same
         call (same tensors, stream and buffers) with only the optional trace.
-        ``nested`` calls the nested-group entry point with t["prefix_parents"]."""
+        ``nested`` calls the nested-group entry point with t["prefix_parents"];
+        ``append`` the appending one with t["k_new"], t["v_new"]."""
         lib = load_library()
-        name = self._entry(shared, nested)
+        name = self._entry(shared, nested, append)
         fn = getattr(lib, name)
         pk = t.get("prefix_k", t.get("k_pool")); pv = t.get("prefix_v", t.get("v_pool"))
         sk = t.get("suffix_k", t.get("k_pool")); sv = t.get("suffix_v", t.get("v_pool"))
         ws = self.workspace
         parents = (_ptr(t["prefix_parents"]),) if nested else ()
-        args = (ctypes.byref(self.problem), _ptr(t["q"]), _ptr(pk), _ptr(pv), _ptr(sk), _ptr(sv),
-                _ptr(t["prefix_tables"]), _ptr(t["prefix_lens"]), *parents,
+        new_kv = (_ptr(t["k_new"]), _ptr(t["v_new"])) if append else ()
+        args = (ctypes.byref(self.problem), _ptr(t["q"]), *new_kv, _ptr(pk), _ptr(pv), _ptr(sk),
+                _ptr(sv), _ptr(t["prefix_tables"]), _ptr(t["prefix_lens"]), *parents,
                 _ptr(t["suffix_tables"]), _ptr(t["suffix_lens"]), _ptr(t["group_ids"]),
                 _ptr(self.out), _ptr(self.lse), _ptr(ws), ws.numel() * ws.element_size(),
                 _stream_handle(stream))
@@ -294,7 +317,11 @@ class Decoder:
             _check(fn(*args, ctypes.byref(trace) if trace is not None else None))
         return call
 
-    def __call__(self, t: dict, shared: bool = True, stream=None, trace=None, nested: bool = False):
+    def __call__(self, t: dict, shared: bool = True, stream=None, trace=None, nested: bool = False,
+                 append: bool = False):
+        if append:
+            self.bind(t, shared=shared, stream=stream, append=True)(trace)
+            return self.out, self.lse
         _decode(self._entry(shared, nested), self.problem, t["q"],
                 t.get("prefix_k", t.get("k_pool")), t.get("prefix_v", t.get("v_pool")),
                 t.get("suffix_k", t.get("k_pool")), t.get("suffix_v", t.get("v_pool")),

@@ -174,12 +174,15 @@ parrot_status launched(hipError_t e, const char* what) {
 
 // shared: prefix-group role for the prefixes (else the split-KV role reads
 // them per request); parents: nested groups (shared path only; NULL = flat).
+// k_new / v_new (both or neither): append this step's token to the suffix
+// pools (which are then written) while attending.
 parrot_status decode(bool shared, const parrot_problem* p, const void* q, const void* prefix_k,
                      const void* prefix_v, const void* suffix_k, const void* suffix_v,
                      const int32_t* ptab, const int32_t* plen, const int32_t* parents,
                      const int32_t* stab, const int32_t* slen, const int32_t* gid, void* out,
                      float* lse, void* workspace, size_t workspace_bytes, void* stream,
-                     const parrot_trace* trace) {
+                     const parrot_trace* trace, const void* k_new = nullptr,
+                     const void* v_new = nullptr) {
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -206,6 +209,13 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
       if (!aligned(r.ptr, r.align)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", r.name, r.align);
     }
   }
+  if (k_new || v_new) {
+    struct { const void* ptr; const char* name; } areq[] = {{k_new, "k_new"}, {v_new, "v_new"}};
+    for (auto& r : areq) {
+      if (!r.ptr) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", r.name);
+      if (!aligned(r.ptr, 16)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", r.name);
+    }
+  }
   if (workspace_bytes < pl.total_bytes)
     return fail(PARROT_ERR_WORKSPACE_TOO_SMALL, "workspace is %zu bytes, need %zu", workspace_bytes, pl.total_bytes);
 
@@ -223,6 +233,8 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
     a.parents = shared ? parents : nullptr;
     a.depth = parents ? pl.depth : 1;
+    a.k_new = k_new; a.v_new = v_new;
+    a.app_k = const_cast<void*>(suffix_k); a.app_v = const_cast<void*>(suffix_v);
     a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
     a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
@@ -295,6 +307,20 @@ parrot_status parrot_per_request_decode(
   return decode(false, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
                 prefix_lens, nullptr, suffix_block_tables, suffix_lens, group_ids, out, lse,
                 workspace, workspace_bytes, stream, trace);
+}
+
+parrot_status parrot_shared_prefix_decode_append(
+    const parrot_problem* p, const void* q, const void* k_new, const void* v_new,
+    const void* prefix_k, const void* prefix_v, void* suffix_k, void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens, const int32_t* group_ids,
+    void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream,
+    const parrot_trace* trace) {
+  if (p && p->num_requests > 0 && (!k_new || !v_new))
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", k_new ? "v_new" : "k_new");
+  return decode(true, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+                prefix_lens, nullptr, suffix_block_tables, suffix_lens, group_ids, out, lse,
+                workspace, workspace_bytes, stream, trace, k_new, v_new);
 }
 
 parrot_status parrot_nested_prefix_decode(

@@ -50,6 +50,9 @@ struct SplitKVArgs {
   const int* stab; const int* slen;
   const int* gid;
   const int* parents;    // nested groups (NULL: flat)
+  const void* k_new;     // this step's token per (request, head), or NULL
+  const void* v_new;
+  void* app_k; void* app_v;   // pools the new token is written to (suffix pools)
   float* o_part; float* lse_part;
   int* merge_meta;       // written by split-KV workgroup 0 for the merge
   int R, H, NG;
@@ -108,6 +111,7 @@ struct PartialsArgs {
 
 // Each launcher attaches the optional (start, stop) timing events to its kernel.
 hipError_t launch_partials(const PartialsArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// a.skv.k_new != NULL selects the kernel that also appends this step's token
 hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
 

@@ -20,20 +20,21 @@ namespace parrot {
 
 constexpr int kPartialsLds = kPrefixLds > kSplitkvLds ? kPrefixLds : kSplitkvLds;
 
-template <int DT, int D>
+template <int DT, int D, bool APPEND>
 __device__ __forceinline__ void run_splitkv(const SplitKVArgs& a, char* lds, int wg) {
   if (a.with_prefix)
-    splitkv_role<DT, D, false>(a, lds, wg);   // per-request path: cached loads
+    splitkv_role<DT, D, false, APPEND>(a, lds, wg);   // per-request path: cached loads
   else
-    splitkv_role<DT, D, true>(a, lds, wg);    // shared path: streaming loads
+    splitkv_role<DT, D, true, APPEND>(a, lds, wg);    // shared path: streaming loads
 }
 
-template <int DT, int D>
+// APPEND: also write this decode step's K/V into the cache (decode with append)
+template <int DT, int D, bool APPEND>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
 void k_partials(PartialsArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds[kPartialsLds];
   if ((int)blockIdx.x < a.n_skv)
-    run_splitkv<DT, D>(a.skv, lds, blockIdx.x);
+    run_splitkv<DT, D, APPEND>(a.skv, lds, blockIdx.x);
   else
     prefix_role<DT, D>(a.pre, lds, blockIdx.x - a.n_skv);
 }
@@ -42,7 +43,10 @@ template <int DT, int D>
 static hipError_t launch_partials_t(const PartialsArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const long blocks = (long)a.n_skv + a.n_pre;
   if (blocks <= 0) return hipSuccess;
-  hipExtLaunchKernelGGL((k_partials<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  if (a.skv.k_new)
+    hipExtLaunchKernelGGL((k_partials<DT, D, true>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  else
+    hipExtLaunchKernelGGL((k_partials<DT, D, false>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 

@@ -43,7 +43,14 @@ constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 //  * per-request path (each member re-reads its group's prefix, mostly from
 //    the caches): cached K/V loads, and table entries as scalar loads so the
 //    next block's K/V loads can issue while the current block is in flight.
-template <int DT, int D, bool STREAM>
+//
+// APPEND: the last own token of every request with S_r >= 1 is this decode
+// step's token.  Its K/V are taken from k_new / v_new instead of the pool, and
+// the lanes that hold it write it into the pool slot (stab[r][(S_r-1)/16],
+// (S_r-1)%16) while the block is reduced, so the cache holds it for later
+// steps.  The lane that writes a 16-byte piece is the lane that would have
+// read it, and no other wave reads that (block, head) in the call.
+template <int DT, int D, bool STREAM, bool APPEND = false>
 __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, int wg) {
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;        // bytes per token row
@@ -159,6 +166,8 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     int ntok;      // valid tokens in the block
     int seq;       // r * H + h
     int piece_end; // last block of its sequence
+    int app;       // APPEND: load index holding this lane's piece of the new token, else -1
+    size_t app_off;  // APPEND: pool byte offset of this lane's load `app`
   };
   auto fetch = [&](Blk& B) {
     const int nbp = s_nbp[r];
@@ -178,10 +187,30 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     }
     const int blk = clampi(entry, 0, nblk - 1);
     const size_t off = blk * blk_stride + (size_t)h * BLK_B + (size_t)lane * 16;
+    if constexpr (APPEND) {
+      // the own tokens' last block holds the new token at slot (S - 1) % 16
+      B.app = -1;
+      if (b >= nbp && b == cnt - 1) {
+        const int last = (s_slen[r] - 1) % kBlock;
+        if (tg == last % TPI) B.app = last / TPI;
+      }
+      B.app_off = off + (size_t)(B.app < 0 ? 0 : B.app) * 1024;
+      const size_t noff = ((size_t)(r * H + h) * D) * E::kBytes + (size_t)sub * 16;
+      const char* kn = (const char*)a.k_new + noff;
+      const char* vn = (const char*)a.v_new + noff;
 #pragma unroll
-    for (int i = 0; i < IPB; ++i) {
-      B.k[i] = STREAM ? ld16_stream(kp + off + i * 1024) : ld16(kp + off + i * 1024);
-      B.v[i] = STREAM ? ld16_stream(vp + off + i * 1024) : ld16(vp + off + i * 1024);
+      for (int i = 0; i < IPB; ++i) {
+        const char* ks = (i == B.app) ? kn : kp + off + i * 1024;
+        const char* vs = (i == B.app) ? vn : vp + off + i * 1024;
+        B.k[i] = STREAM ? ld16_stream(ks) : ld16(ks);
+        B.v[i] = STREAM ? ld16_stream(vs) : ld16(vs);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < IPB; ++i) {
+        B.k[i] = STREAM ? ld16_stream(kp + off + i * 1024) : ld16(kp + off + i * 1024);
+        B.v[i] = STREAM ? ld16_stream(vp + off + i * 1024) : ld16(vp + off + i * 1024);
+      }
     }
     B.q = ld16((const char*)a.q + ((size_t)(r * H + h) * D + sub * EPL) * E::kBytes);
     B.ntok = ntok < kBlock ? ntok : kBlock;
@@ -231,6 +260,17 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
   };
 
   auto reduce = [&](Blk& B, bool run_end) {
+    if constexpr (APPEND) {
+      if (B.app >= 0) {                        // write this step's token into the cache
+#pragma unroll
+        for (int i = 0; i < IPB; ++i) {
+          if (i == B.app) {
+            *reinterpret_cast<u32x4*>((char*)a.app_k + B.app_off) = B.k[i];
+            *reinterpret_cast<u32x4*>((char*)a.app_v + B.app_off) = B.v[i];
+          }
+        }
+      }
+    }
     float s[IPB];
 #pragma unroll
     for (int i = 0; i < IPB; ++i) s[i] = group_sum<LPT>(E::dot(B.k[i], B.q)) * a.scale_log2;

@@ -94,6 +94,8 @@ def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
     names = ["q", "pk", "pv", "sk", "sv", "ptab", "plen", "stab", "slen", "gid", "out", "lse", "ws"]
     if fn == "parrot_nested_prefix_decode":
         names.insert(7, "parents")
+    if fn == "parrot_shared_prefix_decode_append":
+        names[1:1] = ["k_new", "v_new"]
     vals = {n: FAKE + 4096 * i for i, n in enumerate(names)}
     vals.update(ptrs)
     ws_bytes = ptrs.get("ws_bytes", 1 << 40)
@@ -102,12 +104,14 @@ def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
 
 
 @pytest.mark.parametrize("fn", ["parrot_shared_prefix_decode", "parrot_per_request_decode",
-                                "parrot_nested_prefix_decode"])
+                                "parrot_nested_prefix_decode", "parrot_shared_prefix_decode_append"])
 @pytest.mark.parametrize("field", ["q", "sk", "sv", "stab", "slen", "gid", "out", "lse", "ws",
-                                   "pk", "pv", "ptab", "plen", "parents"])
+                                   "pk", "pv", "ptab", "plen", "parents", "k_new", "v_new"])
 def test_null_pointer_rejected(parrot_lib, fn, field):
     if field == "parents" and fn != "parrot_nested_prefix_decode":
         pytest.skip("only the nested entry point takes prefix_parents")
+    if field in ("k_new", "v_new") and fn != "parrot_shared_prefix_decode_append":
+        pytest.skip("only the appending entry point takes k_new / v_new")
     st = call(parrot_lib, base_problem(max_prefix_depth=2), fn, **{field: None})
     assert st == B.PARROT_ERR_INVALID_ARGUMENT
     assert "NULL" in B.parrot_last_error()
@@ -138,6 +142,11 @@ def test_nested_entry_checks_like_the_flat_one(parrot_lib):
     assert st == B.PARROT_ERR_WORKSPACE_TOO_SMALL
     st = call(parrot_lib, prob, "parrot_nested_prefix_decode", parents=FAKE + 2)
     assert st == B.PARROT_ERR_INVALID_ARGUMENT and "aligned" in B.parrot_last_error()
+
+
+def test_append_inputs_must_be_aligned(parrot_lib):
+    st = call(parrot_lib, base_problem(), "parrot_shared_prefix_decode_append", k_new=FAKE + 8)
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT and "k_new" in B.parrot_last_error()
 
 
 def test_workspace_too_small(parrot_lib):
