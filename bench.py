@@ -211,6 +211,7 @@ def main():
 
     nested = plan.nested
     flat_layers = flat_dec = None
+    new_kv = None
     if nested:
         # baselines for nested groups: the flat entry points on the same blocks,
         # each group's chain of prefixes laid end to end as one flat prefix
@@ -228,13 +229,17 @@ def main():
             suffix_table_stride=flat.suffix_tables.shape[1],
             num_prefix_blocks=flat.num_blocks, num_suffix_blocks=flat.num_blocks), device=dev)
 
-    def run(shared: bool, trace: bool, flat_baseline: bool = False):
+    def run(shared: bool, trace: bool, flat_baseline: bool = False, append: bool = False):
         """W untimed steps, then K timed steps; every `trace_every`-th timed step
         carries per-kernel (start, stop) event pairs when `trace` is set.  For
         nested groups, `flat_baseline` runs the flat entry points on the
-        flattened groups."""
+        flattened groups; `append` times decode with append (this step's K/V
+        written into every request's last own slot)."""
         if nested and (flat_baseline or not shared):
             calls = [flat_dec.bind(flat_layers[l], shared=shared, stream=stream) for l in range(L)]
+        elif append:
+            calls = [dec.bind(dict(layers[l], k_new=new_kv[l][0], v_new=new_kv[l][1]),
+                              stream=stream, append=True) for l in range(L)]
         else:
             calls = [dec.bind(layers[l], shared=shared, stream=stream, nested=nested)
                      for l in range(L)]
@@ -335,6 +340,30 @@ def main():
                 "speedup_of_nested": round(wall_f / wall, 3),
                 "hbm_gbps": round(flat_bytes / (wall_f / K) / 1e9, 1),
                 "note": "parrot_shared_prefix_decode with each group's prefix chain as one flat prefix",
+            }
+        if not nested:
+            # decode with append: the same step, with this step's K/V written
+            # into the cache by the partial-result kernel (the values equal
+            # what the slots already hold, so later steps see the same data)
+            last = [(r, int(plan.suffix_tables[r][(int(plan.suffix_lens[r]) - 1) // plan.block_size]),
+                     (int(plan.suffix_lens[r]) - 1) % plan.block_size)
+                    for r in range(R) if plan.suffix_lens[r] > 0]
+            rows = torch.tensor([x[0] for x in last], device=dev, dtype=torch.long)
+            blks = torch.tensor([x[1] for x in last], device=dev, dtype=torch.long)
+            slots = torch.tensor([x[2] for x in last], device=dev, dtype=torch.long)
+            new_kv = []
+            for t in layers:
+                pair = []
+                for name in ("k_pool", "v_pool"):
+                    x = torch.zeros((R, plan.heads, plan.head_dim), dtype=t["q"].dtype, device=dev)
+                    x[rows] = t[name][blks, :, slots]
+                    pair.append(x)
+                new_kv.append(pair)
+            wall_a, _ = run(shared=True, trace=False, append=True)
+            result["append_step"] = {
+                "ms_per_step": round(wall_a / K * 1e3, 5),
+                "overhead_vs_plain": round(wall_a / wall - 1.0, 4),
+                "note": "parrot_shared_prefix_decode_append on the same workload",
             }
         wall_n, _ = run(shared=False, trace=False)
         result["per_request_baseline"] = {
