@@ -20,7 +20,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB_NAME = "libparrot_attn.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
-SOURCES = ["api.hip", "partials.hip", "merge.hip"]
+SOURCES = ["api.hip", "partials.hip", "merge.hip", "context_store.cpp"]
 
 # Packed fp32 arithmetic is disabled: the kernels write only scalar float code.
 HIP_FLAGS = [
@@ -57,7 +57,7 @@ def build(verbose: bool = False, extra_flags=(), out_path: str = LIB_PATH,
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(build_dir, src.replace(".hip", ".o"))
+        obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
         cmds.append([hipcc, *HIP_FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC, "-c",
                      os.path.join(CSRC, src), "-o", obj])

@@ -10,6 +10,7 @@
 
 #include "parrot_attn.h"
 #include "common.h"
+#include "errors.h"
 
 namespace {
 
@@ -24,6 +25,28 @@ parrot_status fail(parrot_status s, const char* fmt, ...) {
   g_err = buf;
   return s;
 }
+
+}  // namespace
+
+namespace parrot {
+
+parrot_status set_error(parrot_status s, const char* fmt, ...) {
+  if (s == PARROT_OK) {
+    g_err.clear();
+    return s;
+  }
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+}  // namespace parrot
+
+namespace {
 
 long ceil_div(long a, long b) { return (a + b - 1) / b; }
 

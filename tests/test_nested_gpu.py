@@ -136,3 +136,50 @@ def test_nested_validation_rejects_bad_parents():
     prob.max_prefix_depth = 3                    # the chain 0 <- 1 <- 3 <- 4 has 4 groups
     with pytest.raises(ParrotError, match="deeper"):
         parrot_validate_nested_inputs(*args(dev["prefix_parents"]))
+
+
+def plan_from_store(batch, store, heads, head_dim, dtype):
+    """A LayoutPlan over the store's blocks (block num_blocks is the NaN pad)."""
+    from workloads.gen import LayoutPlan
+    B, NB = store.block_size, store.num_blocks + 1
+    fill = np.zeros(NB, dtype=np.int32)
+    for lens, tabs in ((batch.prefix_lens, batch.prefix_tables),
+                       (batch.suffix_lens, batch.suffix_tables)):
+        for n, row in zip(lens, tabs):
+            for j in range(-(-int(n) // B)):
+                fill[row[j]] = min(B, int(n) - j * B)
+    return LayoutPlan(heads=heads, head_dim=head_dim, block_size=B, dtype=dtype,
+                      sm_scale=1.0 / math.sqrt(head_dim), q_scale=1.0,
+                      group_ids=batch.group_ids, prefix_lens=batch.prefix_lens,
+                      suffix_lens=batch.suffix_lens, prefix_tables=batch.prefix_tables,
+                      suffix_tables=batch.suffix_tables, block_fill=fill,
+                      poison_block=NB - 1, prefix_parents=batch.prefix_parents)
+
+
+def test_context_store_batch_end_to_end():
+    """Prompts registered in the host context store (a system prompt, three
+    task prefixes, own tokens, appended tokens, a prompt that shares nothing)
+    produce a batch that the nested entry point decodes to the oracle's result."""
+    from paper_2405_19888_amd.context import ContextStore
+    say("context store end to end")
+    rng = np.random.default_rng(4)
+    st = ContextStore(block_size=16, num_blocks=600)
+    sysp = rng.integers(0, 1000, size=300).tolist()
+    tasks = [rng.integers(0, 1000, size=n).tolist() for n in (50, 77, 120)]
+    ctxs = []
+    for i in range(12):
+        t = tasks[i % 3]
+        own = rng.integers(0, 1000, size=int(rng.integers(1, 90))).tolist()
+        ctxs.append(st.fill(sysp + t + own, [300, 300 + len(t)]))
+    ctxs.append(st.fill(rng.integers(0, 1000, size=40).tolist(), []))
+    ctxs.append(st.fill(sysp, [300]))                  # prompt = the system prompt alone
+    for c in ctxs[:5]:
+        for _ in range(int(rng.integers(1, 20))):
+            st.append(c)
+    st.append(ctxs[-1])
+    batch = st.build_batch(ctxs, pad_block=st.num_blocks)
+    assert batch.shape.num_groups == 4 and batch.shape.max_prefix_depth == 2
+    plan = plan_from_store(batch, st, heads=8, head_dim=128, dtype="float16")
+    data = make_batch(plan, seed=6)
+    out, lse = run_gpu(plan, data.to("cuda"))
+    assert_close(*to_np(out, lse), *oracle_for(data, plan), "float16", "context store batch")
