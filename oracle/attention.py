@@ -27,6 +27,15 @@ and does not restate it, so the standard definition is written out here):
   first, then g's own prefix, then its own tokens.  Without prefix_parents
   every group stands alone.
 
+  Prefill of a forked context (Section 7, Fill with a parent_context_id: the
+  new prompt tokens of a context forked from a parent are filled on top of the
+  parent's KV cache, so only the new tokens are computed).  Request r brings
+  Q_r <= S_r new rows, its last Q_r own tokens, stacked in request order:
+  row query_offsets[r] + j is own position p = S_r - Q_r + j.  Its keys are
+  those of the decode case cut after own token p: the prefixes of its group's
+  chain, then own tokens 0..p (the usual causal self-attention of a decoder,
+  which the paper takes as given).  With Q_r = S_r = 1 it is one decode step.
+
 All inputs are upcast exactly to float64 before any arithmetic.
 """
 from __future__ import annotations
@@ -179,6 +188,57 @@ def shared_prefix_decode(q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_table
         if K.shape[0] == 0:
             raise ValueError(f"request {r} has an empty context")
         out[i], lse[i] = attend(qf[r], K, V, sm_scale)
+    return out, lse
+
+
+def prefill_positions(query_offsets, suffix_lens) -> list:
+    """(request, own position) of every query row, in row order."""
+    qo = _ints(query_offsets)
+    S = _ints(suffix_lens)
+    if qo.shape[0] != S.shape[0] + 1 or qo[0] != 0:
+        raise ValueError("query_offsets must hold R + 1 entries starting at 0")
+    rows = []
+    for r in range(S.shape[0]):
+        Q = int(qo[r + 1] - qo[r])
+        if Q < 0 or Q > S[r]:
+            raise ValueError(f"request {r}: {Q} query rows for {S[r]} own tokens")
+        rows += [(r, int(S[r]) - Q + j) for j in range(Q)]
+    return rows
+
+
+def shared_prefix_prefill(q, query_offsets, prefix_k, prefix_v, suffix_k, suffix_v,
+                          prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids,
+                          sm_scale: float, rows: Optional[Sequence[int]] = None,
+                          prefix_parents=None):
+    """Naive per-row prefill attention: row i of request r at own position p
+    attends to r's prefix chain and its own tokens 0..p.
+
+    q: [T, H, D] query rows (T = query_offsets[R]).  Returns (out [n, H, D],
+    lse [n, H]) in float64 for the rows listed in ``rows`` (all by default).
+    """
+    qf = to_f64(q)
+    pos = prefill_positions(query_offsets, suffix_lens)
+    if len(pos) != qf.shape[0]:
+        raise ValueError(f"{qf.shape[0]} query rows, offsets describe {len(pos)}")
+    rows = list(range(len(pos)) if rows is None else rows)
+    H, D = qf.shape[1], qf.shape[2]
+    out = np.zeros((len(rows), H, D))
+    lse = np.zeros((len(rows), H))
+    kv = {}
+    gid = _ints(group_ids)
+    plen = _ints(prefix_lens)
+    for i, t in enumerate(rows):
+        r, p = pos[t]
+        if r not in kv:
+            kv[r] = request_kv(r, prefix_k=prefix_k, prefix_v=prefix_v, suffix_k=suffix_k,
+                               suffix_v=suffix_v, prefix_tables=prefix_tables,
+                               prefix_lens=prefix_lens, suffix_tables=suffix_tables,
+                               suffix_lens=suffix_lens, group_ids=group_ids,
+                               prefix_parents=prefix_parents)
+        K, V = kv[r]
+        n_prefix = sum(int(plen[a]) for a in group_chain(int(gid[r]), prefix_parents))
+        n = n_prefix + p + 1
+        out[i], lse[i] = attend(qf[t], K[:n], V[:n], sm_scale)
     return out, lse
 
 

@@ -377,3 +377,199 @@ ALL_PINS = {
     "nested_flatten": pin_nested_flatten,
     "nested_spike": pin_nested_spike,
 }
+
+
+# ------------------------------------------------------------------ prefill
+# Pins for a prefill implementation with the signature of the oracle's
+# ``shared_prefix_prefill(q, query_offsets, prefix_k, prefix_v, suffix_k,
+# suffix_v, prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids,
+# sm_scale, rows=None, prefix_parents=None)``.
+
+def prefill_args(batch, q_rows, offsets, **over):
+    args = decode_args(batch, q=q_rows)
+    args["query_offsets"] = offsets
+    args.update(over)
+    return args
+
+
+def tiny_prefill_case(nested=False, seed=6):
+    """(batch, q_rows, offsets): every row count from 0 to S_r (a chunk of a
+    prompt whose first own tokens are already cached, a whole prompt, none)."""
+    from workloads import make_prefill_queries
+    batch = tiny_nested_batch(seed=seed) if nested else tiny_paged_batch(seed=seed)
+    S = batch.plan.suffix_lens
+    qr = [int(s) if i % 3 == 0 else int(s) // 2 if i % 3 == 1 else min(int(s), 1)
+          for i, s in enumerate(S)]
+    q, off = make_prefill_queries(batch.plan, qr, seed=seed)
+    return batch, q, off
+
+
+def _row_owner(offsets, t):
+    """Brute-force: the request whose row range holds row t."""
+    for r in range(len(offsets) - 1):
+        if offsets[r] <= t < offsets[r + 1]:
+            return r
+    raise AssertionError(f"row {t} belongs to no request")
+
+
+def prefill_brute_force(batch, q_rows, offsets):
+    """Pure-Python loops: row t of request r is own token S_r - Q_r + (t - offsets[r])."""
+    p = batch.plan
+    B = p.block_size
+    q = q_rows.double().tolist()
+    kp = batch.k_pool.double().tolist()
+    vp = batch.v_pool.double().tolist()
+    outs, lses = [], []
+    for t in range(len(q)):
+        r = _row_owner(offsets, t)
+        S = int(p.suffix_lens[r])
+        Q = int(offsets[r + 1] - offsets[r])
+        pos = S - Q + (t - int(offsets[r]))
+        keys = []
+        for g in _walk_up(p.prefix_parents, int(p.group_ids[r])):
+            for j in range(int(p.prefix_lens[g])):
+                keys.append((int(p.prefix_tables[g][j // B]), j % B))
+        for j in range(pos + 1):
+            keys.append((int(p.suffix_tables[r][j // B]), j % B))
+        orow, lrow = [], []
+        for h in range(p.heads):
+            es = [math.exp(p.sm_scale * sum(q[t][h][d] * kp[blk][h][slot][d]
+                                             for d in range(p.head_dim)))
+                  for (blk, slot) in keys]
+            z = sum(es)
+            lrow.append(math.log(z))
+            orow.append([sum(es[j] * vp[blk][h][slot][d] for j, (blk, slot) in enumerate(keys)) / z
+                         for d in range(p.head_dim)])
+        outs.append(orow)
+        lses.append(lrow)
+    return np.array(outs), np.array(lses)
+
+
+def pin_prefill_brute_force(prefill):
+    for nested in (False, True):
+        batch, q, off = tiny_prefill_case(nested)
+        out, lse = prefill(**prefill_args(batch, q, off))
+        bo, bl = prefill_brute_force(batch, q, off)
+        _close(out, bo, 1e-12, 1e-13, f"prefill brute force out (nested={nested})")
+        _close(lse, bl, 1e-12, 1e-13, f"prefill brute force lse (nested={nested})")
+
+
+def pin_prefill_sdpa(prefill):
+    """torch's scaled_dot_product_attention in float64 with a boolean mask
+    that lets row j see the prefix and own tokens up to its position."""
+    from workloads import make_prefill_queries
+    batch = c1_batch()          # contiguous: identity block tables
+    p = batch.plan
+    qr = [int(s) - (r % 3) if int(s) > 2 else int(s) for r, s in enumerate(p.suffix_lens)]
+    q, off = make_prefill_queries(p, qr, seed=1)
+    out, lse = prefill(**prefill_args(batch, q, off))
+    B = p.block_size
+    kk = batch.k_pool.double().permute(0, 2, 1, 3)   # [NB, B, H, D]
+    vv = batch.v_pool.double().permute(0, 2, 1, 3)
+
+    def seq(x, tbl, n):
+        return x[tbl[: -(-n // B)]].reshape(-1, p.heads, p.head_dim)[:n]
+    for r in range(p.num_requests):
+        g = int(p.group_ids[r])
+        P = int(p.prefix_lens[g]) if g >= 0 else 0
+        S, Q = int(p.suffix_lens[r]), int(off[r + 1] - off[r])
+        if Q == 0:
+            continue
+        parts_k = [seq(kk, p.prefix_tables[g], P)] if g >= 0 else []
+        parts_v = [seq(vv, p.prefix_tables[g], P)] if g >= 0 else []
+        K = torch.cat(parts_k + [seq(kk, p.suffix_tables[r], S)]).permute(1, 0, 2)[None]
+        V = torch.cat(parts_v + [seq(vv, p.suffix_tables[r], S)]).permute(1, 0, 2)[None]
+        qq = q[off[r]:off[r + 1]].double().permute(1, 0, 2)[None]     # [1, H, Q, D]
+        key = torch.arange(P + S)[None, :]
+        row = torch.arange(Q)[:, None]
+        mask = key <= P + (S - Q) + row                                # [Q, P + S]
+        ref = torch.nn.functional.scaled_dot_product_attention(qq, K, V, attn_mask=mask,
+                                                               scale=p.sm_scale)
+        _close(out[off[r]:off[r + 1]], ref[0].permute(1, 0, 2).numpy(), 0, 1e-12,
+               f"prefill sdpa request {r}")
+
+
+def pin_prefill_last_row_is_decode(prefill):
+    """A request's last row sits at its last own token: it is that request's
+    decode step with this row as the query (the decode pins fix that case)."""
+    import oracle
+    for nested in (False, True):
+        batch, q, off = tiny_prefill_case(nested)
+        p = batch.plan
+        out, lse = prefill(**prefill_args(batch, q, off))
+        last = [r for r in range(p.num_requests) if off[r + 1] > off[r]]
+        qd = batch.q.clone()
+        for r in last:
+            qd[r] = q[int(off[r + 1]) - 1]
+        do, dl = oracle.shared_prefix_decode(**decode_args(batch, q=qd), requests=last)
+        rows = [int(off[r + 1]) - 1 for r in last]
+        _close(out[rows], do, 1e-12, 1e-13, f"last row vs decode (nested={nested})")
+        _close(lse[rows], dl, 1e-12, 1e-13, f"last row lse vs decode (nested={nested})")
+
+
+def pin_prefill_causal(prefill):
+    """Own tokens after a row's position change nothing (poisoned with NaN
+    they stay unread); a dominant key at own position j takes over exactly the
+    rows at positions >= j."""
+    batch, q, off = tiny_prefill_case(False)
+    p = batch.plan
+    B = p.block_size
+    out, lse = prefill(**prefill_args(batch, q, off))
+    for r in range(p.num_requests):
+        S, Q = int(p.suffix_lens[r]), int(off[r + 1] - off[r])
+        if Q == 0:
+            continue
+        first = S - Q                                  # position of row off[r]
+        k, v = batch.k_pool.clone(), batch.v_pool.clone()
+        for j in range(first + 1, S):
+            blk, slot = int(p.suffix_tables[r][j // B]), j % B
+            k[blk, :, slot] = float("nan")
+            v[blk, :, slot] = float("nan")
+        o1, l1 = prefill(**prefill_args(batch, q, off, prefix_k=k, prefix_v=v, suffix_k=k,
+                                        suffix_v=v), rows=[int(off[r])])
+        assert np.array_equal(o1[0], out[off[r]]) and np.array_equal(l1[0], lse[off[r]]), \
+            f"request {r}: a later own token changed row {off[r]}"
+        j = S - 1 if Q > 1 else first                  # spike at the last own token
+        blk, slot = int(p.suffix_tables[r][j // B]), j % B
+        h = 0
+        rows = list(range(int(off[r]), int(off[r + 1])))
+        for t in rows:
+            pos = first + (t - int(off[r]))
+            k = batch.k_pool.clone()
+            qv = q[t, h].double()
+            k[blk, h, slot, :] = (40.0 / (p.sm_scale * float(qv @ qv)) * qv).to(k.dtype)
+            o2, _ = prefill(**prefill_args(batch, q, off, prefix_k=k, suffix_k=k), rows=[t])
+            vj = batch.v_pool[blk, h, slot].double().numpy()
+            if pos >= j:
+                _close(o2[0, h], vj, 0, 1e-9, f"spike at own {j} seen by row {t}")
+            else:
+                assert np.array_equal(o2[0, h], out[t, h]), f"row {t} saw own token {j} > {pos}"
+
+
+def pin_prefill_first_row_single_key(prefill):
+    """Row at own position 0 of an ungrouped request sees one key: out = V_0,
+    lse = s_0."""
+    from workloads import make_prefill_queries
+    batch = tiny_paged_batch()
+    p = batch.plan
+    qr = [int(s) if int(p.group_ids[r]) < 0 else 0 for r, s in enumerate(p.suffix_lens)]
+    q, off = make_prefill_queries(p, qr, seed=3)
+    out, lse = prefill(**prefill_args(batch, q, off))
+    B = p.block_size
+    for r in range(p.num_requests):
+        if qr[r] == 0:
+            continue
+        t = int(off[r])
+        blk, slot = int(p.suffix_tables[r][0]), 0
+        s0 = p.sm_scale * (q[t].double() * batch.k_pool[blk, :, slot].double()).sum(-1)
+        _close(out[t], batch.v_pool[blk, :, slot].double().numpy(), 0, 1e-13, f"first row {t}")
+        _close(lse[t], s0.numpy(), 0, 1e-13, f"first row lse {t}")
+
+
+PREFILL_PINS = {
+    "prefill_brute_force": pin_prefill_brute_force,
+    "prefill_sdpa": pin_prefill_sdpa,
+    "prefill_last_row_is_decode": pin_prefill_last_row_is_decode,
+    "prefill_causal": pin_prefill_causal,
+    "prefill_first_row_single_key": pin_prefill_first_row_single_key,
+}

@@ -13,7 +13,7 @@ import pytest
 import oracle
 import oracle.attention as oa
 import oracle_pins as pins
-from oracle_pins import ALL_PINS, GOLDEN, pin_decomposition, tiny_paged_batch, decode_args
+from oracle_pins import ALL_PINS, GOLDEN, PREFILL_PINS, pin_decomposition, tiny_paged_batch, decode_args
 
 
 @pytest.mark.parametrize("name", sorted(ALL_PINS))
@@ -275,3 +275,73 @@ def test_pins_catch_planted_mistake(mutant, monkeypatch):
         except (AssertionError, ValueError, IndexError):
             caught.append(name)
     assert caught, f"no pin caught the planted mistake {mutant}"
+
+
+# ------------------------------------------------------------------ prefill
+@pytest.mark.parametrize("name", sorted(PREFILL_PINS))
+def test_oracle_prefill_pin(name):
+    PREFILL_PINS[name](oracle.shared_prefix_prefill)
+
+
+def test_prefill_rejects_bad_offsets():
+    batch, q, off = pins.tiny_prefill_case()
+    args = pins.prefill_args(batch, q, off)
+    bad = off.copy()
+    bad[1] = bad[0] + int(batch.plan.suffix_lens[0]) + 1       # more rows than own tokens
+    with pytest.raises(ValueError):
+        oracle.shared_prefix_prefill(**dict(args, query_offsets=bad))
+    with pytest.raises(ValueError):
+        oracle.shared_prefix_prefill(**dict(args, q=q[:-1]))
+
+
+def _positions_mutant(monkeypatch, f):
+    real = oa.prefill_positions
+
+    def g(query_offsets, suffix_lens):
+        rows = real(query_offsets, suffix_lens)
+        S = [int(x) for x in suffix_lens]
+        qo = [int(x) for x in query_offsets]
+        return [f(r, p, S, qo) for r, p in rows]
+    monkeypatch.setattr(oa, "prefill_positions", g)
+
+
+PREFILL_MUTANTS = {
+    # a row does not see its own token
+    "self_excluded": lambda mp: _positions_mutant(mp, lambda r, p, S, qo: (r, p - 1)),
+    # a row sees the next own token too
+    "next_included": lambda mp: _positions_mutant(mp, lambda r, p, S, qo: (r, min(p + 1, S[r] - 1))),
+    # rows see every own token (no causal cut)
+    "not_causal": lambda mp: _positions_mutant(mp, lambda r, p, S, qo: (r, S[r] - 1)),
+    # rows numbered from the first own token instead of the last Q_r
+    "positions_from_start": lambda mp: _positions_mutant(
+        mp, lambda r, p, S, qo: (r, p - (S[r] - (qo[r + 1] - qo[r])))),
+}
+
+
+@pytest.mark.parametrize("mutant", sorted(PREFILL_MUTANTS))
+def test_prefill_pins_catch_planted_mistake(mutant, monkeypatch):
+    PREFILL_MUTANTS[mutant](monkeypatch)
+    caught = []
+    for name, pin in PREFILL_PINS.items():
+        try:
+            pin(oracle.shared_prefix_prefill)
+        except (AssertionError, ValueError, IndexError):
+            caught.append(name)
+    assert caught, f"no pin caught the planted mistake {mutant}"
+
+
+@pytest.mark.parametrize("mutant", ["prefix_ignored", "chain_leaf_only", "wrong_group",
+                                    "gather_slot_shift", "lse_without_max"])
+def test_prefill_pins_catch_shared_mistakes(mutant, monkeypatch):
+    """Mistakes in the parts prefill shares with decode are caught by the
+    prefill pins on their own."""
+    MUTANTS[mutant](monkeypatch)
+    caught = []
+    for name, pin in PREFILL_PINS.items():
+        if name == "prefill_last_row_is_decode":
+            continue              # compares against the (equally mutated) decode
+        try:
+            pin(oracle.shared_prefix_prefill)
+        except (AssertionError, ValueError, IndexError):
+            caught.append(name)
+    assert caught, f"no prefill pin caught the planted mistake {mutant}"

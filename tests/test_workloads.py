@@ -122,3 +122,22 @@ def test_parents_must_point_to_lower_groups():
         build_plan(heads=1, head_dim=64, block_size=16, dtype="float32", group_of_request=[0, 1],
                    prefix_lens=[16, 16], suffix_lens=[1, 1], sm_scale=1.0,
                    prefix_parents=[1, -1])
+
+
+def test_prefill_queries_layout():
+    from workloads import make_prefill_queries, prefill_rows, query_offsets_for
+    plan = make_plan(get_config("tiny"))
+    rng = np.random.default_rng(0)
+    for recipe in ("all", 3, 0.5):
+        qr = prefill_rows(plan, recipe, rng)
+        assert np.all(qr >= 0) and np.all(qr <= plan.suffix_lens)
+        q, off = make_prefill_queries(plan, qr, seed=2)
+        assert off[0] == 0 and off[-1] == q.shape[0] == qr.sum()
+        assert np.array_equal(np.diff(off), qr)
+        assert q.shape[1:] == (plan.heads, plan.head_dim)
+        q2, _ = make_prefill_queries(plan, qr, seed=2)
+        assert torch.equal(q, q2)
+    with pytest.raises(ValueError):
+        query_offsets_for(plan, plan.suffix_lens + 1)
+    with pytest.raises(ValueError):
+        query_offsets_for(plan, [1])

@@ -33,6 +33,12 @@ then cast to the workload dtype with round-to-nearest-even.  The device
 recipe (``make_device_layers``) draws the same shapes with torch's Philox
 generator on the GPU instead; it is used where host generation of many
 gigabytes would be too slow, and its values differ from the host recipe.
+
+Prefill queries (``make_prefill_queries``): request r contributes Q_r <= S_r
+query rows, its last Q_r own tokens, stacked in request order into a
+[sum Q_r, H, D] array; query_offsets[r] is the first row of request r and
+query_offsets[R] the row count.  Their values come from a torch CPU generator
+seeded with seed * 1000003 + 104729, N(0,1) * q_scale as float32, then cast.
 """
 from __future__ import annotations
 
@@ -361,3 +367,36 @@ def make_device_layer(plan: LayoutPlan, layer: int, device, seed: int = 0) -> di
 def make_device_layers(plan: LayoutPlan, layers: int, device, seed: int = 0) -> list[dict]:
     """``make_device_layer`` for layers 0..layers-1."""
     return [make_device_layer(plan, l, device, seed) for l in range(layers)]
+
+
+def query_offsets_for(plan: LayoutPlan, query_rows: Sequence[int]) -> np.ndarray:
+    """int32 [R + 1] row offsets for Q_r = query_rows[r] rows of request r
+    (0 <= Q_r <= S_r)."""
+    qr = np.asarray(query_rows, dtype=np.int64)
+    if qr.shape != (plan.num_requests,):
+        raise ValueError("one row count per request")
+    if np.any(qr < 0) or np.any(qr > plan.suffix_lens):
+        raise ValueError("query rows must lie in [0, S_r]")
+    return np.concatenate([[0], np.cumsum(qr)]).astype(np.int32)
+
+
+def prefill_rows(plan: LayoutPlan, recipe, rng: np.random.Generator) -> np.ndarray:
+    """Row counts per request: "all" (Q_r = S_r), an int (min(S_r, n)), or a
+    fraction in (0, 1) (ceil(f S_r)); each clipped to [0, S_r]."""
+    S = plan.suffix_lens.astype(np.int64)
+    if recipe == "all":
+        return S.copy()
+    if isinstance(recipe, float):
+        return np.minimum(S, np.ceil(recipe * S).astype(np.int64))
+    return np.minimum(S, int(recipe))
+
+
+def make_prefill_queries(plan: LayoutPlan, query_rows: Sequence[int], seed: int = 0):
+    """(q_rows [sum Q_r, H, D] in the plan dtype, query_offsets int32 [R + 1])."""
+    off = query_offsets_for(plan, query_rows)
+    g = torch.Generator()
+    g.manual_seed(int(seed) * 1_000_003 + 104_729)
+    q = torch.randn((int(off[-1]), plan.heads, plan.head_dim), generator=g, dtype=torch.float32)
+    if plan.q_scale != 1.0:
+        q.mul_(plan.q_scale)
+    return q.to(TORCH_DTYPES[plan.dtype]), off
