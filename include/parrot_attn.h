@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 2
+#define PARROT_ABI_VERSION 3
 
 typedef enum {
   PARROT_OK = 0,
@@ -251,6 +251,80 @@ parrot_status parrot_validate_inputs(
  * in [-1, g) and that no chain holds more than max_prefix_depth groups. */
 parrot_status parrot_validate_nested_inputs(
     const parrot_problem* p,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* prefix_parents,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, int32_t* scratch, void* stream);
+
+/*
+ * Prefill of forked contexts (Section 7: Fill with a parent_context_id fills a
+ * new context's prompt tokens on top of its parent's KV cache, so the parent's
+ * tokens -- the group's shared prefix -- are not computed again; Section 5.3
+ * for the sharing).  For each request r, its last Q_r own tokens are new:
+ *   query_offsets        int32 [R + 1]: rows [query_offsets[r],
+ *                        query_offsets[r+1]) of q belong to r, so
+ *                        Q_r = query_offsets[r+1] - query_offsets[r], with
+ *                        query_offsets[0] = 0, query_offsets[R] = T and
+ *                        0 <= Q_r <= min(suffix_lens[r], max_query_rows).
+ * Row query_offsets[r] + j is own position p = S_r - Q_r + j; it attends to
+ * the prefixes of r's group chain (as parrot_nested_prefix_decode; one group
+ * when prefix_parents is NULL) and then to r's own tokens 0..p (causal).  The
+ * keys and values of all own tokens, the new ones included, must already be
+ * in the suffix pools (the caller writes them, as for any layer's prefill).
+ * Q_r < S_r continues a prompt whose first own tokens are cached (chunked
+ * prefill).  Per row and head the result is the decode formula over those
+ * keys.
+ *
+ * Two kernels run on `stream`: the partial-result kernel (prefix items: the
+ * rows of all requests reading a group's prefix, 64 per tile, against one
+ * prefix chunk staged in LDS; own items: 64 rows of one request against one
+ * chunk of its own tokens with a per-row causal limit; both on MFMA), then the
+ * merge kernel per (row, head).
+ *
+ *   rows                 (host) row counts; see parrot_prefill_rows
+ *   q                    [T][H][D] dtype, 16-byte aligned
+ *   prefix_parents       int32 [NG] as parrot_nested_prefix_decode, or NULL
+ *                        for flat groups
+ *   out                  [T][H][D] dtype;  lse  float32 [T][H]
+ *   workspace            >= parrot_prefill_workspace_bytes(p, rows) bytes,
+ *                        256-byte aligned
+ * Other arguments as parrot_shared_prefix_decode.  `p->max_group_size` is not
+ * used (rows->max_group_rows takes its place).  Rows of a call whose offsets
+ * break the rules above get unspecified values but every access stays in
+ * bounds; parrot_validate_prefill_inputs checks them.
+ */
+typedef struct {
+  int32_t num_query_rows;   /* T = query_offsets[R] >= 0; T = 0 is a no-op */
+  int32_t max_query_rows;   /* >= every Q_r; >= 1 when T > 0 */
+  int32_t max_group_rows;   /* >= the rows that read any one group's prefix (the
+                               rows of its members and, with nested groups, of
+                               its descendants' members) */
+} parrot_prefill_rows;
+
+/* Bytes of workspace parrot_shared_prefix_prefill needs (0 when T = 0);
+ * depends on the current device's compute-unit count like
+ * parrot_workspace_bytes.  (size_t)-1 if the arguments are invalid. */
+size_t parrot_prefill_workspace_bytes(const parrot_problem* p, const parrot_prefill_rows* rows);
+
+parrot_status parrot_shared_prefix_prefill(
+    const parrot_problem* p, const parrot_prefill_rows* rows,
+    const void* q, const int32_t* query_offsets,
+    const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* prefix_parents,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
+    void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/* parrot_validate_inputs (with the parent checks when prefix_parents is not
+ * NULL) plus the row offsets: query_offsets[0] = 0, non-decreasing,
+ * query_offsets[R] = T, every Q_r <= min(S_r, max_query_rows), and at most
+ * max_group_rows rows reading any one group. */
+parrot_status parrot_validate_prefill_inputs(
+    const parrot_problem* p, const parrot_prefill_rows* rows, const int32_t* query_offsets,
     const int32_t* prefix_block_tables, const int32_t* prefix_lens,
     const int32_t* prefix_parents,
     const int32_t* suffix_block_tables, const int32_t* suffix_lens,

@@ -60,11 +60,20 @@ class ParrotTrace(ctypes.Structure):
     ]
 
 
+class ParrotPrefillRows(ctypes.Structure):
+    _fields_ = [
+        ("num_query_rows", ctypes.c_int32),
+        ("max_query_rows", ctypes.c_int32),
+        ("max_group_rows", ctypes.c_int32),
+    ]
+
+
 EXPORTED = (
     "parrot_workspace_bytes", "parrot_shared_prefix_decode", "parrot_per_request_decode",
     "parrot_nested_prefix_decode", "parrot_shared_prefix_decode_append",
-    "parrot_validate_inputs", "parrot_validate_nested_inputs", "parrot_last_error",
-    "parrot_abi_version",
+    "parrot_validate_inputs", "parrot_validate_nested_inputs",
+    "parrot_prefill_workspace_bytes", "parrot_shared_prefix_prefill",
+    "parrot_validate_prefill_inputs", "parrot_last_error", "parrot_abi_version",
 )
 
 _lib: Optional[ctypes.CDLL] = None
@@ -101,6 +110,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p,
                                                       vp, vp]
         lib.parrot_validate_nested_inputs.restype = ctypes.c_int
+    rows_p = ctypes.POINTER(ParrotPrefillRows)
+    if hasattr(lib, "parrot_shared_prefix_prefill"):     # absent from ABI 1-2 builds
+        lib.parrot_prefill_workspace_bytes.argtypes = [prob_p, rows_p]
+        lib.parrot_prefill_workspace_bytes.restype = sz
+        lib.parrot_shared_prefix_prefill.argtypes = [
+            prob_p, rows_p, vp, i32p, vp, vp, vp, vp, i32p, i32p, i32p, i32p, i32p, i32p, vp, vp,
+            vp, sz, vp, ctypes.POINTER(ParrotTrace)]
+        lib.parrot_shared_prefix_prefill.restype = ctypes.c_int
+        lib.parrot_validate_prefill_inputs.argtypes = [prob_p, rows_p, i32p, i32p, i32p, i32p,
+                                                       i32p, i32p, i32p, vp, vp]
+        lib.parrot_validate_prefill_inputs.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []
@@ -237,6 +257,61 @@ def parrot_validate_inputs(problem, prefix_block_tables, prefix_lens, suffix_blo
         _stream_handle(stream)))
 
 
+def make_prefill_rows(num_query_rows, max_query_rows, max_group_rows) -> ParrotPrefillRows:
+    return ParrotPrefillRows(int(num_query_rows), int(max_query_rows), int(max_group_rows))
+
+
+def prefill_rows_from_host(query_offsets, group_ids, num_groups, prefix_parents=None
+                           ) -> ParrotPrefillRows:
+    """Row counts of a prefill call from host copies of its offsets and groups."""
+    import numpy as np
+    off = np.asarray(query_offsets, dtype=np.int64)
+    q = np.diff(off)
+    per_group = np.zeros(max(int(num_groups), 1), dtype=np.int64)
+    par = None if prefix_parents is None else np.asarray(prefix_parents)
+    for r, g in enumerate(np.asarray(group_ids)):
+        x = int(g)
+        while x >= 0:
+            per_group[x] += q[r]
+            x = int(par[x]) if par is not None else -1
+    return make_prefill_rows(int(off[-1]), max(int(q.max()) if q.size else 0, 1),
+                             int(per_group.max()) if num_groups else 0)
+
+
+def parrot_prefill_workspace_bytes(problem: ParrotProblem, rows: ParrotPrefillRows) -> int:
+    n = load_library().parrot_prefill_workspace_bytes(ctypes.byref(problem), ctypes.byref(rows))
+    if n == ctypes.c_size_t(-1).value:
+        raise ParrotError(PARROT_ERR_INVALID_ARGUMENT, parrot_last_error())
+    return int(n)
+
+
+def parrot_shared_prefix_prefill(problem, rows, q, query_offsets, prefix_k, prefix_v, suffix_k,
+                                 suffix_v, prefix_block_tables, prefix_lens, prefix_parents,
+                                 suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
+                                 stream=None, trace=None):
+    """Prefill of forked contexts' new rows (see the C header); prefix_parents
+    may be None for flat groups."""
+    lib = load_library()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.parrot_shared_prefix_prefill(
+        ctypes.byref(problem), ctypes.byref(rows), _ptr(q), _ptr(query_offsets), _ptr(prefix_k),
+        _ptr(prefix_v), _ptr(suffix_k), _ptr(suffix_v), _ptr(prefix_block_tables),
+        _ptr(prefix_lens), _ptr(prefix_parents), _ptr(suffix_block_tables), _ptr(suffix_lens),
+        _ptr(group_ids), _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream_handle(stream),
+        ctypes.byref(trace) if trace is not None else None))
+
+
+def parrot_validate_prefill_inputs(problem, rows, query_offsets, prefix_block_tables, prefix_lens,
+                                   prefix_parents, suffix_block_tables, suffix_lens, group_ids,
+                                   scratch, stream=None):
+    """Device-side content check of a prefill call's inputs (synchronises)."""
+    lib = load_library()
+    _check(lib.parrot_validate_prefill_inputs(
+        ctypes.byref(problem), ctypes.byref(rows), _ptr(query_offsets), _ptr(prefix_block_tables),
+        _ptr(prefix_lens), _ptr(prefix_parents), _ptr(suffix_block_tables), _ptr(suffix_lens),
+        _ptr(group_ids), _ptr(scratch), _stream_handle(stream)))
+
+
 def problem_from_host(*, num_heads, head_dim, block_size, dtype, sm_scale, group_ids, prefix_lens,
                       suffix_lens, prefix_table_stride, suffix_table_stride, num_prefix_blocks,
                       num_suffix_blocks, prefix_parents=None) -> ParrotProblem:
@@ -328,4 +403,44 @@ class Decoder:
                 t["prefix_tables"], t["prefix_lens"], t["suffix_tables"], t["suffix_lens"],
                 t["group_ids"], self.out, self.lse, self.workspace, stream=stream, trace=trace,
                 prefix_parents=t.get("prefix_parents") if nested else None)
+        return self.out, self.lse
+
+
+class Prefiller:
+    """Owns the output, lse and workspace buffers of one prefill shape."""
+
+    def __init__(self, problem: ParrotProblem, rows: ParrotPrefillRows, device="cuda"):
+        self.problem = problem
+        self.rows = rows
+        self.device = torch.device(device)
+        inv = {v: k for k, v in DTYPE_CODES.items()}
+        self.dtype = inv[problem.dtype]
+        T, H, D = rows.num_query_rows, problem.num_heads, problem.head_dim
+        self.out = torch.empty((T, H, D), dtype=self.dtype, device=self.device)
+        self.lse = torch.empty((T, H), dtype=torch.float32, device=self.device)
+        nbytes = parrot_prefill_workspace_bytes(problem, rows)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+
+    def bind(self, t: dict, stream=None, nested: bool = False):
+        """Marshal once; the returned callable re-issues the same call.  ``t``
+        holds q_rows, query_offsets, the pools (k_pool / v_pool or
+        prefix_k ... suffix_v) and the int arrays; ``nested`` passes
+        t["prefix_parents"]."""
+        fn = load_library().parrot_shared_prefix_prefill
+        ws = self.workspace
+        args = (ctypes.byref(self.problem), ctypes.byref(self.rows), _ptr(t["q_rows"]),
+                _ptr(t["query_offsets"]), _ptr(t.get("prefix_k", t.get("k_pool"))),
+                _ptr(t.get("prefix_v", t.get("v_pool"))), _ptr(t.get("suffix_k", t.get("k_pool"))),
+                _ptr(t.get("suffix_v", t.get("v_pool"))), _ptr(t["prefix_tables"]),
+                _ptr(t["prefix_lens"]), _ptr(t["prefix_parents"]) if nested else None,
+                _ptr(t["suffix_tables"]), _ptr(t["suffix_lens"]), _ptr(t["group_ids"]),
+                _ptr(self.out), _ptr(self.lse), _ptr(ws), ws.numel() * ws.element_size(),
+                _stream_handle(stream))
+
+        def call(trace: Optional[ParrotTrace] = None):
+            _check(fn(*args, ctypes.byref(trace) if trace is not None else None))
+        return call
+
+    def __call__(self, t: dict, stream=None, trace=None, nested: bool = False):
+        self.bind(t, stream=stream, nested=nested)(trace)
         return self.out, self.lse

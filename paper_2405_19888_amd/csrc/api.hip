@@ -366,12 +366,202 @@ parrot_status parrot_nested_prefix_decode(
 
 namespace {
 
+// ------------------------------------------------------------------ prefill
+constexpr int kPrefillChunkMax = 8192;   // the prefill tile's table holds 512 blocks
+constexpr int kPrefillChunkMin = 256;
+
+struct PrefillPlan {
+  int depth, cp, co, seg_p, seg_pre, seg_s, seg, qtiles_p, qtiles_o;
+  long n_pre, n_own;
+  size_t o_bytes, lse_bytes, info_bytes, total_bytes;
+};
+
+// Chunk of a key range of at most `len` tokens: the whole range up to 8192
+// tokens (fewest partial results), halved while the items of that chunk size
+// (`items_per_chunk` per chunk) would not give every CU two workgroups.
+int prefill_chunk(long len, double items_per_chunk) {
+  int c = kPrefillChunkMax;
+  while (c > kPrefillChunkMin && c / 2 >= len) c /= 2;
+  const double cus = num_cus();
+  while (c > kPrefillChunkMin && items_per_chunk * (double)ceil_div(len, c) < 2 * cus) c /= 2;
+  return c;
+}
+
+parrot_status check_prefill(const parrot_problem* p, const parrot_prefill_rows* rows, bool nested,
+                            PrefillPlan* pl) {
+  if (!p) return fail(PARROT_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (!rows) return fail(PARROT_ERR_INVALID_ARGUMENT, "rows is NULL");
+  // the decode checks, with the group bound that prefill replaces by rows
+  parrot_problem d = *p;
+  if (d.num_groups > 0) d.max_group_size = d.num_requests > 0 ? 1 : d.max_group_size;
+  parrot::Plan dpl;
+  PARROT_TRY(check_problem(&d, &dpl));
+  *pl = PrefillPlan{};
+  const long T = rows->num_query_rows;
+  if (T < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_query_rows %ld < 0", T);
+  if (T == 0) return PARROT_OK;
+  if (p->num_requests == 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "num_query_rows %ld > 0 with no requests", T);
+  const int mq = rows->max_query_rows;
+  if (mq < 1 || mq > p->max_suffix_len)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "max_query_rows %d not in [1, max_suffix_len = %d]", mq,
+                p->max_suffix_len);
+  if ((long)p->num_requests * mq < T)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "num_query_rows %ld > num_requests * max_query_rows", T);
+  const int mg = p->num_groups > 0 ? rows->max_group_rows : 0;
+  if (mg < 0 || mg > T)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "max_group_rows %d not in [0, num_query_rows]", mg);
+  if (T * p->num_heads > 0x7fffffffL)
+    return fail(PARROT_ERR_UNSUPPORTED, "num_query_rows * num_heads > 2^31 - 1");
+  const int H = p->num_heads;
+  pl->depth = p->num_groups > 0 ? (nested ? std::max(1, (int)p->max_prefix_depth) : 1) : 0;
+  pl->qtiles_p = (int)ceil_div(mg, 64);
+  pl->qtiles_o = (int)ceil_div(mq, 64);
+  if (p->num_groups > 0 && pl->qtiles_p > 0) {
+    pl->cp = prefill_chunk(p->max_prefix_len, (double)p->num_groups * H * pl->qtiles_p);
+    pl->seg_p = (int)ceil_div(p->max_prefix_len, pl->cp);
+  } else {
+    pl->cp = kPrefillChunkMin;
+    pl->seg_p = 0;
+  }
+  if (pl->seg_p > 0xFFFF)
+    return fail(PARROT_ERR_UNSUPPORTED, "max_prefix_len %d needs %d prefix chunks (at most 65535)",
+                p->max_prefix_len, pl->seg_p);
+  pl->co = prefill_chunk(p->max_suffix_len, (double)p->num_requests * H * pl->qtiles_o);
+  pl->seg_s = (int)ceil_div(p->max_suffix_len, pl->co);
+  pl->seg_pre = pl->depth * pl->seg_p;
+  pl->seg = pl->seg_pre + pl->seg_s;
+  pl->n_pre = (long)p->num_groups * pl->seg_p * H * pl->qtiles_p;
+  pl->n_own = (long)p->num_requests * pl->seg_s * H * pl->qtiles_o;
+  if (pl->n_pre + pl->n_own > 0x7fffffffL)
+    return fail(PARROT_ERR_UNSUPPORTED, "prefill needs %ld work items (at most 2^31 - 1)", pl->n_pre + pl->n_own);
+  const size_t n_slots = (size_t)T * H * pl->seg;
+  auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
+  pl->lse_bytes = align256(n_slots * sizeof(float));
+  pl->info_bytes = align256((size_t)T * parrot::kMetaInts * sizeof(int32_t));
+  pl->total_bytes = pl->o_bytes + pl->lse_bytes + pl->info_bytes;
+  return PARROT_OK;
+}
+
+parrot_status prefill(const parrot_problem* p, const parrot_prefill_rows* rows, const void* q,
+                      const int32_t* qoff, const void* prefix_k, const void* prefix_v,
+                      const void* suffix_k, const void* suffix_v, const int32_t* ptab,
+                      const int32_t* plen, const int32_t* parents, const int32_t* stab,
+                      const int32_t* slen, const int32_t* gid, void* out, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream,
+                      const parrot_trace* trace) {
+  PrefillPlan pl;
+  PARROT_TRY(check_prefill(p, rows, parents != nullptr, &pl));
+  if (rows->num_query_rows == 0) {
+    g_err.clear();
+    return PARROT_OK;
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const parrot_trace none = {nullptr, nullptr, nullptr, nullptr};
+  const parrot_trace& tr = trace ? *trace : none;
+  struct { const void* ptr; const char* name; size_t align; } req[] = {
+      {q, "q", 16}, {qoff, "query_offsets", 4}, {suffix_k, "suffix_k", 16},
+      {suffix_v, "suffix_v", 16}, {stab, "suffix_block_tables", 4}, {slen, "suffix_lens", 4},
+      {gid, "group_ids", 4}, {out, "out", 16}, {lse, "lse", 4}, {workspace, "workspace", 256}};
+  for (auto& r : req) {
+    if (!r.ptr) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", r.name);
+    if (!aligned(r.ptr, r.align)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", r.name, r.align);
+  }
+  if (p->num_groups > 0) {
+    struct { const void* ptr; const char* name; size_t align; } preq[] = {
+        {prefix_k, "prefix_k", 16}, {prefix_v, "prefix_v", 16},
+        {ptab, "prefix_block_tables", 4}, {plen, "prefix_lens", 4}};
+    for (auto& r : preq) {
+      if (!r.ptr) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is NULL", r.name);
+      if (!aligned(r.ptr, r.align)) return fail(PARROT_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", r.name, r.align);
+    }
+    if (parents && !aligned(parents, 4)) return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_parents is not 4-byte aligned");
+  }
+  if (workspace_bytes < pl.total_bytes)
+    return fail(PARROT_ERR_WORKSPACE_TOO_SMALL, "workspace is %zu bytes, need %zu", workspace_bytes, pl.total_bytes);
+
+  float* o_part = reinterpret_cast<float*>(workspace);
+  float* lse_part = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + pl.o_bytes);
+  int* merge_meta = reinterpret_cast<int*>(reinterpret_cast<char*>(workspace) + pl.o_bytes + pl.lse_bytes);
+  const int T = rows->num_query_rows;
+  {
+    parrot::PrefillArgs a{};
+    a.q = q; a.pk = prefix_k; a.pv = prefix_v; a.sk = suffix_k; a.sv = suffix_v;
+    a.ptab = ptab; a.plen = plen; a.stab = stab; a.slen = slen; a.gid = gid;
+    a.parents = p->num_groups > 0 ? parents : nullptr; a.qoff = qoff;
+    a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
+    a.T = T; a.R = p->num_requests; a.H = p->num_heads; a.NG = p->num_groups;
+    a.depth = std::max(1, pl.depth);
+    a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
+    a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len; a.max_q = rows->max_query_rows;
+    a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.seg_pre = pl.seg_pre; a.seg_s = pl.seg_s;
+    a.cp = pl.cp; a.co = pl.co; a.qtiles_p = pl.qtiles_p; a.qtiles_o = pl.qtiles_o;
+    a.n_pre = (int)pl.n_pre; a.n_own = (int)pl.n_own;
+    a.meta_wgs = (T + 255) / 256;
+    a.scale_log2 = p->sm_scale * parrot::kLog2e;
+    PARROT_TRY(launched(parrot::launch_prefill(a, (int)p->dtype, p->head_dim, s, ev(tr.partials_start),
+                                               ev(tr.partials_stop)),
+                        "prefill kernel"));
+  }
+  {
+    parrot::MergeArgs a{};
+    a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
+    a.out = out; a.lse = lse;
+    a.R = T; a.H = p->num_heads;
+    a.seg = pl.seg; a.seg_p = pl.seg_p; a.seg_pre = pl.seg_pre;
+    PARROT_TRY(launched(parrot::launch_merge(a, (int)p->dtype, p->head_dim, s, ev(tr.merge_start),
+                                             ev(tr.merge_stop)),
+                        "merge kernel"));
+  }
+  g_err.clear();
+  return PARROT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t parrot_prefill_workspace_bytes(const parrot_problem* p, const parrot_prefill_rows* rows) {
+  PrefillPlan pl;
+  // sized for nested groups (depth max_prefix_depth): enough for flat calls too
+  if (check_prefill(p, rows, true, &pl) != PARROT_OK) return (size_t)-1;
+  g_err.clear();
+  return pl.total_bytes;
+}
+
+parrot_status parrot_shared_prefix_prefill(
+    const parrot_problem* p, const parrot_prefill_rows* rows, const void* q,
+    const int32_t* query_offsets, const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v, const int32_t* prefix_block_tables,
+    const int32_t* prefix_lens, const int32_t* prefix_parents,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens, const int32_t* group_ids,
+    void* out, float* lse, void* workspace, size_t workspace_bytes, void* stream,
+    const parrot_trace* trace) {
+  return prefill(p, rows, q, query_offsets, prefix_k, prefix_v, suffix_k, suffix_v,
+                 prefix_block_tables, prefix_lens, prefix_parents, suffix_block_tables,
+                 suffix_lens, group_ids, out, lse, workspace, workspace_bytes, stream, trace);
+}
+
+}  // extern "C"
+
+namespace {
+
 parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tables,
                        const int32_t* prefix_lens, const int32_t* prefix_parents,
                        const int32_t* suffix_block_tables, const int32_t* suffix_lens,
-                       const int32_t* group_ids, int32_t* scratch, void* stream) {
+                       const int32_t* group_ids, int32_t* scratch, void* stream,
+                       const parrot_prefill_rows* rows = nullptr,
+                       const int32_t* query_offsets = nullptr) {
   parrot::Plan pl;
-  PARROT_TRY(check_problem(p, &pl));
+  if (rows) {
+    PrefillPlan fp;
+    PARROT_TRY(check_prefill(p, rows, prefix_parents != nullptr, &fp));
+    if (!query_offsets || !aligned(query_offsets, 4))
+      return fail(PARROT_ERR_INVALID_ARGUMENT, "query_offsets is NULL or misaligned");
+  } else {
+    PARROT_TRY(check_problem(p, &pl));
+  }
   if (p->num_requests == 0) { g_err.clear(); return PARROT_OK; }
   if (!scratch || !aligned(scratch, 4)) return fail(PARROT_ERR_INVALID_ARGUMENT, "scratch is NULL or misaligned");
   if (!suffix_block_tables || !suffix_lens || !group_ids)
@@ -390,6 +580,10 @@ parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tabl
   a.pstride = p->prefix_table_stride; a.sstride = p->suffix_table_stride;
   a.max_p = p->max_prefix_len; a.max_s = p->max_suffix_len;
   a.npblk = p->num_prefix_blocks; a.nsblk = p->num_suffix_blocks;
+  if (rows) {
+    a.qoff = query_offsets; a.T = rows->num_query_rows;
+    a.max_q = rows->max_query_rows; a.max_grp = rows->max_group_rows;
+  }
   PARROT_TRY(launched(parrot::launch_validate(a, s), "validation kernel"));
   int32_t res[3] = {0, 0, 0};
   e = hipMemcpyAsync(res, scratch, sizeof res, hipMemcpyDeviceToHost, s);
@@ -400,10 +594,13 @@ parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tabl
                                "prefix block id out of [0, num_prefix_blocks)",
                                "suffix block id out of [0, num_suffix_blocks)",
                                "prefix parent not in [-1, group)",
-                               "prefix chain deeper than max_prefix_depth"};
+                               "prefix chain deeper than max_prefix_depth",
+                               "query_offsets not 0 = offsets[0] <= ... <= offsets[R] = num_query_rows",
+                               "query rows of a request > min(suffix length, max_query_rows)",
+                               "rows reading a group's prefix > max_group_rows"};
   if (res[0] != 0)
     return fail(PARROT_ERR_INVALID_ARGUMENT, "%s at entry %d (value %d)",
-                (res[0] > 0 && res[0] <= 8) ? what[res[0]] : "unknown", res[1], res[2]);
+                (res[0] > 0 && res[0] <= 11) ? what[res[0]] : "unknown", res[1], res[2]);
   g_err.clear();
   return PARROT_OK;
 }
@@ -429,6 +626,18 @@ parrot_status parrot_validate_nested_inputs(const parrot_problem* p, const int32
     return fail(PARROT_ERR_INVALID_ARGUMENT, "prefix_parents is NULL");
   return validate(p, prefix_block_tables, prefix_lens, prefix_parents, suffix_block_tables,
                   suffix_lens, group_ids, scratch, stream);
+}
+
+parrot_status parrot_validate_prefill_inputs(const parrot_problem* p, const parrot_prefill_rows* rows,
+                                             const int32_t* query_offsets,
+                                             const int32_t* prefix_block_tables,
+                                             const int32_t* prefix_lens, const int32_t* prefix_parents,
+                                             const int32_t* suffix_block_tables,
+                                             const int32_t* suffix_lens, const int32_t* group_ids,
+                                             int32_t* scratch, void* stream) {
+  if (!rows) return fail(PARROT_ERR_INVALID_ARGUMENT, "rows is NULL");
+  return validate(p, prefix_block_tables, prefix_lens, prefix_parents, suffix_block_tables,
+                  suffix_lens, group_ids, scratch, stream, rows, query_offsets);
 }
 
 const char* parrot_last_error(void) { return g_err.c_str(); }

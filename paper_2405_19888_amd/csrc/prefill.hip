@@ -1,0 +1,233 @@
+// Prefill of forked contexts: the new rows of each request against its
+// group's shared prefix (and the prefixes of the group's ancestors) and,
+// causally, against its own tokens (Section 7: Fill with a parent context
+// fills only the new tokens on top of the parent's KV cache).
+//
+// The work splits the same way as decode, with many query rows per request:
+//
+//   prefix items (g, chunk c, head h, row tile qt): the rows of every request
+//     that reads g's prefix, stacked in request order, 64 per tile, against
+//     chunk c of the prefix.  No mask: every prefix token precedes every row.
+//     The chunk is streamed from HBM once per tile of 64 rows drawn from all
+//     of the group's members (one read for the whole group when it has at
+//     most 64 rows).
+//   own items (r, chunk k, head h, row tile t): 64 consecutive rows of request
+//     r against its own tokens [k*co, (k+1)*co), each row cut after its own
+//     position.
+//
+// Both kinds run tile_core (MFMA QK^T and PV over LDS-staged 16-token blocks)
+// and write one partial result per (row, head, item); the decode merge kernel
+// then combines them per row, reading the row descriptors that the first
+// workgroups write.  Work items are spread so that the items a workgroup runs
+// after another on the same XCD share a key chunk (row tiles are the fastest
+// index), which keeps that chunk in the XCD's L2.
+#include "prefix_role.h"
+
+namespace parrot {
+
+constexpr int kPrefillMaxBlocks = 512;                       // chunk <= 8192 tokens
+constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks);
+constexpr int kXcds = 8;                                     // workgroups go round-robin over XCDs
+
+// Work item of workgroup `bid` of `n`: XCD x (bid % 8) runs a contiguous range
+// of items, in launch order.  A bijection of [0, n).
+PARROT_DEV int xcd_item(int bid, int n) {
+  const int x = bid % kXcds, l = bid / kXcds;
+  const int per = n / kXcds, rem = n % kXcds;
+  return x * per + min(x, rem) + l;
+}
+
+struct ReqRows { int start, count, S; };
+
+// Rows of request r, clamped so that every row index stays in [0, T) and a
+// request has at most min(S_r, max_q) rows (the launch covers no more).
+PARROT_DEV ReqRows req_rows(const PrefillArgs& a, int r) {
+  const int S = clampi(a.slen[r], 0, a.max_s);
+  const int start = clampi(a.qoff[r], 0, a.T);
+  const long n = (long)a.qoff[r + 1] - (long)a.qoff[r];
+  const int cap = min(min(S, a.max_q), a.T - start);
+  return {start, (int)(n < 0 ? 0 : (n > cap ? cap : n)), S};
+}
+
+// Row descriptor for the merge: own-chunk slots and the prefix chunks per
+// level of the row's chain (the decode descriptor, per row).  Rows that no
+// request holds get an empty descriptor (output 0, lse -inf).
+PARROT_DEV void write_row_meta(const PrefillArgs& a, int t) {
+  int lo = 0, hi = a.R - 1, r = -1;          // last request with qoff[r] <= t
+  while (lo <= hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a.qoff[mid] <= t) { r = mid; lo = mid + 1; } else { hi = mid - 1; }
+  }
+  int4 m = {0, 0, 0, 0};
+  if (r >= 0) {
+    const ReqRows rw = req_rows(a, r);
+    if (t >= rw.start && t < rw.start + rw.count) {
+      const int pos = rw.S - rw.count + (t - rw.start);
+      int np[kMaxDepth] = {0, 0, 0, 0};
+      int chain[kMaxDepth];
+      int nlev = 0;
+      int x = a.gid[r];
+      while (x >= 0 && x < a.NG && nlev < a.depth) {
+        chain[nlev++] = x;
+        x = a.parents ? a.parents[x] : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kMaxDepth; ++i)
+        if (i < nlev) np[nlev - 1 - i] = (clampi(a.plen[chain[i]], 0, a.max_p) + a.cp - 1) / a.cp;
+      m = int4{pos / a.co + 1, nlev, (int)((unsigned)np[0] | ((unsigned)np[1] << 16)),
+               (int)((unsigned)np[2] | ((unsigned)np[3] << 16))};
+    }
+  }
+  *reinterpret_cast<int4*>(a.merge_meta + kMetaInts * t) = m;
+}
+
+// Prefix item: chunk c of group g's prefix for row tile qt of the rows that
+// read it, head h.
+template <int DT, int D>
+__device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* lds, int item) {
+  const int qt = item % a.qtiles_p; item /= a.qtiles_p;
+  const int h = item % a.H; item /= a.H;
+  const int c = item % a.seg_p;
+  const int g = item / a.seg_p;
+  if (g >= a.NG) return;
+  const int P = clampi(a.plen[g], 0, a.max_p);
+  const int t0 = c * a.cp;
+  if (t0 >= P) return;
+  const int t1 = min(P, t0 + a.cp);
+  int lvl = 0;                                         // ancestors of g (< depth)
+  if (a.parents) {
+    int x = a.parents[g];
+    while (x >= 0 && x < a.NG && lvl < a.depth - 1) { ++lvl; x = a.parents[x]; }
+  }
+  const TileLds tl(lds, kPrefillMaxBlocks);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const long qbase = (long)qt * 64;
+  const int b0 = t0 / kBlock, nb = (t1 - t0 + kBlock - 1) / kBlock;
+  if (wave == 0) {
+    // rows of the requests that read g's prefix, in request order; this tile
+    // takes rows [qbase, qbase + 64) of that list
+    long base = 0;
+    for (int b = 0; b < a.R && base < qbase + 64; b += kWave) {
+      const int r = b + lane;
+      bool reads = false;
+      if (r < a.R) {
+        int x = a.gid[r];
+        for (int d = 0; d < a.depth && x >= 0 && x < a.NG; ++d) {
+          if (x == g) { reads = true; break; }
+          x = a.parents ? a.parents[x] : -1;
+        }
+      }
+      ReqRows rw = {0, 0, 0};
+      if (reads) rw = req_rows(a, r);
+      long inc = rw.count;                             // inclusive scan over lanes
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) {
+        const long v = __shfl_up(inc, d);
+        if (lane >= d) inc += v;
+      }
+      const long first = base + inc - rw.count;
+      const long lo = first > qbase ? first : qbase;
+      const long hi = min(first + rw.count, qbase + 64);
+      for (long x = lo; x < hi; ++x) tl.rows[x - qbase] = rw.start + (int)(x - first);
+      base += __shfl(inc, kWave - 1);
+    }
+    if (lane == 0) *tl.count = (int)(base - qbase > 64 ? 64 : (base - qbase < 0 ? 0 : base - qbase));
+  } else if (wave == 1) {
+    const int* tbl = a.ptab + (long)g * a.pstride;
+    for (int i = lane; i < nb; i += kWave) tl.tbl[i] = clampi(tbl[b0 + i], 0, a.npblk - 1);
+  }
+  __syncthreads();
+  const int nq = *tl.count;
+  if (nq <= 0) return;                                 // uniform over the workgroup
+  TileJob j;
+  j.q = a.q; j.pk = a.pk; j.pv = a.pv; j.H = a.H; j.h = h;
+  j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
+  j.seg = a.seg; j.slot = lvl * a.seg_p + c; j.scale_log2 = a.scale_log2;
+  tile_core<DT, D, false>(j, tl, nq);
+}
+
+// Own item: own tokens [k*co, (k+1)*co) of request r for its row tile t,
+// head h; row i of the tile sees own tokens up to its position.
+template <int DT, int D>
+__device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds, int item) {
+  const int t = item % a.qtiles_o; item /= a.qtiles_o;
+  const int h = item % a.H; item /= a.H;
+  const int k = item % a.seg_s;
+  const int r = item / a.seg_s;
+  if (r >= a.R) return;
+  const ReqRows rw = req_rows(a, r);
+  const int row0 = t * 64;
+  if (row0 >= rw.count) return;
+  const int nq = min(64, rw.count - row0);
+  const int pos0 = rw.S - rw.count + row0;             // position of the tile's first row
+  const int t0 = k * a.co;
+  if (t0 > pos0 + nq - 1) return;
+  const int t1 = min(min(rw.S, t0 + a.co), pos0 + nq);
+  const TileLds tl(lds, kPrefillMaxBlocks);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int b0 = t0 / kBlock, nb = (t1 - t0 + kBlock - 1) / kBlock;
+  if (wave == 0) {
+    if (lane < nq) {
+      tl.rows[lane] = rw.start + row0 + lane;
+      tl.lim[lane] = pos0 + lane;
+    }
+  } else if (wave == 1) {
+    const int* tbl = a.stab + (long)r * a.sstride;
+    for (int i = lane; i < nb; i += kWave) tl.tbl[i] = clampi(tbl[b0 + i], 0, a.nsblk - 1);
+  }
+  __syncthreads();
+  TileJob j;
+  j.q = a.q; j.pk = a.sk; j.pv = a.sv; j.H = a.H; j.h = h;
+  j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
+  j.seg = a.seg; j.slot = a.seg_pre + k; j.scale_log2 = a.scale_log2;
+  tile_core<DT, D, true>(j, tl, nq);
+}
+
+template <int DT, int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+void k_prefill(PrefillArgs a) {
+  __shared__ __attribute__((aligned(1024))) char lds[kPrefillLds];
+  const int bid = blockIdx.x;
+  if (bid < a.meta_wgs) {
+    const int t = bid * 256 + (int)threadIdx.x;
+    if (t < a.T) write_row_meta(a, t);
+  }
+  const int item = xcd_item(bid, (int)gridDim.x);
+  if (item < a.n_pre)
+    prefill_prefix_item<DT, D>(a, lds, item);
+  else if (item - a.n_pre < a.n_own)
+    prefill_own_item<DT, D>(a, lds, item - a.n_pre);
+}
+
+template <int DT, int D>
+static hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const long items = (long)a.n_pre + a.n_own;
+  const long blocks = items > a.meta_wgs ? items : a.meta_wgs;
+  if (blocks <= 0) return hipSuccess;
+  hipExtLaunchKernelGGL((k_prefill<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+  if (a.R > kMaxRequests || a.R < 1 || a.T < 1 || a.H < 1 || a.seg_s < 1 || a.qtiles_o < 1)
+    return hipErrorInvalidValue;
+  if (a.cp % 32 != 0 || a.co % 32 != 0 || a.cp > kPrefillMaxBlocks * kBlock ||
+      a.co > kPrefillMaxBlocks * kBlock || a.cp < 32 || a.co < 32)
+    return hipErrorInvalidValue;
+  if (a.meta_wgs != (a.T + 255) / 256 || (long)a.n_pre + a.n_own > 0x7fffffffL)
+    return hipErrorInvalidValue;
+  switch (dtype * 1000 + D) {
+    case kF32 * 1000 + 64: return launch_prefill_t<kF32, 64>(a, s, e0, e1);
+    case kF32 * 1000 + 128: return launch_prefill_t<kF32, 128>(a, s, e0, e1);
+    case kF16 * 1000 + 64: return launch_prefill_t<kF16, 64>(a, s, e0, e1);
+    case kF16 * 1000 + 128: return launch_prefill_t<kF16, 128>(a, s, e0, e1);
+    case kBF16 * 1000 + 64: return launch_prefill_t<kBF16, 64>(a, s, e0, e1);
+    case kBF16 * 1000 + 128: return launch_prefill_t<kBF16, 128>(a, s, e0, e1);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace parrot

@@ -100,30 +100,57 @@ template <> struct Mfma<kBF16> {
 }  // namespace prefix_detail
 
 constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
-// LDS bytes the prefix role needs: the stage ring, members, block ids, count.
-constexpr int kPrefixLds = prefix_detail::kRing * prefix_detail::kStageBytes +
-                           (kPrefixWaves * 16 + prefix_detail::kMaxChunkBlocks + 4) * 4;
+// LDS bytes of a query tile whose key range spans up to `blocks` blocks: the
+// stage ring, the tile's query rows, the key block ids, a count, and the rows'
+// last visible key (causal tiles).
+constexpr int tile_lds_bytes(int blocks) {
+  return prefix_detail::kRing * prefix_detail::kStageBytes + (2 * kPrefixWaves * 16 + blocks + 4) * 4;
+}
+constexpr int kPrefixLds = tile_lds_bytes(prefix_detail::kMaxChunkBlocks);
+
+// LDS views shared by the tile's set-up code and tile_core.
+struct TileLds {
+  char (*smem)[prefix_detail::kStageBytes];   // [kRing][kStageBytes]
+  int* rows;                                  // [64] query row of each tile column
+  int* tbl;                                   // [blocks] key blocks, clamped
+  int* count;                                 // set-up scratch
+  int* lim;                                   // [64] last visible key token (causal)
+  PARROT_DEV explicit TileLds(char* lds, int blocks = prefix_detail::kMaxChunkBlocks)
+      : smem(reinterpret_cast<char (*)[prefix_detail::kStageBytes]>(lds)),
+        rows(reinterpret_cast<int*>(lds + prefix_detail::kRing * prefix_detail::kStageBytes)),
+        tbl(rows + kPrefixWaves * 16),
+        count(tbl + blocks),
+        lim(count + 4) {}
+};
+
+// One query tile against one range of a paged key sequence.
+struct TileJob {
+  const void* q;                  // [rows][H][D]
+  const void* pk; const void* pv; // pools of the key sequence
+  int H, h;
+  int t0, t1;                     // key tokens [t0, t1); t0 a multiple of 16
+  float* o_part; float* lse_part; // partial results [rows][H][seg][D], [rows][H][seg]
+  int seg, slot;                  // slots per (row, head); this tile's slot
+  float scale_log2;
+};
+
+// The attention core of a query tile: up to 64 query rows (tl.rows, nq of
+// them) against key tokens [t0, t1) whose blocks are in tl.tbl; with CAUSAL,
+// row i sees only keys up to tl.lim[i].  Rows and blocks must be in LDS and
+// visible to every wave.  Writes one partial result (normalised output and
+// base-2 log-sum-exp; a row that sees no key gets 0 and -inf) per row.
+template <int DT, int D, bool CAUSAL>
+__device__ __forceinline__ void tile_core(const TileJob& j, const TileLds& tl, int nq);
 
 // One workgroup of the prefix role; `wg` is the role-local workgroup index.
 template <int DT, int D>
 __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int wg) {
   using namespace prefix_detail;
   constexpr int W = kPrefixWaves;
-  using E = Elem<DT>;
-  constexpr int ROW_B = D * E::kBytes;
-  constexpr int GRAN = ROW_B / 16;                    // 16-byte granules per row
-  constexpr int BLK_B = kBlock * ROW_B;               // one block of one head
-  constexpr int STAGE_BLK = kTensorStage / BLK_B;     // blocks per stage
-  constexpr int DT16 = D / 16;                        // 16-wide d tiles
-  constexpr int KS = (DT == kF32) ? D / 4 : D / 32;   // MFMA k-steps over D
-  constexpr int PER_WAVE = kStageChunks / W;          // direct-to-LDS loads per wave per stage
-  static_assert(STAGE_BLK >= 1 && GRAN >= 8, "stage holds a block; swizzle fits a row");
-  static_assert(kStageChunks % W == 0, "stage chunks split evenly over waves");
-
-  auto smem = reinterpret_cast<char (*)[kStageBytes]>(lds);                 // [kRing][kStageBytes]
-  int* members = reinterpret_cast<int*>(lds + kRing * kStageBytes);        // [W * 16]
-  int* s_tbl = members + W * 16;                                           // [kMaxChunkBlocks]
-  int& s_count = s_tbl[kMaxChunkBlocks];
+  const TileLds tl(lds);
+  int* members = tl.rows;
+  int* s_tbl = tl.tbl;
+  int& s_count = tl.count[0];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -180,6 +207,37 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   __syncthreads();
   const int nq = min(s_count - qbase, W * 16);
   if (nq <= 0) return;                                 // uniform over the workgroup
+  TileJob job;
+  job.q = a.q; job.pk = a.pk; job.pv = a.pv; job.H = H; job.h = h;
+  job.t0 = t0; job.t1 = t1; job.o_part = a.o_part; job.lse_part = a.lse_part;
+  job.seg = a.seg; job.slot = lvl * a.seg_p + c; job.scale_log2 = a.scale_log2;
+  tile_core<DT, D, false>(job, tl, nq);
+}
+
+template <int DT, int D, bool CAUSAL>
+__device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, int nq) {
+  using namespace prefix_detail;
+  constexpr int W = kPrefixWaves;
+  using E = Elem<DT>;
+  constexpr int ROW_B = D * E::kBytes;
+  constexpr int GRAN = ROW_B / 16;                    // 16-byte granules per row
+  constexpr int BLK_B = kBlock * ROW_B;               // one block of one head
+  constexpr int STAGE_BLK = kTensorStage / BLK_B;     // blocks per stage
+  constexpr int DT16 = D / 16;                        // 16-wide d tiles
+  constexpr int KS = (DT == kF32) ? D / 4 : D / 32;   // MFMA k-steps over D
+  constexpr int PER_WAVE = kStageChunks / W;          // direct-to-LDS loads per wave per stage
+  static_assert(STAGE_BLK >= 1 && GRAN >= 8, "stage holds a block; swizzle fits a row");
+  static_assert(kStageChunks % W == 0, "stage chunks split evenly over waves");
+
+  auto smem = tl.smem;
+  const int* members = tl.rows;
+  const int* s_tbl = tl.tbl;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = a.H, h = a.h, t1 = a.t1;
+  const int b0 = a.t0 / kBlock;
+  const int nb = (a.t1 - a.t0 + kBlock - 1) / kBlock;
 
   const int qi = wave * 16 + (lane & 15);              // this lane's query column
   const bool has_q = wave * 16 < nq;                   // wave-uniform
@@ -263,20 +321,25 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
     return s4;
   };
   // masked, scaled logits of the lane's 4 tokens of block `blk` (chunk-relative)
+  const int lim = CAUSAL ? (q_ok ? tl.lim[qi] : -1) : 0;
   auto logits = [&](const f32x4& s4, int blk, float* s) {
     const int tok_base = (b0 + blk) * kBlock + 4 * (lane >> 4);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s[i] = (tok_base + i < t1) ? s4[i] * a.scale_log2 : -INFINITY;
+    for (int i = 0; i < 4; ++i) {
+      const bool vis = (tok_base + i < t1) && (!CAUSAL || tok_base + i <= lim);
+      s[i] = vis ? s4[i] * a.scale_log2 : -INFINITY;
+    }
   };
   // online-softmax update with n logits per lane; returns the probabilities
   auto update = [&](float* s, float* p, int n) {
     float bm = s[0];
     for (int i = 1; i < n; ++i) bm = fmaxf(bm, s[i]);
     bm = max_xor32(max_xor16(bm));
-    const float mn = fmaxf(m, bm);                   // finite: every block has a token
-    const float alpha = fast_exp2(m - mn);
+    const float mn = fmaxf(m, bm);                   // -inf only for a causal row that sees nothing yet
+    const float mref = (CAUSAL && mn == -INFINITY) ? 0.f : mn;
+    const float alpha = fast_exp2(m - mref);
     float ps = 0.f;
-    for (int i = 0; i < n; ++i) { p[i] = fast_exp2(s[i] - mn); ps += p[i]; }
+    for (int i = 0; i < n; ++i) { p[i] = fast_exp2(s[i] - mref); ps += p[i]; }
     lsum = lsum * alpha + ps;
 #pragma unroll
     for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
@@ -300,10 +363,11 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
           float bm = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
           bm = max_xor32(max_xor16(bm));
           const float mn = fmaxf(m, bm);
-          const float alpha = fast_exp2(m - mn);
+          const float mref = (CAUSAL && mn == -INFINITY) ? 0.f : mn;
+          const float alpha = fast_exp2(m - mref);
           float ps = 0.f;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) { p[i] = fast_exp2(s[i] - mn); ps += p[i]; }
+          for (int i = 0; i < 8; ++i) { p[i] = fast_exp2(s[i] - mref); ps += p[i]; }
           lsum = lsum * alpha + ps;
 #pragma unroll
           for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
@@ -392,12 +456,12 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   float lt = sum_xor16(lsum);
   lt = sum_xor32(lt);
   if (q_ok) {
-    const size_t slot = (size_t)(rq * H + h) * a.seg + lvl * a.seg_p + c;
-    const float inv = 1.f / lt;
+    const size_t slot = (size_t)(rq * H + h) * a.seg + a.slot;
+    const float inv = (CAUSAL && lt == 0.f) ? 0.f : 1.f / lt;
     float* dst = a.o_part + slot * D + 4 * (lane >> 4);
 #pragma unroll
     for (int dt = 0; dt < DT16; ++dt) *reinterpret_cast<f32x4*>(dst + dt * 16) = o[dt] * inv;
-    if (lane < 16) a.lse_part[slot] = m + fast_log2(lt);
+    if (lane < 16) a.lse_part[slot] = (CAUSAL && lt == 0.f) ? -INFINITY : m + fast_log2(lt);
   }
 }
 

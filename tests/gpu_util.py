@@ -81,3 +81,41 @@ def assert_close(out, lse, ref_out, ref_lse, dtype: str, what: str = ""):
     assert err <= tol, f"{what}: max |out err| {err:.3e} > {tol:.1e}"
     assert lerr <= LSE_RTOL, f"{what}: max lse rel err {lerr:.3e} > {LSE_RTOL:.0e}"
     return err, lerr
+
+
+def prefill_rows_for(plan, offsets):
+    from paper_2405_19888_amd import prefill_rows_from_host
+    return prefill_rows_from_host(offsets, plan.group_ids, plan.num_groups,
+                                  plan.prefix_parents if plan.nested else None)
+
+
+def run_prefill(plan, dev: dict, offsets, problem=None, rows=None, poison: bool = True,
+                nested: bool = None):
+    """Validate the prefill inputs on the device, poison outputs and
+    workspace, run the prefill entry point, sync."""
+    from paper_2405_19888_amd import Prefiller, parrot_validate_prefill_inputs
+    nested = plan.nested if nested is None else nested
+    prob = problem or problem_for(plan)
+    rows = rows or prefill_rows_for(plan, offsets)
+    pre = Prefiller(prob, rows)
+    scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
+    parrot_validate_prefill_inputs(prob, rows, dev["query_offsets"], dev["prefix_tables"],
+                                   dev["prefix_lens"], dev["prefix_parents"] if nested else None,
+                                   dev["suffix_tables"], dev["suffix_lens"], dev["group_ids"],
+                                   scratch)
+    if poison:
+        pre.out.fill_(float("nan"))
+        pre.lse.fill_(float("nan"))
+        pre.workspace.fill_(0xFF)
+    out, lse = pre(dev, nested=nested)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def oracle_prefill_for(batch, plan, q_rows, offsets, rows=None, pools=None):
+    kp = pools[0] if pools else batch.k_pool
+    vp = pools[1] if pools else batch.v_pool
+    return oracle.shared_prefix_prefill(
+        q_rows.cpu(), offsets, kp, vp, kp, vp, plan.prefix_tables, plan.prefix_lens,
+        plan.suffix_tables, plan.suffix_lens, plan.group_ids, plan.sm_scale, rows=rows,
+        prefix_parents=plan.prefix_parents if plan.nested else None)

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 2
+    assert B.parrot_abi_version() == 3
 
 
 def base_problem(**over):
@@ -47,6 +47,7 @@ def base_problem(**over):
 def test_struct_layout_matches_header():
     assert ctypes.sizeof(B.ParrotProblem) == 15 * 4
     assert ctypes.sizeof(B.ParrotTrace) == 4 * ctypes.sizeof(ctypes.c_void_p)
+    assert ctypes.sizeof(B.ParrotPrefillRows) == 3 * 4
 
 
 def test_workspace_sizes(parrot_lib):
@@ -180,3 +181,89 @@ def test_missing_library_fails_loudly(tmp_path):
             B.load_library(str(tmp_path / "nope.so"))
         finally:
             B._lib = B._lib_saved
+
+
+# ------------------------------------------------------------------ prefill
+def prefill_rows(**over):
+    kw = dict(num_query_rows=32 * 256, max_query_rows=256, max_group_rows=32 * 256)
+    kw.update(over)
+    return B.make_prefill_rows(**kw)
+
+
+def prefill_call(lib, prob, rows, **ptrs):
+    names = ["q", "qoff", "pk", "pv", "sk", "sv", "ptab", "plen", "parents", "stab", "slen",
+             "gid", "out", "lse", "ws"]
+    vals = {n: FAKE + 4096 * i for i, n in enumerate(names)}
+    vals.update(ptrs)
+    ws_bytes = ptrs.get("ws_bytes", 1 << 40)
+    vals.pop("ws_bytes", None)
+    return lib.parrot_shared_prefix_prefill(ctypes.byref(prob), ctypes.byref(rows),
+                                            *[vals[n] for n in names], ws_bytes, None, None)
+
+
+def test_prefill_workspace_sizes(parrot_lib):
+    prob = base_problem()
+    assert B.parrot_prefill_workspace_bytes(prob, prefill_rows(num_query_rows=0)) == 0
+    w = B.parrot_prefill_workspace_bytes(prob, prefill_rows())
+    # at least one prefix slot and one own slot per (row, head), D + 1 floats
+    # each, plus a 16-byte descriptor per row
+    T, H, D = 32 * 256, 32, 128
+    assert w >= T * H * 2 * (D + 1) * 4 + T * 16
+    assert B.parrot_prefill_workspace_bytes(prob, prefill_rows(num_query_rows=32 * 128,
+                                                               max_query_rows=128,
+                                                               max_group_rows=32 * 128)) < w
+    # nested groups need a slot range per level
+    assert B.parrot_prefill_workspace_bytes(base_problem(max_prefix_depth=3), prefill_rows()) > w
+
+
+@pytest.mark.parametrize("over,msg", [
+    (dict(num_query_rows=-1), "num_query_rows"),
+    (dict(max_query_rows=0), "max_query_rows"),
+    (dict(max_query_rows=513), "max_query_rows"),
+    (dict(num_query_rows=32 * 256 + 1, max_group_rows=0), "num_query_rows"),
+    (dict(max_group_rows=32 * 256 + 1), "max_group_rows"),
+    (dict(max_group_rows=-1), "max_group_rows"),
+])
+def test_prefill_bad_rows_rejected(parrot_lib, over, msg):
+    with pytest.raises(B.ParrotError) as e:
+        B.parrot_prefill_workspace_bytes(base_problem(), prefill_rows(**over))
+    assert msg in str(e.value)
+    st = prefill_call(parrot_lib, base_problem(), prefill_rows(**over))
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT and msg in B.parrot_last_error()
+
+
+def test_prefill_ignores_max_group_size(parrot_lib):
+    """Prefill bounds group rows through max_group_rows instead."""
+    w = B.parrot_prefill_workspace_bytes(base_problem(max_group_size=0), prefill_rows())
+    assert w == B.parrot_prefill_workspace_bytes(base_problem(), prefill_rows())
+
+
+@pytest.mark.parametrize("field", ["q", "qoff", "sk", "sv", "stab", "slen", "gid", "out", "lse",
+                                   "ws", "pk", "pv", "ptab", "plen"])
+def test_prefill_null_pointer_rejected(parrot_lib, field):
+    st = prefill_call(parrot_lib, base_problem(), prefill_rows(), **{field: None})
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT and "NULL" in B.parrot_last_error()
+
+
+def test_prefill_parents_optional_but_aligned(parrot_lib):
+    prob, rows = base_problem(), prefill_rows()
+    need = B.parrot_prefill_workspace_bytes(prob, rows)
+    assert prefill_call(parrot_lib, prob, rows, parents=FAKE + 2) == B.PARROT_ERR_INVALID_ARGUMENT
+    assert "aligned" in B.parrot_last_error()
+    st = prefill_call(parrot_lib, prob, rows, parents=None, ws_bytes=need - 1)
+    assert st == B.PARROT_ERR_WORKSPACE_TOO_SMALL and str(need) in B.parrot_last_error()
+
+
+def test_prefill_no_rows_is_ok_without_device(parrot_lib):
+    st = prefill_call(parrot_lib, base_problem(), prefill_rows(num_query_rows=0), q=None,
+                      out=None, lse=None, ws=None, ws_bytes=0)
+    assert st == B.PARROT_OK and B.parrot_last_error() == ""
+
+
+def test_prefill_rows_from_host():
+    off = [0, 3, 3, 10, 12]
+    rows = B.prefill_rows_from_host(off, group_ids=[0, 1, 1, -1], num_groups=2,
+                                    prefix_parents=[-1, 0])
+    assert (rows.num_query_rows, rows.max_query_rows, rows.max_group_rows) == (12, 7, 10)
+    flat = B.prefill_rows_from_host(off, group_ids=[0, 1, 1, -1], num_groups=2)
+    assert flat.max_group_rows == 7

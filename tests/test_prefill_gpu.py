@@ -1,0 +1,155 @@
+"""GPU parity for the prefill of forked contexts: each request's new rows
+against its group chain's prefixes and, causally, its own tokens, through
+the C ABI, against the float64 oracle.
+
+Every case prints its name before touching the GPU, validates the device
+inputs (row offsets included) before the call, and NaN-poisons outputs and
+workspace first; unused cache slots hold NaN.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import (assert_close, oracle_prefill_for, prefill_rows_for, problem_for,
+                      run_prefill, to_np)
+from workloads import build_plan, make_batch, make_prefill_queries
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ["float16", "bfloat16", "float32"]
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def prefill_case(kind, dtype, D, seed=0):
+    """(plan, per-request row counts)."""
+    rng = np.random.default_rng(seed)
+    scale = 1.0 / math.sqrt(D)
+    if kind == "mixed":
+        # groups of several sizes, ungrouped requests, whole prompts, chunks of
+        # prompts, no rows; own lengths across several 256-token chunks
+        gor = [0] * 5 + [1] * 3 + [2] + [-1] * 3
+        sl = [1, 17, 300, 64, 0, 33, 520, 7, 129, 700, 1, 65]
+        qr = [1, 17, 100, 64, 0, 5, 520, 0, 129, 300, 1, 64]
+        plan = build_plan(heads=3, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
+                          prefix_lens=[700, 33, 1], suffix_lens=sl, sm_scale=scale,
+                          shuffle=True, rng=rng)
+        return plan, [qr[i] for i in plan_order(plan, sl)]
+    if kind == "wide_group":
+        # 150+ rows read one prefix: three row tiles that cut through requests
+        gor = [0] * 9
+        sl = [40, 1, 70, 16, 17, 2, 33, 64, 9]
+        plan = build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
+                          prefix_lens=[1100], suffix_lens=sl, sm_scale=scale, shuffle=True, rng=rng)
+        return plan, list(plan.suffix_lens)
+    if kind == "nested":
+        # 0 <- 1 <- 3, 0 <- 2; members at every level, one ungrouped
+        gor = [3, 3, 1, 2, 2, 0, -1, 1]
+        sl = [90, 5, 130, 1, 64, 20, 300, 0]
+        plan = build_plan(heads=4, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
+                          prefix_lens=[600, 48, 257, 16], prefix_parents=[-1, 0, 0, 1],
+                          suffix_lens=sl, sm_scale=scale, shuffle=True, rng=rng)
+        return plan, [min(int(s), 70) for s in plan.suffix_lens]
+    if kind == "long_rows":
+        # one request with many row tiles and own chunks, next to a short one
+        plan = build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype,
+                          group_of_request=[0, 0], prefix_lens=[300], suffix_lens=[1000, 3],
+                          sm_scale=scale, rng=rng)
+        return plan, [1000, 3]
+    if kind == "single":
+        plan = build_plan(heads=1, head_dim=D, block_size=16, dtype=dtype, group_of_request=[-1],
+                          prefix_lens=[], suffix_lens=[1], sm_scale=scale, rng=rng)
+        return plan, [1]
+    raise ValueError(kind)
+
+
+def plan_order(plan, sl):
+    """Map the drawn (shuffled) requests back to the row recipe: request r of
+    the plan has suffix length sl[i] for the returned i (first unused match)."""
+    used, out = set(), []
+    for s in plan.suffix_lens:
+        i = next(j for j, x in enumerate(sl) if x == int(s) and j not in used)
+        used.add(i)
+        out.append(i)
+    return out
+
+
+def device_dict(batch, q, off):
+    dev = batch.to("cuda")
+    dev["q_rows"] = q.to("cuda")
+    dev["query_offsets"] = torch.from_numpy(np.ascontiguousarray(off)).to("cuda")
+    return dev
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("kind", ["mixed", "wide_group", "nested", "long_rows", "single"])
+def test_prefill_parity(kind, dtype, D):
+    say("prefill", kind, dtype, D)
+    plan, qr = prefill_case(kind, dtype, D)
+    batch = make_batch(plan, seed=5)
+    q, off = make_prefill_queries(plan, qr, seed=5)
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off)
+    ref = oracle_prefill_for(batch, plan, q, off)
+    assert_close(*to_np(out, lse), *ref, dtype, f"prefill {kind} {dtype} D={D}")
+
+
+def test_prefill_rows_as_decode():
+    """One row per request at its last own token is a decode step: the prefill
+    result equals the decode entry point's on the same queries."""
+    from gpu_util import run_gpu
+    say("prefill one row per request vs decode")
+    plan, _ = prefill_case("mixed", "float16", 128)
+    batch = make_batch(plan, seed=2)
+    qr = [1 if int(s) > 0 else 0 for s in plan.suffix_lens]
+    q, off = make_prefill_queries(plan, qr, seed=2)
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off)
+    have = [r for r in range(plan.num_requests) if qr[r]]
+    qd = batch.q.clone()
+    for i, r in enumerate(have):
+        qd[r] = q[i]
+    dev = batch.to("cuda")
+    dev["q"] = qd.to("cuda")
+    dout, dlse = run_gpu(plan, dev)
+    o, l = to_np(out, lse)
+    do, dl = to_np(dout, dlse)
+    assert np.max(np.abs(o - do[have])) <= 2e-3
+    assert np.max(np.abs(l - dl[have]) / np.maximum(1, np.abs(dl[have]))) <= 1e-4
+
+
+def test_prefill_validation_catches_bad_rows():
+    from paper_2405_19888_amd import ParrotError, parrot_validate_prefill_inputs
+    say("prefill validation")
+    plan, qr = prefill_case("mixed", "float16", 64)
+    batch = make_batch(plan)
+    q, off = make_prefill_queries(plan, qr)
+    prob = problem_for(plan)
+    rows = prefill_rows_for(plan, off)
+    scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
+    dev = device_dict(batch, q, off)
+
+    def check(offsets, rows_=rows, msg=""):
+        d = dict(dev, query_offsets=torch.from_numpy(np.asarray(offsets, np.int32)).to("cuda"))
+        with pytest.raises(ParrotError, match=msg):
+            parrot_validate_prefill_inputs(prob, rows_, d["query_offsets"], d["prefix_tables"],
+                                           d["prefix_lens"], None, d["suffix_tables"],
+                                           d["suffix_lens"], d["group_ids"], scratch)
+    bad = off.copy()
+    bad[0] = 1
+    check(bad, msg="query_offsets")
+    # a request below the longest own length gets one row more than its own
+    # tokens (the row bound on the host still holds)
+    r = int(np.argmin(np.where(plan.suffix_lens > 0, plan.suffix_lens, 1 << 30)))
+    bad = off.copy()
+    bad[r + 1:] += int(plan.suffix_lens[r]) - qr[r] + 1       # one row more than own tokens
+    from paper_2405_19888_amd import make_prefill_rows
+    check(bad, make_prefill_rows(int(bad[-1]), int(np.diff(bad).max()), rows.max_group_rows + 600),
+          msg="suffix length")
+    check(off, make_prefill_rows(rows.num_query_rows, rows.max_query_rows,
+                                 rows.max_group_rows - 1), msg="max_group_rows")
