@@ -11,6 +11,11 @@ still in the 256 MB Infinity Cache when it is read again.  A multi-layer
 workload (`--config c5`: 32 LLaMA-7B layers) cycles through all of its own
 layers instead, and a step is one layer of it.
 
+After the decode line's measurements, a prefill leg (`--prefill`, default the
+Fill of 64 contexts forked from a 6000-token system prompt) times
+parrot_shared_prefix_prefill and reports it under "prefill" with an MFMA
+roofline; `--mode prefill` prints only that leg as the line.
+
 Prints one JSON line.  `value` is requests per second per layer
 (R / seconds per step).  The `roofline` object describes the dominant kernel
 (the partial-result kernel) from HIP events attached to its launches on the
@@ -108,6 +113,175 @@ def cpu_baseline(plan, layer_dev, budget_s: float):
     }
 
 
+def prefill_work(plan, query_rows):
+    """Keys seen by all rows of a prefill call, split into prefix and own keys.
+    Row j of request r sits at own position p = S_r - Q_r + j and sees the
+    chain's prefix tokens plus own tokens 0..p."""
+    pre = own = 0
+    for r in range(plan.num_requests):
+        g = int(plan.group_ids[r])
+        P = plan.chain_prefix_len(g) if g >= 0 else 0
+        S, Q = int(plan.suffix_lens[r]), int(query_rows[r])
+        pre += Q * P
+        own += S * (S + 1) // 2 - (S - Q) * (S - Q + 1) // 2
+    return pre, own
+
+
+def cpu_prefill_baseline(plan, q_rows, offsets, layer_dev, budget_s: float):
+    """The oracle on host copies of one layer, one prefill row at a time, for
+    ~budget_s (rows drawn at random over the whole batch)."""
+    import numpy as np
+    import oracle
+
+    q = q_rows.cpu()
+    kp = layer_dev["k_pool"].cpu()
+    vp = layer_dev["v_pool"].cpu()
+    T = int(offsets[-1])
+    order = np.random.default_rng(0).permutation(T)
+    t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
+    done = 0
+    while True:
+        t = int(order[done % T])
+        oracle.shared_prefix_prefill(q, offsets, kp, vp, kp, vp, plan.prefix_tables,
+                                     plan.prefix_lens, plan.suffix_tables, plan.suffix_lens,
+                                     plan.group_ids, plan.sm_scale, rows=[t],
+                                     prefix_parents=plan.prefix_parents if plan.nested else None)
+        done += 1
+        wall = time.perf_counter() - t_wall0
+        if wall >= budget_s:
+            break
+    cpu = time.process_time() - t_cpu0
+    return {
+        "value": done / wall,
+        "unit": "rows/s per layer",
+        "cores": max(1, int(round(cpu / wall))),
+        "cores_available": len(os.sched_getaffinity(0)),
+        "kind": "oracle",
+        "sample": f"{done} random query rows of one layer of the same workload, one oracle "
+                  f"call each, {wall:.1f} s wall, {cpu:.1f} s CPU",
+    }
+
+
+def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines: bool,
+                cpu_budget: float) -> dict:
+    """Time parrot_shared_prefix_prefill on a prefill workload: `steps` calls,
+    each one layer's Fill of every request's new rows, cycling `n_layers`
+    distinct-KV layers.  Returns the leg's JSON object."""
+    import numpy as np
+    import torch
+    from paper_2405_19888_amd import ParrotTrace, Prefiller, parrot_validate_prefill_inputs
+    from paper_2405_19888_amd import prefill_rows_from_host, problem_from_host
+    from workloads import (get_config, make_device_layer, make_device_prefill_queries, make_plan,
+                           one_group_per_request, prefill_rows)
+    from workloads.gen import TORCH_DTYPES
+
+    cfg = get_config(cfg_name)
+    if cfg.prefill_rows is None:
+        raise SystemExit(f"{cfg_name} is not a prefill workload")
+    plan = make_plan(cfg)
+    qr = prefill_rows(plan, cfg.prefill_rows, None)
+    dev = "cuda"
+    layers = []
+    for l in range(n_layers):
+        t = make_device_layer(plan, l, dev, seed=cfg.seed)
+        t["q_rows"], t["query_offsets"] = make_device_prefill_queries(plan, qr, dev, cfg.seed, l)
+        layers.append(t)
+    offsets = layers[0]["query_offsets"].cpu().numpy()
+
+    def setup(p):
+        prob = problem_from_host(
+            num_heads=p.heads, head_dim=p.head_dim, block_size=p.block_size,
+            dtype=TORCH_DTYPES[p.dtype], sm_scale=p.sm_scale, group_ids=p.group_ids,
+            prefix_lens=p.prefix_lens, suffix_lens=p.suffix_lens,
+            prefix_table_stride=p.prefix_tables.shape[1],
+            suffix_table_stride=p.suffix_tables.shape[1],
+            num_prefix_blocks=p.num_blocks, num_suffix_blocks=p.num_blocks,
+            prefix_parents=p.prefix_parents if p.nested else None)
+        rows = prefill_rows_from_host(offsets, p.group_ids, p.num_groups,
+                                      p.prefix_parents if p.nested else None)
+        return prob, rows
+
+    prob, rows = setup(plan)
+    scratch = torch.zeros(16, dtype=torch.int32, device=dev)
+    t0 = layers[0]
+    parrot_validate_prefill_inputs(prob, rows, t0["query_offsets"], t0["prefix_tables"],
+                                   t0["prefix_lens"], t0["prefix_parents"] if plan.nested else None,
+                                   t0["suffix_tables"], t0["suffix_lens"], t0["group_ids"], scratch)
+    pre = Prefiller(prob, rows, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(calls, trace: bool):
+        events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)] \
+            if trace else []
+        for evs in events:
+            for e in evs:
+                e.record(stream)
+        torch.cuda.synchronize()
+        traces = [ParrotTrace(*[e.cuda_event for e in evs]) for evs in events]
+        for i in range(warmup):
+            calls[i % len(calls)]()
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for i in range(steps):
+            calls[i % len(calls)](traces[i] if trace else None)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        per = None
+        if trace:
+            per = {"prefill_us": sum(e[0].elapsed_time(e[1]) for e in events) * 1e3 / steps,
+                   "merge_us": sum(e[2].elapsed_time(e[3]) for e in events) * 1e3 / steps}
+        return wall, per
+
+    calls = [pre.bind(t, stream=stream, nested=plan.nested) for t in layers]
+    wall, per = timed(calls, trace=False)
+    _, per = timed(calls, trace=True)
+    T = int(offsets[-1])
+    pre_keys, own_keys = prefill_work(plan, qr)
+    flops = 4 * plan.head_dim * plan.heads * (pre_keys + own_keys)
+    achieved = flops / (per["prefill_us"] * 1e-6) / 1e12
+    out = {
+        "metric": "prefill query rows/sec per layer",
+        "value": round(T / (wall / steps), 1), "unit": "rows/s",
+        "steps": steps, "warmup": warmup, "ms_per_step": round(wall / steps * 1e3, 5),
+        "dtype": DTYPE_TAG[plan.dtype],
+        "config": {"workload": cfg.name, "requests": plan.num_requests, "rows": T,
+                   "heads": plan.heads, "head_dim": plan.head_dim,
+                   "prefix_lens": [int(x) for x in plan.prefix_lens],
+                   "rows_per_request_mean": round(float(np.mean(qr)), 1),
+                   "own_len_mean": round(float(plan.suffix_lens.mean()), 1),
+                   "layers_cycled": n_layers},
+        "roofline": {
+            "kernel": "k_prefill (prefix items + causal own items, MFMA)",
+            "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
+            "traffic": None, "algorithmic_flops": flops,
+            "avg_us": round(per["prefill_us"], 3),
+        },
+        "kernels_us": {k: round(v, 3) for k, v in per.items()},
+        "tflops_step": round(flops / (wall / steps) / 1e12, 1),
+    }
+    if baselines:
+        # no sharing: each request its own group (same kernels and blocks)
+        solo = one_group_per_request(plan)
+        sprob, srows = setup(solo)
+        spre = Prefiller(sprob, srows, device=dev)
+        ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+                for k, v in (("prefix_tables", solo.prefix_tables), ("prefix_lens", solo.prefix_lens),
+                             ("group_ids", solo.group_ids))}
+        scalls = [spre.bind(dict(t, **ints), stream=stream) for t in layers]
+        wall_s, _ = timed(scalls, trace=False)
+        out["per_request_baseline"] = {
+            "value": round(T / (wall_s / steps), 1), "unit": "rows/s",
+            "ms_per_step": round(wall_s / steps * 1e3, 5),
+            "speedup_of_shared": round(wall_s / wall, 3),
+            "note": "the same entry point with one group per request (prefix rows not stacked "
+                    "across requests)",
+        }
+        out["cpu_baseline"] = cpu_prefill_baseline(plan, layers[0]["q_rows"], offsets, layers[0],
+                                                   cpu_budget)
+    return out
+
+
 def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
     """Read + write GB/s of a plain device-to-device copy (a ceiling for
     bandwidth-bound kernels on this device, measured in the same process)."""
@@ -154,12 +328,25 @@ def main():
     ap.add_argument("--trace-every", type=int, default=16,
                     help="attach per-kernel HIP events to every N-th timed step (each traced "
                          "launch costs a few microseconds of stream time)")
+    ap.add_argument("--prefill", default="prefill",
+                    help="prefill workload timed after the decode line ('none' to skip)")
+    ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--mode", choices=("decode", "prefill"), default="decode",
+                    help="prefill: time only the prefill workload (--prefill) and print its line")
     args = ap.parse_args()
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU: run with --gpus 1 "
                                    "(no multi-GPU path exists)"}))
         sys.exit(2)
+
+    if args.mode == "prefill":
+        leg = prefill_leg(args.prefill, args.steps, args.warmup, min(args.layers, 4),
+                          not args.no_baselines, args.cpu_budget)
+        leg.update(n_gpus=1, higher_is_better=True, scaling="weak", vs_baseline=None,
+                   data="synthetic")
+        print(json.dumps(leg), flush=True)
+        return
 
     import numpy as np
     import torch
@@ -373,6 +560,11 @@ def main():
             "hbm_gbps": round(ab["naive_total"] / (wall_n / K) / 1e9, 1),
         }
         result["cpu_baseline"] = cpu_baseline(plan, layers[0], args.cpu_budget)
+    if args.prefill != "none":
+        # the Fill step of the same kind of batch: every forked context's own
+        # prompt rows against the shared prefix (its own line object)
+        result["prefill"] = prefill_leg(args.prefill, args.prefill_steps, 3, 2,
+                                        not args.no_baselines, min(args.cpu_budget, 10.0))
     print(json.dumps(result), flush=True)
 
 

@@ -1,4 +1,5 @@
-"""The five synthetic decode workloads, plus the prefix-length sweep.
+"""The five synthetic decode workloads, a nested one, two prefill workloads,
+plus the prefix-length sweep.
 
 Each workload is one continuous-batching decode iteration (one query per
 request) over a paged KV cache, shaped after the model sizes and sharing
@@ -61,6 +62,8 @@ class ConfigSpec:
     paged: bool = True              # False: identity block tables (contiguous KV)
     shuffle_requests: bool = True   # interleave group members in the batch
     seed: int = 0
+    prefill_rows: object = None     # prefill workloads: rows per request ("all", n or a
+                                    # fraction of S_r; see gen.prefill_rows); None = decode
 
     @property
     def num_requests(self) -> int:
@@ -129,6 +132,21 @@ CONFIGS: dict[str, ConfigSpec] = {
         group_sizes=(0,) + (8,) * 8, prefix_parents=(-1,) + (0,) * 8,
         prefix_len=("list", [6000] + [256] * 8),
         suffix_len=("uniform", 64, 512), sm_scale=_INV_SQRT128),
+    "prefill_sys6000_g64": ConfigSpec(
+        name="prefill_sys6000_g64",
+        description="Fill of 64 contexts forked from a 6000-token system prompt, "
+                    "LLaMA-7B layer: 32 heads x 128, fp16 paged; each fills its "
+                    "own prompt of U[100,1000] tokens (every own token a query row)",
+        layers=1, heads=32, head_dim=128, block_size=16, dtype="float16",
+        group_sizes=(64,), prefix_len=("fixed", 6000),
+        suffix_len=("uniform", 100, 1000), sm_scale=_INV_SQRT128, prefill_rows="all"),
+    "prefill_sys6000_g64_q16": ConfigSpec(
+        name="prefill_sys6000_g64_q16",
+        description="as prefill_sys6000_g64, but each context fills only its last "
+                    "16 own tokens (a continued, chunked prompt)",
+        layers=1, heads=32, head_dim=128, block_size=16, dtype="float16",
+        group_sizes=(64,), prefix_len=("fixed", 6000),
+        suffix_len=("uniform", 100, 1000), sm_scale=_INV_SQRT128, prefill_rows=16),
 }
 
 # Short aliases in the order the workloads are listed (C1..C5).
@@ -136,6 +154,7 @@ ALIASES = {
     "c1": "tiny", "c2": "llama7b_g32_p2048", "c3": "sysprompt_g64_p6000",
     "c4": "mapreduce_13b_4x32", "c5": "mixed_7b_32layer",
     "nested": "nested_sys6000_8x8_fs256",
+    "prefill": "prefill_sys6000_g64", "prefill_q16": "prefill_sys6000_g64_q16",
 }
 
 

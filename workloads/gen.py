@@ -278,6 +278,22 @@ def flatten_nested(plan: LayoutPlan) -> LayoutPlan:
                    prefix_tables=ptab, prefix_parents=None)
 
 
+def one_group_per_request(plan: LayoutPlan) -> LayoutPlan:
+    """The same batch with no sharing: every grouped request gets a group of
+    its own holding its whole chain of prefixes (same physical blocks, so the
+    chain's outer prefixes must fill whole blocks, as for ``flatten_nested``).
+    A baseline: the shared-prefix kernels then read each prefix once per
+    request."""
+    flat = flatten_nested(plan) if plan.nested else plan
+    members = [r for r in range(flat.num_requests) if flat.group_ids[r] >= 0]
+    src = [int(flat.group_ids[r]) for r in members]
+    gid = np.full(flat.num_requests, -1, dtype=np.int32)
+    gid[members] = np.arange(len(members), dtype=np.int32)
+    ptab = flat.prefix_tables[src] if members else flat.prefix_tables[:0]
+    return replace(flat, group_ids=gid, prefix_lens=flat.prefix_lens[src].astype(np.int32),
+                   prefix_tables=np.ascontiguousarray(ptab), prefix_parents=None)
+
+
 @dataclass
 class DecodeBatch:
     """One layer of one decode iteration: a plan plus its values (CPU tensors)."""
@@ -400,3 +416,17 @@ def make_prefill_queries(plan: LayoutPlan, query_rows: Sequence[int], seed: int 
     if plan.q_scale != 1.0:
         q.mul_(plan.q_scale)
     return q.to(TORCH_DTYPES[plan.dtype]), off
+
+
+def make_device_prefill_queries(plan: LayoutPlan, query_rows: Sequence[int], device,
+                                seed: int = 0, layer: int = 0):
+    """Device-drawn prefill rows (torch Philox on ``device``, seed
+    seed * 1000003 + 7919 * layer + 104729): (q_rows, offsets as int32 tensor)."""
+    off = query_offsets_for(plan, query_rows)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1_000_003 + 7919 * int(layer) + 104_729)
+    q = torch.randn((int(off[-1]), plan.heads, plan.head_dim), generator=g, device=device,
+                    dtype=torch.float32)
+    if plan.q_scale != 1.0:
+        q.mul_(plan.q_scale)
+    return q.to(TORCH_DTYPES[plan.dtype]), torch.from_numpy(off).to(device)
