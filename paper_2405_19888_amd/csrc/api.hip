@@ -414,8 +414,9 @@ parrot_status check_prefill(const parrot_problem* p, const parrot_prefill_rows* 
     return fail(PARROT_ERR_UNSUPPORTED, "num_query_rows * num_heads > 2^31 - 1");
   const int H = p->num_heads;
   pl->depth = p->num_groups > 0 ? (nested ? std::max(1, (int)p->max_prefix_depth) : 1) : 0;
-  pl->qtiles_p = (int)ceil_div(mg, 64);
-  pl->qtiles_o = (int)ceil_div(mq, 64);
+  const int rows_per_tile = p->dtype == PARROT_DTYPE_F32 ? 64 : 128;   // the kernel's tile height
+  pl->qtiles_p = (int)ceil_div(mg, rows_per_tile);
+  pl->qtiles_o = (int)ceil_div(mq, rows_per_tile);
   if (p->num_groups > 0 && pl->qtiles_p > 0) {
     pl->cp = prefill_chunk(p->max_prefix_len, (double)p->num_groups * H * pl->qtiles_p);
     pl->seg_p = (int)ceil_div(p->max_prefix_len, pl->cp);
@@ -430,10 +431,13 @@ parrot_status check_prefill(const parrot_problem* p, const parrot_prefill_rows* 
   pl->seg_s = (int)ceil_div(p->max_suffix_len, pl->co);
   pl->seg_pre = pl->depth * pl->seg_p;
   pl->seg = pl->seg_pre + pl->seg_s;
-  pl->n_pre = (long)p->num_groups * pl->seg_p * H * pl->qtiles_p;
-  pl->n_own = (long)p->num_requests * pl->seg_s * H * pl->qtiles_o;
-  if (pl->n_pre + pl->n_own > 0x7fffffffL)
-    return fail(PARROT_ERR_UNSUPPORTED, "prefill needs %ld work items (at most 2^31 - 1)", pl->n_pre + pl->n_own);
+  // work items per head (the grid holds them for every head, 8 heads apart
+  // per XCD)
+  pl->n_pre = (long)p->num_groups * pl->seg_p * pl->qtiles_p;
+  pl->n_own = (long)p->num_requests * pl->seg_s * pl->qtiles_o;
+  const long grid = 8L * ceil_div(H, 8) * (pl->n_pre + pl->n_own);
+  if (grid > 0x7fffffffL)
+    return fail(PARROT_ERR_UNSUPPORTED, "prefill needs %ld workgroups (at most 2^31 - 1)", grid);
   const size_t n_slots = (size_t)T * H * pl->seg;
   auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));

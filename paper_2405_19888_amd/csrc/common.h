@@ -108,7 +108,7 @@ struct PrefillArgs {
   int seg, seg_p, seg_pre, seg_s;
   int cp, co;            // prefix and own chunk tokens
   int qtiles_p, qtiles_o;   // 64-row tiles per group, per request
-  int n_pre, n_own;      // prefix-chunk and own-chunk work items
+  int n_pre, n_own;      // prefix-chunk and own-chunk work items per head
   int meta_wgs;          // workgroups that also write the row descriptors (256 rows each)
   float scale_log2;
 };
@@ -222,6 +222,17 @@ PARROT_DEV void lds_dma16(const void* src, unsigned lds_base) {
       "global_load_lds_dwordx4 %1, off"
       :
       : "s"(lds_base), "v"(src)
+      : "memory", "m0");
+}
+// The same load in the instruction's scalar-base form: a wave-uniform 64-bit
+// base plus a per-lane 32-bit byte offset (lane l reads base + voff).
+PARROT_DEV void lds_dma16_sbase(const void* base, unsigned voff, unsigned lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2"
+      :
+      : "s"(lds_base), "v"(voff), "s"(base)
       : "memory", "m0");
 }
 #pragma clang diagnostic pop

@@ -6,36 +6,36 @@
 // The work splits the same way as decode, with many query rows per request:
 //
 //   prefix items (g, chunk c, head h, row tile qt): the rows of every request
-//     that reads g's prefix, stacked in request order, 64 per tile, against
-//     chunk c of the prefix.  No mask: every prefix token precedes every row.
-//     The chunk is streamed from HBM once per tile of 64 rows drawn from all
-//     of the group's members (one read for the whole group when it has at
-//     most 64 rows).
-//   own items (r, chunk k, head h, row tile t): 64 consecutive rows of request
-//     r against its own tokens [k*co, (k+1)*co), each row cut after its own
-//     position.
+//     that reads g's prefix, stacked in request order, one tile of rows at a
+//     time, against chunk c of the prefix.  No mask: every prefix token
+//     precedes every row.  The chunk is streamed once per tile of rows drawn
+//     from all of the group's members (once for the whole group when its rows
+//     fit one tile).
+//   own items (r, chunk k, head h, row tile t): one tile of consecutive rows
+//     of request r against its own tokens [k*co, (k+1)*co), each row cut
+//     after its own position.
 //
-// Both kinds run tile_core (MFMA QK^T and PV over LDS-staged 16-token blocks)
-// and write one partial result per (row, head, item); the decode merge kernel
+// Tiles hold 128 rows on fp16 / bf16 caches (wide_tile) and 64 on fp32 caches
+// (decode's tile_core); both run QK^T and PV on MFMA over LDS-staged 16-token
+// blocks and write one partial result per (row, head, item); the decode merge kernel
 // then combines them per row, reading the row descriptors that the first
-// workgroups write.  Work items are spread so that the items a workgroup runs
-// after another on the same XCD share a key chunk (row tiles are the fastest
-// index), which keeps that chunk in the XCD's L2.
-#include "prefix_role.h"
+// workgroups write.
+//
+// Work items are placed per XCD (workgroup b runs on XCD b mod 8): XCD x takes
+// every item of heads x, x + 8, ..., one head after another, prefix items
+// before own items and row tiles fastest.  Each XCD then holds the same share
+// of the work, and the workgroups that run together on it read the same head's
+// key chunk, which stays in that XCD's L2.
+#include "prefill_tile.h"
 
 namespace parrot {
 
 constexpr int kPrefillMaxBlocks = 512;                       // chunk <= 8192 tokens
-constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks);
+// query rows per tile: the wide tile for 16-bit caches, decode's tile for fp32
+template <int DT> constexpr int kTileRows = DT == kF32 ? kPrefixWaves * 16 : kWideRows;
+constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks, kWideRows);
 constexpr int kXcds = 8;                                     // workgroups go round-robin over XCDs
 
-// Work item of workgroup `bid` of `n`: XCD x (bid % 8) runs a contiguous range
-// of items, in launch order.  A bijection of [0, n).
-PARROT_DEV int xcd_item(int bid, int n) {
-  const int x = bid % kXcds, l = bid / kXcds;
-  const int per = n / kXcds, rem = n % kXcds;
-  return x * per + min(x, rem) + l;
-}
 
 struct ReqRows { int start, count, S; };
 
@@ -84,9 +84,8 @@ PARROT_DEV void write_row_meta(const PrefillArgs& a, int t) {
 // Prefix item: chunk c of group g's prefix for row tile qt of the rows that
 // read it, head h.
 template <int DT, int D>
-__device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* lds, int item) {
+__device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* lds, int h, int item) {
   const int qt = item % a.qtiles_p; item /= a.qtiles_p;
-  const int h = item % a.H; item /= a.H;
   const int c = item % a.seg_p;
   const int g = item / a.seg_p;
   if (g >= a.NG) return;
@@ -99,16 +98,17 @@ __device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* 
     int x = a.parents[g];
     while (x >= 0 && x < a.NG && lvl < a.depth - 1) { ++lvl; x = a.parents[x]; }
   }
-  const TileLds tl(lds, kPrefillMaxBlocks);
+  constexpr int ROWS = kTileRows<DT>;
+  const TileLds tl(lds, kPrefillMaxBlocks, ROWS);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const long qbase = (long)qt * 64;
+  const long qbase = (long)qt * ROWS;
   const int b0 = t0 / kBlock, nb = (t1 - t0 + kBlock - 1) / kBlock;
   if (wave == 0) {
     // rows of the requests that read g's prefix, in request order; this tile
-    // takes rows [qbase, qbase + 64) of that list
+    // takes rows [qbase, qbase + ROWS) of that list
     long base = 0;
-    for (int b = 0; b < a.R && base < qbase + 64; b += kWave) {
+    for (int b = 0; b < a.R && base < qbase + ROWS; b += kWave) {
       const int r = b + lane;
       bool reads = false;
       if (r < a.R) {
@@ -128,11 +128,11 @@ __device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* 
       }
       const long first = base + inc - rw.count;
       const long lo = first > qbase ? first : qbase;
-      const long hi = min(first + rw.count, qbase + 64);
+      const long hi = min(first + rw.count, qbase + ROWS);
       for (long x = lo; x < hi; ++x) tl.rows[x - qbase] = rw.start + (int)(x - first);
       base += __shfl(inc, kWave - 1);
     }
-    if (lane == 0) *tl.count = (int)(base - qbase > 64 ? 64 : (base - qbase < 0 ? 0 : base - qbase));
+    if (lane == 0) *tl.count = (int)(base - qbase > ROWS ? ROWS : (base - qbase < 0 ? 0 : base - qbase));
   } else if (wave == 1) {
     const int* tbl = a.ptab + (long)g * a.pstride;
     for (int i = lane; i < nb; i += kWave) tl.tbl[i] = clampi(tbl[b0 + i], 0, a.npblk - 1);
@@ -143,35 +143,38 @@ __device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* 
   TileJob j;
   j.q = a.q; j.pk = a.pk; j.pv = a.pv; j.H = a.H; j.h = h;
   j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
-  j.seg = a.seg; j.slot = lvl * a.seg_p + c; j.scale_log2 = a.scale_log2;
-  tile_core<DT, D, false>(j, tl, nq);
+  j.seg = a.seg; j.slot = lvl * a.seg_p + c; j.scale_log2 = a.scale_log2; j.lim_min = 0;
+  if constexpr (DT == kF32)
+    tile_core<DT, D, false>(j, tl, nq);
+  else
+    wide_tile<DT, D, false>(j, tl, nq);
 }
 
 // Own item: own tokens [k*co, (k+1)*co) of request r for its row tile t,
 // head h; row i of the tile sees own tokens up to its position.
 template <int DT, int D>
-__device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds, int item) {
+__device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds, int h, int item) {
   const int t = item % a.qtiles_o; item /= a.qtiles_o;
-  const int h = item % a.H; item /= a.H;
   const int k = item % a.seg_s;
   const int r = item / a.seg_s;
   if (r >= a.R) return;
+  constexpr int ROWS = kTileRows<DT>;
   const ReqRows rw = req_rows(a, r);
-  const int row0 = t * 64;
+  const int row0 = t * ROWS;
   if (row0 >= rw.count) return;
-  const int nq = min(64, rw.count - row0);
+  const int nq = min(ROWS, rw.count - row0);
   const int pos0 = rw.S - rw.count + row0;             // position of the tile's first row
   const int t0 = k * a.co;
   if (t0 > pos0 + nq - 1) return;
   const int t1 = min(min(rw.S, t0 + a.co), pos0 + nq);
-  const TileLds tl(lds, kPrefillMaxBlocks);
+  const TileLds tl(lds, kPrefillMaxBlocks, ROWS);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b0 = t0 / kBlock, nb = (t1 - t0 + kBlock - 1) / kBlock;
   if (wave == 0) {
-    if (lane < nq) {
-      tl.rows[lane] = rw.start + row0 + lane;
-      tl.lim[lane] = pos0 + lane;
+    for (int i = lane; i < nq; i += kWave) {
+      tl.rows[i] = rw.start + row0 + i;
+      tl.lim[i] = pos0 + i;
     }
   } else if (wave == 1) {
     const int* tbl = a.stab + (long)r * a.sstride;
@@ -181,12 +184,17 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
   TileJob j;
   j.q = a.q; j.pk = a.sk; j.pv = a.sv; j.H = a.H; j.h = h;
   j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
-  j.seg = a.seg; j.slot = a.seg_pre + k; j.scale_log2 = a.scale_log2;
-  tile_core<DT, D, true>(j, tl, nq);
+  j.seg = a.seg; j.slot = a.seg_pre + k; j.scale_log2 = a.scale_log2; j.lim_min = pos0;
+  if constexpr (DT == kF32)
+    tile_core<DT, D, true>(j, tl, nq);
+  else
+    wide_tile<DT, D, true>(j, tl, nq);
 }
 
+// Occupancy: the wide tile keeps two column sets of accumulators (two waves
+// per SIMD, two workgroups per CU); decode's tile fits three.
 template <int DT, int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DT == kF32 ? 3 : 2, DT == kF32 ? 3 : 2)))
 void k_prefill(PrefillArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds[kPrefillLds];
   const int bid = blockIdx.x;
@@ -194,16 +202,21 @@ void k_prefill(PrefillArgs a) {
     const int t = bid * 256 + (int)threadIdx.x;
     if (t < a.T) write_row_meta(a, t);
   }
-  const int item = xcd_item(bid, (int)gridDim.x);
+  // XCD x, its l-th workgroup: head x + 8 (l / per), item l % per of that head
+  const int x = bid % kXcds, l = bid / kXcds;
+  const int per = a.n_pre + a.n_own;                   // items per head
+  const int j = l / per, item = l % per;
+  const int h = x + kXcds * j;
+  if (h >= a.H) return;
   if (item < a.n_pre)
-    prefill_prefix_item<DT, D>(a, lds, item);
-  else if (item - a.n_pre < a.n_own)
-    prefill_own_item<DT, D>(a, lds, item - a.n_pre);
+    prefill_prefix_item<DT, D>(a, lds, h, item);
+  else
+    prefill_own_item<DT, D>(a, lds, h, item - a.n_pre);
 }
 
 template <int DT, int D>
 static hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  const long items = (long)a.n_pre + a.n_own;
+  const long items = (long)kXcds * ((a.H + kXcds - 1) / kXcds) * ((long)a.n_pre + a.n_own);
   const long blocks = items > a.meta_wgs ? items : a.meta_wgs;
   if (blocks <= 0) return hipSuccess;
   hipExtLaunchKernelGGL((k_prefill<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
@@ -217,7 +230,8 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int D, hipStream_t s,
   if (a.cp % 32 != 0 || a.co % 32 != 0 || a.cp > kPrefillMaxBlocks * kBlock ||
       a.co > kPrefillMaxBlocks * kBlock || a.cp < 32 || a.co < 32)
     return hipErrorInvalidValue;
-  if (a.meta_wgs != (a.T + 255) / 256 || (long)a.n_pre + a.n_own > 0x7fffffffL)
+  if (a.meta_wgs != (a.T + 255) / 256 || a.n_pre < 0 || a.n_own < 1 ||
+      (long)kXcds * ((a.H + kXcds - 1) / kXcds) * ((long)a.n_pre + a.n_own) > 0x7fffffffL)
     return hipErrorInvalidValue;
   switch (dtype * 1000 + D) {
     case kF32 * 1000 + 64: return launch_prefill_t<kF32, 64>(a, s, e0, e1);

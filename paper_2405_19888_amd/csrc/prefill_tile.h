@@ -1,0 +1,277 @@
+// The prefill query tile on MFMA (gfx950, fp16 / bf16 caches): 128 query rows
+// against one range of a paged key sequence.
+//
+// Decode's prefix tile (tile_core) gives each wave 16 queries: enough to make
+// a bandwidth-bound prefix stream cheap, but a prefill tile is bound by the
+// matrix cores, and with 16 queries per wave the LDS reads of K and V, the
+// online softmax and the per-stage bookkeeping cost more than the MFMAs.  Here
+// each wave owns 32 queries as two 16-query column sets that share every K
+// and V fragment read from LDS, so one K read feeds two QK^T MFMAs and one
+// transposed V read feeds two PV MFMAs.  The rest follows tile_core:
+//   * K/V stages of 16 KiB (K and V of 32 tokens for D = 128, 64 for D = 64)
+//     fill a ring of three LDS buffers through direct-to-LDS loads, two stages
+//     ahead; the loads take a scalar base (pool + block * stride) and a
+//     per-lane offset, and each stage's two block ids are read from LDS one
+//     stage before they are needed, so issuing a stage waits on nothing;
+//   * S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_{f16,bf16}, the
+//     same XOR-swizzled LDS rows and ds_read_b64_tr_b16 reads of V^T;
+//   * online softmax in fp32 with a lazily moved reference: the exponentials
+//     use a reference max that is raised only when a row's max exceeds it by
+//     more than 8 (log2 units), so the accumulators are rescaled a few times
+//     per row instead of at every step, and probabilities stay below 2^8
+//     (exact enough in fp16 / bf16, whose relative precision does not depend
+//     on magnitude);
+//   * masking (the end of the key range, the causal diagonal) only in the
+//     stages that need it.
+#pragma once
+
+#include "prefix_role.h"
+
+namespace parrot {
+
+constexpr int kWideRows = 128;   // query rows per tile: 4 waves x 2 sets x 16
+
+template <int DT, int D, bool CAUSAL>
+__device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, int nq) {
+  using namespace prefix_detail;
+  static_assert(DT == kF16 || DT == kBF16, "16-bit caches only");
+  constexpr int W = kPrefixWaves;
+  constexpr int ROW_B = D * 2;
+  constexpr int GRAN = ROW_B / 16;                    // 16-byte granules per row
+  constexpr int BLK_B = kBlock * ROW_B;               // one block of one head
+  constexpr int STAGE_BLK = kTensorStage / BLK_B;     // blocks per stage (2 or 4)
+  constexpr int STAGE_TOK = STAGE_BLK * kBlock;
+  constexpr int DT16 = D / 16;                        // 16-wide d tiles
+  constexpr int KS = D / 32;                          // MFMA k-steps over D
+  constexpr int PER_WAVE = kStageChunks / W;          // direct-to-LDS loads per wave per stage
+  constexpr float kLazy = 8.f;                        // reference-max slack, log2 units
+  static_assert(STAGE_BLK % 2 == 0 && GRAN >= 8, "stages hold block pairs; swizzle fits a row");
+
+  auto smem = tl.smem;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = a.H, h = a.h, t1 = a.t1;
+  const int b0 = a.t0 / kBlock;
+  const int nb = (a.t1 - a.t0 + kBlock - 1) / kBlock;
+  // a negative scale flips the sign of q (exact), so that the raw logit max
+  // times |scale| is the scaled max; a zero scale is taken as 1e-30, which
+  // leaves every finite logit at 0 (to within 1e-22) and a masked one at -inf
+  const float scale = fmaxf(fabsf(a.scale_log2), 1e-30f);
+  const unsigned qsign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
+
+  int qi[2], lim[2];
+  bool q_ok[2];
+  u32x4 qf[2][KS];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    qi[c] = wave * 32 + c * 16 + (lane & 15);
+    q_ok[c] = qi[c] < nq;
+    const int rq = q_ok[c] ? tl.rows[qi[c]] : 0;
+    lim[c] = CAUSAL ? (q_ok[c] ? tl.lim[qi[c]] : -1) : 0;
+    const char* qrow = (const char*)a.q + (size_t)(rq * H + h) * ROW_B;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      u32x4 v = q_ok[c] ? ld16(qrow + (32 * ks + 8 * (lane >> 4)) * 2) : u32x4{0u, 0u, 0u, 0u};
+      qf[c][ks] = v ^ u32x4{qsign, qsign, qsign, qsign};
+    }
+  }
+  const bool has_q = wave * 32 < nq;                  // wave-uniform (set 1 may be empty:
+                                                      // it is computed on zero queries)
+
+  // Direct-to-LDS stage loads: wave w issues chunks w, w + W, ... (1 KiB each);
+  // lane l of a chunk fills LDS bytes [16 l, 16 l + 16) of it, i.e. block
+  // c_bl of the stage, token row t, granule slot pos, from the global granule
+  // pos ^ f(t) of that row.
+  const size_t blk_stride = (size_t)H * BLK_B;
+  int c_bl[PER_WAVE];
+  unsigned c_off[PER_WAVE];
+  bool c_v[PER_WAVE];
+#pragma unroll
+  for (int j = 0; j < PER_WAVE; ++j) {
+    const int q = wave + j * W;
+    const int off = (q % (kStageChunks / 2)) * 1024 + lane * 16;
+    c_v[j] = q >= kStageChunks / 2;
+    c_bl[j] = off / BLK_B;
+    const int t = (off % BLK_B) / ROW_B;
+    const int pos = (off % ROW_B) / 16;
+    c_off[j] = (unsigned)(h * BLK_B + t * ROW_B + ((pos ^ swz(t)) << 4));
+  }
+  const int nstages = (nb + STAGE_BLK - 1) / STAGE_BLK;
+  const int last = nstages - 1;
+  auto table = [&](int st, int* tb) {
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) tb[j] = tl.tbl[min(st * STAGE_BLK + c_bl[j], nb - 1)];
+  };
+  auto issue = [&](const int* tb, int buf) {
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const unsigned blk = (unsigned)__builtin_amdgcn_readfirstlane(tb[j]);
+      const char* base = (const char*)(c_v[j] ? a.pv : a.pk) + (size_t)blk * blk_stride;
+      lds_dma16_sbase(base, c_off[j], lds_addr(&smem[buf][(wave + j * W) * 1024]));
+    }
+  };
+
+  float mref[2] = {-INFINITY, -INFINITY};   // reference max of the exponentials
+  float lsum[2] = {0.f, 0.f};
+  f32x4 o[2][DT16];
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int i = 0; i < DT16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int kt_row = lane & 15;                               // K: token row of this lane
+  const int vt_row = 4 * (lane >> 4) + ((lane & 15) >> 2);    // V^T: token row
+  const int vt_half = 8 * (lane & 1);
+  const int vt_pair = (lane & 3) >> 1;
+
+  // one pair of blocks (32 tokens) of stage buffer `buf`, first block `bl`;
+  // `tok0` is the pair's first key token; `masked` selects the masking path
+  auto pair = [&](int buf, int bl, int tok0, bool masked) {
+    const char* kb = &smem[buf][bl * BLK_B];
+    const char* vb = &smem[buf][kTensorStage + bl * BLK_B];
+    // Software pipeline of one pair: all K fragments are read, the QK^T
+    // MFMAs issued, then all V^T fragments are read before the softmax, so
+    // that the LDS latency of V hides under the softmax arithmetic.  The
+    // scheduling barriers keep the compiler from sinking the reads next to
+    // their uses (it would then wait for each read in turn).
+    u32x4 kf[2][KS];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const char* krow = kb + b * BLK_B + kt_row * ROW_B;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz(kt_row)) << 4));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    f32x4 s[2][2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) s[c][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        s[0][b] = Mfma<DT>::qk(kf[b][ks], qf[0][ks], s[0][b]);
+        s[1][b] = Mfma<DT>::qk(kf[b][ks], qf[1][ks], s[1][b]);
+      }
+    unsigned long long va[DT16], vb2[DT16];
+    const char* vrow = vb + vt_row * ROW_B + vt_half;
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+      va[dt] = Mfma<DT>::tr_read(vrow + off);
+      vb2[dt] = Mfma<DT>::tr_read(vrow + BLK_B + off);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    unsigned long long pk[2][2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float x[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { x[i] = s[c][0][i]; x[4 + i] = s[c][1][i]; }
+      if (masked) {
+        // token tok0 + 4 (lane / 16) + 16 (i / 4) + i % 4 is visible below `bound`
+        const int rel = (CAUSAL ? min(t1, lim[c] + 1) : t1) - tok0 - 4 * (lane >> 4);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = (i >> 2) * kBlock + (i & 3) < rel ? x[i] : -INFINITY;
+      }
+      float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+      bm = max_xor32(max_xor16(bm));
+      const float bms = bm == -INFINITY ? -INFINITY : bm * scale;
+      if (__builtin_amdgcn_ballot_w64(bms > mref[c] + kLazy) != 0) {
+        const float mn = fmaxf(mref[c], bms);
+        const float alpha = mn == -INFINITY ? 1.f : fast_exp2(mref[c] - mn);
+        lsum[c] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT16; ++dt) o[c][dt] *= alpha;
+        mref[c] = mn;
+      }
+      const float nm = mref[c] == -INFINITY ? 0.f : -mref[c];
+      float p[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(x[i], scale, nm));   // masked: 0
+      lsum[c] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+      pk[c][0] = Mfma<DT>::pack_p(p);
+      pk[c][1] = Mfma<DT>::pack_p(p + 4);
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      o[0][dt] = Mfma<DT>::pv2(va[dt], vb2[dt], pk[0][0], pk[0][1], o[0][dt]);
+      o[1][dt] = Mfma<DT>::pv2(va[dt], vb2[dt], pk[1][0], pk[1][1], o[1][dt]);
+    }
+  };
+
+  // Ring of kRing stage buffers, kRing - 1 stages in flight (see tile_core).
+  int tb[PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < kRing - 1; ++i) {
+    table(min(i, last), tb);
+    issue(tb, i);
+  }
+  table(min(kRing - 1, last), tb);
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : : "v"(qf[c][ks]));
+  wait_vmcnt<0>();
+  const int full_end = CAUSAL ? min(t1, a.lim_min + 1) : t1;   // keys before it need no mask
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st % kRing;
+    wait_vmcnt<(kRing - 2) * PER_WAVE>();
+    lds_sync();
+    if (st == last && (t1 & (kBlock - 1)) != 0) {
+      // zero the V rows past the end of the range's last, partly filled block
+      // (their probabilities are 0, but 0 * NaN would poison the product); when
+      // that block opens a pair, the pair's second slot holds a second copy of
+      // it (loads past the range re-read the last block): zero that one too
+      const int bl = (nb - 1) - st * STAGE_BLK;
+      const int first = t1 & (kBlock - 1);
+      const int copies = (bl & 1) ? 1 : 2;
+      const int per = (kBlock - first) * GRAN;
+      for (int i = tid; i < copies * per; i += W * 64) {
+        const int cp = i / per, k = i % per;
+        char* vz = &smem[buf][kTensorStage + (bl + cp) * BLK_B];
+        const int t = first + k / GRAN;
+        *reinterpret_cast<u32x4*>(vz + t * ROW_B + ((k % GRAN) << 4)) = u32x4{0u, 0u, 0u, 0u};
+      }
+      lds_sync();
+    }
+    issue(tb, (st + kRing - 1) % kRing);
+    table(min(st + kRing, last), tb);
+    if (has_q) {
+      const int tok_st = (b0 + st * STAGE_BLK) * kBlock;
+      const int nbl = min(STAGE_BLK, nb - st * STAGE_BLK);
+#pragma unroll
+      for (int bl = 0; bl < STAGE_BLK; bl += 2) {
+        if (bl < nbl) {
+          // a pair whose second block lies past the range reads a zeroed or
+          // stale buffer slot; its tokens are masked
+          const int tok0 = tok_st + bl * kBlock;
+          pair(buf, bl, tok0, tok0 + 2 * kBlock > full_end);
+        }
+      }
+    }
+  }
+  wait_vmcnt<0>();   // the re-read stages issued by the last iterations
+
+  if (!has_q) return;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    float lt = sum_xor16(lsum[c]);
+    lt = sum_xor32(lt);
+    if (q_ok[c]) {
+      const int rq = tl.rows[qi[c]];
+      const size_t slot = (size_t)(rq * H + h) * a.seg + a.slot;
+      const bool empty = lt == 0.f;                   // a causal row that saw no key
+      const float inv = empty ? 0.f : 1.f / lt;
+      float* dst = a.o_part + slot * D + 4 * (lane >> 4);
+#pragma unroll
+      for (int dt = 0; dt < DT16; ++dt) *reinterpret_cast<f32x4*>(dst + dt * 16) = o[c][dt] * inv;
+      if (lane < 16) a.lse_part[slot] = empty ? -INFINITY : mref[c] + fast_log2(lt);
+    }
+  }
+}
+
+}  // namespace parrot

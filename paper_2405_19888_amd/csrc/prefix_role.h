@@ -100,25 +100,26 @@ template <> struct Mfma<kBF16> {
 }  // namespace prefix_detail
 
 constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
-// LDS bytes of a query tile whose key range spans up to `blocks` blocks: the
-// stage ring, the tile's query rows, the key block ids, a count, and the rows'
-// last visible key (causal tiles).
-constexpr int tile_lds_bytes(int blocks) {
-  return prefix_detail::kRing * prefix_detail::kStageBytes + (2 * kPrefixWaves * 16 + blocks + 4) * 4;
+// LDS bytes of a query tile of up to `rows` rows whose key range spans up to
+// `blocks` blocks: the stage ring, the tile's query rows, the key block ids, a
+// count, and the rows' last visible key (causal tiles).
+constexpr int tile_lds_bytes(int blocks, int rows = kPrefixWaves * 16) {
+  return prefix_detail::kRing * prefix_detail::kStageBytes + (2 * rows + blocks + 4) * 4;
 }
 constexpr int kPrefixLds = tile_lds_bytes(prefix_detail::kMaxChunkBlocks);
 
-// LDS views shared by the tile's set-up code and tile_core.
+// LDS views shared by the tile's set-up code and the tile cores.
 struct TileLds {
   char (*smem)[prefix_detail::kStageBytes];   // [kRing][kStageBytes]
-  int* rows;                                  // [64] query row of each tile column
+  int* rows;                                  // [rows] query row of each tile column
   int* tbl;                                   // [blocks] key blocks, clamped
   int* count;                                 // set-up scratch
-  int* lim;                                   // [64] last visible key token (causal)
-  PARROT_DEV explicit TileLds(char* lds, int blocks = prefix_detail::kMaxChunkBlocks)
+  int* lim;                                   // [rows] last visible key token (causal)
+  PARROT_DEV explicit TileLds(char* lds, int blocks = prefix_detail::kMaxChunkBlocks,
+                              int nrows = kPrefixWaves * 16)
       : smem(reinterpret_cast<char (*)[prefix_detail::kStageBytes]>(lds)),
         rows(reinterpret_cast<int*>(lds + prefix_detail::kRing * prefix_detail::kStageBytes)),
-        tbl(rows + kPrefixWaves * 16),
+        tbl(rows + nrows),
         count(tbl + blocks),
         lim(count + 4) {}
 };
@@ -132,6 +133,7 @@ struct TileJob {
   float* o_part; float* lse_part; // partial results [rows][H][seg][D], [rows][H][seg]
   int seg, slot;                  // slots per (row, head); this tile's slot
   float scale_log2;
+  int lim_min;                    // causal tiles: the smallest row limit (tl.lim)
 };
 
 // The attention core of a query tile: up to 64 query rows (tl.rows, nq of

@@ -94,7 +94,10 @@ def test_dtype_cast_is_round_to_nearest_even():
 def test_aliases_cover_all_configs():
     assert sorted(ALIASES.values()) == sorted(["tiny", "llama7b_g32_p2048", "sysprompt_g64_p6000",
                                                "mapreduce_13b_4x32", "mixed_7b_32layer",
-                                               "nested_sys6000_8x8_fs256"])
+                                               "nested_sys6000_8x8_fs256", "prefill_sys6000_g64",
+                                               "prefill_sys6000_g64_q16"])
+    from workloads import CONFIGS
+    assert set(ALIASES.values()) == set(CONFIGS)
 
 
 def test_nested_plan_chains_and_flattening():
