@@ -26,11 +26,13 @@ PARROT_DEV float group_max(float x) {
 // i then reads the log-sum-exp of slot i while the partial outputs of the
 // first kBatch slots are loaded in the same round; later slots (long prefixes
 // or long runs) are read batch by batch with their weights.
-template <int DT, int D>
+// kBatch: partial outputs loaded per round (registers: kBatch * D / 64 per
+// lane); the small variant serves calls with at most 8 slots per sequence.
+template <int DT, int D, int kBatch>
 __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   using E = Elem<DT>;
   constexpr int EPL = D / kWave;
-  constexpr int kBatch = 64 / EPL;          // 32 slots for D = 128
+  static_assert(kBatch <= kWave, "one batch's weights fit one lane each");
   const int lane = threadIdx.x & 63;
   const long w = (long)blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (w >= (long)a.R * a.H) return;
@@ -78,7 +80,13 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   const float l_lane = lane < n ? a.lse_part[base + slot_lane] : -INFINITY;
   float v[kBatch][EPL];
 #pragma unroll
-  for (int u = 0; u < kBatch; ++u) load_o(min(u, n - 1), v[u]);
+  for (int u = 0; u < kBatch; ++u) {
+    if constexpr (kBatch <= 8) {            // few slots: load only the partials that exist
+      if (u < n) load_o(u, v[u]);
+    } else {
+      load_o(min(u, n - 1), v[u]);
+    }
+  }
 
   float mx = l_lane;
   for (int i = lane + kWave; i < n; i += kWave) mx = fmaxf(mx, a.lse_part[base + slot_of(i)]);
@@ -126,7 +134,11 @@ template <int DT, int D>
 static hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const long waves = (long)a.R * a.H;
   if (waves <= 0) return hipSuccess;
-  hipExtLaunchKernelGGL((k_merge<DT, D>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, e0, e1, 0, a);
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  if (a.seg <= 8)
+    hipExtLaunchKernelGGL((k_merge<DT, D, 8>), grid, dim3(256), 0, s, e0, e1, 0, a);
+  else
+    hipExtLaunchKernelGGL((k_merge<DT, D, 64 / (D / kWave)>), grid, dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 

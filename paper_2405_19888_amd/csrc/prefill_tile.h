@@ -25,6 +25,8 @@
 //     stages that need it.
 #pragma once
 
+#include <type_traits>
+
 #include "prefix_role.h"
 
 namespace parrot {
@@ -217,8 +219,10 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
     for (int ks = 0; ks < KS; ++ks) asm volatile("" : : "v"(qf[c][ks]));
   wait_vmcnt<0>();
   const int full_end = CAUSAL ? min(t1, a.lim_min + 1) : t1;   // keys before it need no mask
-  for (int st = 0; st < nstages; ++st) {
-    const int buf = st % kRing;
+  // one stage; `bufc` carries the ring buffer as a constant, so that every LDS
+  // address of the stage is a lane constant plus an immediate offset
+  auto step = [&](int st, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
     wait_vmcnt<(kRing - 2) * PER_WAVE>();
     lds_sync();
     if (st == last && (t1 & (kBlock - 1)) != 0) {
@@ -253,6 +257,12 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
         }
       }
     }
+  };
+  static_assert(kRing == 3, "the stage loop is unrolled over the ring");
+  for (int st = 0; st < nstages; st += kRing) {
+    step(st, std::integral_constant<int, 0>{});
+    if (st + 1 < nstages) step(st + 1, std::integral_constant<int, 1>{});
+    if (st + 2 < nstages) step(st + 2, std::integral_constant<int, 2>{});
   }
   wait_vmcnt<0>();   // the re-read stages issued by the last iterations
 
