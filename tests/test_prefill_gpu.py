@@ -153,3 +153,35 @@ def test_prefill_validation_catches_bad_rows():
           msg="suffix length")
     check(off, make_prefill_rows(rows.num_query_rows, rows.max_query_rows,
                                  rows.max_group_rows - 1), msg="max_group_rows")
+
+
+@pytest.mark.parametrize("name", ["prefill", "prefill_q16"])
+def test_prefill_workload_sampled(name):
+    """The benchmark's prefill workloads at full size, in the launch the
+    benchmark times: sampled rows (first and last rows of requests, rows at
+    row-tile edges, random rows) against the oracle, and every row finite."""
+    from workloads import (get_config, make_device_layer, make_device_prefill_queries,
+                           make_plan, prefill_rows)
+    cfg = get_config(name)
+    plan = make_plan(cfg)
+    qr = prefill_rows(plan, cfg.prefill_rows, None)
+    say("prefill workload", cfg.name, int(qr.sum()), "rows")
+    dev = make_device_layer(plan, 0, "cuda", seed=cfg.seed)
+    dev["q_rows"], dev["query_offsets"] = make_device_prefill_queries(plan, qr, "cuda", cfg.seed, 0)
+    off = dev["query_offsets"].cpu().numpy()
+    out, lse = run_prefill(plan, dev, off)
+    o, l = to_np(out, lse)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    rng = np.random.default_rng(1)
+    reqs = sorted(set(rng.choice(plan.num_requests, size=6, replace=False).tolist()) | {0, plan.num_requests - 1})
+    rows = set()
+    for r in reqs:
+        a, b = int(off[r]), int(off[r + 1])
+        if b > a:
+            rows |= {a, b - 1, min(b - 1, a + 127), min(b - 1, a + 128)}
+    rows |= set(rng.integers(0, int(off[-1]), size=6).tolist())
+    rows = sorted(rows)
+    host = type("B", (), {})()
+    host.k_pool, host.v_pool = dev["k_pool"].cpu(), dev["v_pool"].cpu()
+    ref = oracle_prefill_for(host, plan, dev["q_rows"].cpu(), off, rows=rows)
+    assert_close(o[rows], l[rows], *ref, plan.dtype, f"{cfg.name} sampled rows")
