@@ -179,10 +179,13 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[i] = (i >> 2) * kBlock + (i & 3) < rel ? x[i] : -INFINITY;
       }
-      float bm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-      bm = max_xor32(max_xor16(bm));
-      const float bms = bm == -INFINITY ? -INFINITY : bm * scale;
-      if (__builtin_amdgcn_ballot_w64(bms > mref[c] + kLazy) != 0) {
+      // The row's reference only has to move when some lane's own logits
+      // exceed it by more than kLazy: that test needs no cross-lane max, and
+      // the cross-lane max is taken only in the (rare) branch that moves it.
+      const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+      if (__builtin_amdgcn_ballot_w64(lm * scale > mref[c] + kLazy) != 0) {
+        const float bm = max_xor32(max_xor16(lm));
+        const float bms = bm == -INFINITY ? -INFINITY : bm * scale;
         const float mn = fmaxf(mref[c], bms);
         const float alpha = mn == -INFINITY ? 1.f : fast_exp2(mref[c] - mn);
         lsum[c] *= alpha;
