@@ -33,7 +33,16 @@ namespace parrot {
 constexpr int kPrefillMaxBlocks = 512;                       // chunk <= 8192 tokens
 // query rows per tile: the wide tile for 16-bit caches, decode's tile for fp32
 template <int DT> constexpr int kTileRows = DT == kF32 ? kPrefixWaves * 16 : kWideRows;
-constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks, kWideRows);
+template <int DT> constexpr int kTileRing = DT == kF32 ? prefix_detail::kRing : kWideRing;
+constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks, kWideRows, kWideRing);
+constexpr int kPrefillLdsF32 = tile_lds_bytes(kPrefillMaxBlocks);
+
+// The one LDS view of a prefill tile: its stage ring, rows, block table and
+// limits laid out for the tile core that DT selects (both item kinds use it).
+template <int DT>
+PARROT_DEV TileLds prefill_lds(char* lds) {
+  return TileLds(lds, kPrefillMaxBlocks, kTileRows<DT>, kTileRing<DT>);
+}
 constexpr int kXcds = 8;                                     // workgroups go round-robin over XCDs
 
 
@@ -99,7 +108,7 @@ __device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* 
     while (x >= 0 && x < a.NG && lvl < a.depth - 1) { ++lvl; x = a.parents[x]; }
   }
   constexpr int ROWS = kTileRows<DT>;
-  const TileLds tl(lds, kPrefillMaxBlocks, ROWS);
+  const TileLds tl = prefill_lds<DT>(lds);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const long qbase = (long)qt * ROWS;
@@ -141,7 +150,7 @@ __device__ __forceinline__ void prefill_prefix_item(const PrefillArgs& a, char* 
   const int nq = *tl.count;
   if (nq <= 0) return;                                 // uniform over the workgroup
   TileJob j;
-  j.q = a.q; j.pk = a.pk; j.pv = a.pv; j.H = a.H; j.h = h;
+  j.q = a.q; j.pk = a.pk; j.pv = a.pv; j.npool = a.npblk; j.H = a.H; j.h = h;
   j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
   j.seg = a.seg; j.slot = lvl * a.seg_p + c; j.scale_log2 = a.scale_log2; j.lim_min = 0;
   if constexpr (DT == kF32)
@@ -167,7 +176,7 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
   const int t0 = k * a.co;
   if (t0 > pos0 + nq - 1) return;
   const int t1 = min(min(rw.S, t0 + a.co), pos0 + nq);
-  const TileLds tl(lds, kPrefillMaxBlocks, ROWS);
+  const TileLds tl = prefill_lds<DT>(lds);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b0 = t0 / kBlock, nb = (t1 - t0 + kBlock - 1) / kBlock;
@@ -182,7 +191,7 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
   }
   __syncthreads();
   TileJob j;
-  j.q = a.q; j.pk = a.sk; j.pv = a.sv; j.H = a.H; j.h = h;
+  j.q = a.q; j.pk = a.sk; j.pv = a.sv; j.npool = a.nsblk; j.H = a.H; j.h = h;
   j.t0 = t0; j.t1 = t1; j.o_part = a.o_part; j.lse_part = a.lse_part;
   j.seg = a.seg; j.slot = a.seg_pre + k; j.scale_log2 = a.scale_log2; j.lim_min = pos0;
   if constexpr (DT == kF32)
@@ -196,7 +205,9 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
 template <int DT, int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DT == kF32 ? 3 : 2, DT == kF32 ? 3 : 2)))
 void k_prefill(PrefillArgs a) {
-  __shared__ __attribute__((aligned(1024))) char lds[kPrefillLds];
+  __shared__ __attribute__((aligned(1024))) char lds[DT == kF32 ? kPrefillLdsF32 : kPrefillLds];
+  static_assert(sizeof(lds) >= tile_lds_bytes(kPrefillMaxBlocks, kTileRows<DT>, kTileRing<DT>),
+                "the LDS array holds the tile's layout");
   const int bid = blockIdx.x;
   if (bid < a.meta_wgs) {
     const int t = bid * 256 + (int)threadIdx.x;

@@ -32,6 +32,7 @@
 namespace parrot {
 
 constexpr int kWideRows = 128;   // query rows per tile: 4 waves x 2 sets x 16
+constexpr int kWideRing = prefix_detail::kRing;   // stage buffers (two stages in flight)
 
 template <int DT, int D, bool CAUSAL>
 __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, int nq) {
@@ -108,7 +109,9 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
   auto issue = [&](const int* tb, int buf) {
 #pragma unroll
     for (int j = 0; j < PER_WAVE; ++j) {
-      const unsigned blk = (unsigned)__builtin_amdgcn_readfirstlane(tb[j]);
+      // block ids are clamped when the table is filled; clamping again here
+      // keeps every load inside the pool whatever the LDS table holds
+      const unsigned blk = min((unsigned)__builtin_amdgcn_readfirstlane(tb[j]), (unsigned)(a.npool - 1));
       const char* base = (const char*)(c_v[j] ? a.pv : a.pk) + (size_t)blk * blk_stride;
       lds_dma16_sbase(base, c_off[j], lds_addr(&smem[buf][(wave + j * W) * 1024]));
     }

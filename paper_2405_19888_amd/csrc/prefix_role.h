@@ -103,22 +103,22 @@ constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
 // LDS bytes of a query tile of up to `rows` rows whose key range spans up to
 // `blocks` blocks: the stage ring, the tile's query rows, the key block ids, a
 // count, and the rows' last visible key (causal tiles).
-constexpr int tile_lds_bytes(int blocks, int rows = kPrefixWaves * 16) {
-  return prefix_detail::kRing * prefix_detail::kStageBytes + (2 * rows + blocks + 4) * 4;
+constexpr int tile_lds_bytes(int blocks, int rows = kPrefixWaves * 16, int ring = prefix_detail::kRing) {
+  return ring * prefix_detail::kStageBytes + (2 * rows + blocks + 4) * 4;
 }
 constexpr int kPrefixLds = tile_lds_bytes(prefix_detail::kMaxChunkBlocks);
 
 // LDS views shared by the tile's set-up code and the tile cores.
 struct TileLds {
-  char (*smem)[prefix_detail::kStageBytes];   // [kRing][kStageBytes]
+  char (*smem)[prefix_detail::kStageBytes];   // [ring][kStageBytes]
   int* rows;                                  // [rows] query row of each tile column
   int* tbl;                                   // [blocks] key blocks, clamped
   int* count;                                 // set-up scratch
   int* lim;                                   // [rows] last visible key token (causal)
   PARROT_DEV explicit TileLds(char* lds, int blocks = prefix_detail::kMaxChunkBlocks,
-                              int nrows = kPrefixWaves * 16)
+                              int nrows = kPrefixWaves * 16, int ring = prefix_detail::kRing)
       : smem(reinterpret_cast<char (*)[prefix_detail::kStageBytes]>(lds)),
-        rows(reinterpret_cast<int*>(lds + prefix_detail::kRing * prefix_detail::kStageBytes)),
+        rows(reinterpret_cast<int*>(lds + ring * prefix_detail::kStageBytes)),
         tbl(rows + nrows),
         count(tbl + blocks),
         lim(count + 4) {}
@@ -128,6 +128,7 @@ struct TileLds {
 struct TileJob {
   const void* q;                  // [rows][H][D]
   const void* pk; const void* pv; // pools of the key sequence
+  int npool;                      // blocks in those pools
   int H, h;
   int t0, t1;                     // key tokens [t0, t1); t0 a multiple of 16
   float* o_part; float* lse_part; // partial results [rows][H][seg][D], [rows][H][seg]
@@ -210,7 +211,7 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   const int nq = min(s_count - qbase, W * 16);
   if (nq <= 0) return;                                 // uniform over the workgroup
   TileJob job;
-  job.q = a.q; job.pk = a.pk; job.pv = a.pv; job.H = H; job.h = h;
+  job.q = a.q; job.pk = a.pk; job.pv = a.pv; job.npool = a.npblk; job.H = H; job.h = h;
   job.t0 = t0; job.t1 = t1; job.o_part = a.o_part; job.lse_part = a.lse_part;
   job.seg = a.seg; job.slot = lvl * a.seg_p + c; job.scale_log2 = a.scale_log2;
   tile_core<DT, D, false>(job, tl, nq);
