@@ -200,10 +200,10 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
     wide_tile<DT, D, true>(j, tl, nq);
 }
 
-// Occupancy: the wide tile keeps two column sets of accumulators (two waves
-// per SIMD, two workgroups per CU); decode's tile fits three.
+// Occupancy: three waves per SIMD (three workgroups per CU: 3 x 51 KiB of
+// LDS, at most 168 registers per lane), for either tile core.
 template <int DT, int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(DT == kF32 ? 3 : 2, DT == kF32 ? 3 : 2)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 void k_prefill(PrefillArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds[DT == kF32 ? kPrefillLdsF32 : kPrefillLds];
   static_assert(sizeof(lds) >= tile_lds_bytes(kPrefillMaxBlocks, kTileRows<DT>, kTileRing<DT>),

@@ -135,11 +135,10 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
   auto pair = [&](int buf, int bl, int tok0, bool masked) {
     const char* kb = &smem[buf][bl * BLK_B];
     const char* vb = &smem[buf][kTensorStage + bl * BLK_B];
-    // Software pipeline of one pair: all K fragments are read, the QK^T
-    // MFMAs issued, then all V^T fragments are read before the softmax, so
-    // that the LDS latency of V hides under the softmax arithmetic.  The
-    // scheduling barriers keep the compiler from sinking the reads next to
-    // their uses (it would then wait for each read in turn).
+    // K fragments feed the QK^T MFMAs of both sets; the V^T fragments are
+    // read next to their PV MFMAs.  Reading them all ahead (or all K ahead)
+    // needs about 24 more registers, which costs the third wave per SIMD;
+    // with three waves the other waves hide the LDS latency better (measured).
     u32x4 kf[2][KS];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -148,7 +147,6 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       for (int ks = 0; ks < KS; ++ks)
         kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz(kt_row)) << 4));
     }
-    __builtin_amdgcn_sched_barrier(0);
     f32x4 s[2][2];
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -161,15 +159,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
         s[0][b] = Mfma<DT>::qk(kf[b][ks], qf[0][ks], s[0][b]);
         s[1][b] = Mfma<DT>::qk(kf[b][ks], qf[1][ks], s[1][b]);
       }
-    unsigned long long va[DT16], vb2[DT16];
-    const char* vrow = vb + vt_row * ROW_B + vt_half;
-#pragma unroll
-    for (int dt = 0; dt < DT16; ++dt) {
-      const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
-      va[dt] = Mfma<DT>::tr_read(vrow + off);
-      vb2[dt] = Mfma<DT>::tr_read(vrow + BLK_B + off);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+
     unsigned long long pk[2][2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
@@ -204,10 +194,14 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       pk[c][0] = Mfma<DT>::pack_p(p);
       pk[c][1] = Mfma<DT>::pack_p(p + 4);
     }
+    const char* vrow = vb + vt_row * ROW_B + vt_half;
 #pragma unroll
     for (int dt = 0; dt < DT16; ++dt) {
-      o[0][dt] = Mfma<DT>::pv2(va[dt], vb2[dt], pk[0][0], pk[0][1], o[0][dt]);
-      o[1][dt] = Mfma<DT>::pv2(va[dt], vb2[dt], pk[1][0], pk[1][1], o[1][dt]);
+      const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+      const unsigned long long va = Mfma<DT>::tr_read(vrow + off);
+      const unsigned long long vb2 = Mfma<DT>::tr_read(vrow + BLK_B + off);
+      o[0][dt] = Mfma<DT>::pv2(va, vb2, pk[0][0], pk[0][1], o[0][dt]);
+      o[1][dt] = Mfma<DT>::pv2(va, vb2, pk[1][0], pk[1][1], o[1][dt]);
     }
   };
 
