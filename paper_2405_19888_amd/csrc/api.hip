@@ -378,12 +378,13 @@ struct PrefillPlan {
 
 // Chunk of a key range of at most `len` tokens: the whole range up to 8192
 // tokens (fewest partial results), halved while the items of that chunk size
-// (`items_per_chunk` per chunk) would not give every CU two workgroups.
+// (`items_per_chunk` per chunk) would not fill every CU with the three
+// workgroups it holds.
 int prefill_chunk(long len, double items_per_chunk) {
   int c = kPrefillChunkMax;
   while (c > kPrefillChunkMin && c / 2 >= len) c /= 2;
   const double cus = num_cus();
-  while (c > kPrefillChunkMin && items_per_chunk * (double)ceil_div(len, c) < 2 * cus) c /= 2;
+  while (c > kPrefillChunkMin && items_per_chunk * (double)ceil_div(len, c) < 3 * cus) c /= 2;
   return c;
 }
 
