@@ -13,8 +13,8 @@
 //     ahead; the loads take a scalar base (pool + block * stride) and a
 //     per-lane offset, and each stage's two block ids are read from LDS one
 //     stage before they are needed, so issuing a stage waits on nothing;
-//   * S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_{f16,bf16}, the
-//     same XOR-swizzled LDS rows and ds_read_b64_tr_b16 reads of V^T;
+//   * S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_16x16x32_{f16,bf16} over
+//     XOR-swizzled LDS rows (swz_wide below), V^T read with ds_read_b64_tr_b16;
 //   * online softmax in fp32 with a lazily moved reference: the exponentials
 //     use a reference max that is raised only when a row's max exceeds it by
 //     more than 8 (log2 units), so the accumulators are rescaled a few times
@@ -30,6 +30,20 @@
 #include "prefix_role.h"
 
 namespace parrot {
+
+// LDS row swizzle of the wide tile: 16-byte granule j of token row t sits at
+// granule j ^ f(t).  The LDS serves 256 bytes per pass (64 banks), i.e. 16
+// lanes of a 16-byte K read (16 token rows, one logical granule) or 32 lanes of
+// an 8-byte transposed V read (8 token rows, two adjacent granules).  f spreads
+// both over all 64 banks: for 256-byte rows (D = 128) f is a bijection of the
+// 16 rows whose values differ above bit 0 within rows 0-7 and within rows
+// 8-15; for 128-byte rows (D = 64) two rows share a 256-byte span, and f is a
+// bijection within each row parity with the same property.
+template <int GRAN>
+PARROT_DEV int swz_wide(int t) {
+  if constexpr (GRAN == 16) return ((t & 7) << 1) | ((t >> 3) & 1);
+  else return (t & 6) | ((t >> 3) & 1);
+}
 
 constexpr int kWideRows = 128;   // query rows per tile: 4 waves x 2 sets x 16
 constexpr int kWideRing = prefix_detail::kRing;   // stage buffers (two stages in flight)
@@ -48,7 +62,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
   constexpr int KS = D / 32;                          // MFMA k-steps over D
   constexpr int PER_WAVE = kStageChunks / W;          // direct-to-LDS loads per wave per stage
   constexpr float kLazy = 8.f;                        // reference-max slack, log2 units
-  static_assert(STAGE_BLK % 2 == 0 && GRAN >= 8, "stages hold block pairs; swizzle fits a row");
+  static_assert(STAGE_BLK % 2 == 0 && (GRAN == 8 || GRAN == 16), "stages hold block pairs; swizzle fits a row");
 
   auto smem = tl.smem;
   const int tid = threadIdx.x;
@@ -98,7 +112,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
     c_bl[j] = off / BLK_B;
     const int t = (off % BLK_B) / ROW_B;
     const int pos = (off % ROW_B) / 16;
-    c_off[j] = (unsigned)(h * BLK_B + t * ROW_B + ((pos ^ swz(t)) << 4));
+    c_off[j] = (unsigned)(h * BLK_B + t * ROW_B + ((pos ^ swz_wide<GRAN>(t)) << 4));
   }
   const int nstages = (nb + STAGE_BLK - 1) / STAGE_BLK;
   const int last = nstages - 1;
@@ -145,7 +159,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       const char* krow = kb + b * BLK_B + kt_row * ROW_B;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz(kt_row)) << 4));
+        kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz_wide<GRAN>(kt_row)) << 4));
     }
     f32x4 s[2][2];
 #pragma unroll
@@ -197,7 +211,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
     const char* vrow = vb + vt_row * ROW_B + vt_half;
 #pragma unroll
     for (int dt = 0; dt < DT16; ++dt) {
-      const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+      const int off = ((2 * dt + vt_pair) ^ swz_wide<GRAN>(vt_row)) << 4;
       const unsigned long long va = Mfma<DT>::tr_read(vrow + off);
       const unsigned long long vb2 = Mfma<DT>::tr_read(vrow + BLK_B + off);
       o[0][dt] = Mfma<DT>::pv2(va, vb2, pk[0][0], pk[0][1], o[0][dt]);
