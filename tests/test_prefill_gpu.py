@@ -185,3 +185,34 @@ def test_prefill_workload_sampled(name):
     host.k_pool, host.v_pool = dev["k_pool"].cpu(), dev["v_pool"].cpu()
     ref = oracle_prefill_for(host, plan, dev["q_rows"].cpu(), off, rows=rows)
     assert_close(o[rows], l[rows], *ref, plan.dtype, f"{cfg.name} sampled rows")
+
+
+@pytest.mark.parametrize("chunked", [False, True])
+def test_prefill_contexts_from_store(chunked):
+    """Fill through the host context store: prompts that fork from a shared
+    system prompt and three task prefixes (and one that shares nothing) are
+    registered, and the prefill entry point computes their own tokens' rows
+    (all of them, or the last part of each prompt) with the store's group
+    forest, against the oracle."""
+    from paper_2405_19888_amd.context import ContextStore
+    from test_nested_gpu import plan_from_store
+    say("prefill from context store, chunked =", chunked)
+    rng = np.random.default_rng(8)
+    st = ContextStore(block_size=16, num_blocks=800)
+    sysp = rng.integers(0, 1000, size=300).tolist()
+    tasks = [rng.integers(0, 1000, size=n).tolist() for n in (50, 77, 120)]
+    ctxs = []
+    for i in range(10):
+        t = tasks[i % 3]
+        own = rng.integers(0, 1000, size=int(rng.integers(1, 200))).tolist()
+        ctxs.append(st.fill(sysp + t + own, [300, 300 + len(t)]))
+    ctxs.append(st.fill(rng.integers(0, 1000, size=150).tolist(), []))
+    batch = st.build_batch(ctxs, pad_block=st.num_blocks)
+    plan = plan_from_store(batch, st, heads=4, head_dim=128, dtype="bfloat16")
+    data = make_batch(plan, seed=9)
+    S = plan.suffix_lens
+    qr = [int(s) - (int(s) // 3 if chunked else 0) for s in S]
+    q, off = make_prefill_queries(plan, qr, seed=9)
+    out, lse = run_prefill(plan, device_dict(data, q, off), off)
+    ref = oracle_prefill_for(data, plan, q, off)
+    assert_close(*to_np(out, lse), *ref, "bfloat16", f"store prefill chunked={chunked}")
