@@ -43,13 +43,16 @@ DTYPE_TAG = {"float32": "f32", "float16": "f16", "bfloat16": "bf16"}
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "partials_counters.json")
 KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/partials.hip", "paper_2405_19888_amd/csrc/prefix_role.h",
                   "paper_2405_19888_amd/csrc/splitkv_role.h", "paper_2405_19888_amd/csrc/common.h"]
+PREFILL_COUNTERS_FILE = os.path.join(ROOT, "profiles", "prefill_counters.json")
+PREFILL_SOURCES = ["paper_2405_19888_amd/csrc/prefill.hip", "paper_2405_19888_amd/csrc/prefill_tile.h",
+                   "paper_2405_19888_amd/csrc/prefix_role.h", "paper_2405_19888_amd/csrc/common.h"]
 
 
-def kernel_source_hash() -> str:
-    """Hash of the partials kernel's code with comments and blank space removed,
-    so that counters taken on it stay attached until the code itself changes."""
+def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
+    """Hash of a kernel's code with comments and blank space removed, so that
+    counters taken on it stay attached until the code itself changes."""
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
             src = f.read()
         src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
@@ -254,7 +257,8 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
             "kernel": "k_prefill (prefix items + causal own items, MFMA)",
             "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
-            "traffic": None, "algorithmic_flops": flops,
+            "traffic": traffic_from_counters(cfg.name, PREFILL_COUNTERS_FILE, PREFILL_SOURCES),
+            "algorithmic_flops": flops,
             "avg_us": round(per["prefill_us"], 3),
         },
         "kernels_us": {k: round(v, 3) for k, v in per.items()},
@@ -300,14 +304,14 @@ def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
     return gbps
 
 
-def traffic_from_counters(plan_key: str):
-    """HBM bytes per partial-result launch from committed rocprofv3 counter runs,
-    only if they were taken on the current kernel source."""
-    if not os.path.exists(COUNTERS_FILE):
+def traffic_from_counters(plan_key: str, path: str = COUNTERS_FILE, sources=KERNEL_SOURCES):
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3
+    counter runs, only if they were taken on the current kernel source."""
+    if not os.path.exists(path):
         return None
-    with open(COUNTERS_FILE) as f:
+    with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_hash") != kernel_source_hash() or rec.get("workload") != plan_key:
+    if rec.get("source_hash") != kernel_source_hash(sources) or rec.get("workload") != plan_key:
         return None
     return rec.get("bytes_per_launch")
 
@@ -340,6 +344,17 @@ def main():
                                    "(no multi-GPU path exists)"}))
         sys.exit(2)
 
+    if args.copy_mib > 0:
+        import torch
+        n = args.copy_mib << 19                      # fp16 elements in that many MiB
+        src = torch.ones(n, dtype=torch.float16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
+
     if args.mode == "prefill":
         leg = prefill_leg(args.prefill, args.steps, args.warmup, min(args.layers, 4),
                           not args.no_baselines, args.cpu_budget)
@@ -355,14 +370,6 @@ def main():
     from workloads import get_config, make_device_layer, make_plan
     from workloads.gen import TORCH_DTYPES
 
-    if args.copy_mib > 0:
-        n = args.copy_mib << 19                      # fp16 elements in that many MiB
-        src = torch.ones(n, dtype=torch.float16, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     cfg = get_config(args.config)
     plan = make_plan(cfg)
     dev = "cuda"
