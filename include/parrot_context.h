@@ -15,9 +15,10 @@
  * released when no context references it.
  *
  * For a batch of contexts the store emits exactly the arrays
- * parrot_nested_prefix_decode takes: one group per trie node on the batch's
- * paths (parents numbered below children), each group's prefix table, and
- * each context's group, own-token table and own-token count.
+ * parrot_nested_prefix_decode and parrot_shared_prefix_prefill take: one group
+ * per trie node on the batch's paths (parents numbered below children), each
+ * group's prefix table, and each context's group, own-token table and
+ * own-token count.
  *
  * The store is not thread-safe: one thread owns it.  All pointers are HOST
  * pointers.  Block ids are in [0, num_blocks) of the caller's KV pools.
