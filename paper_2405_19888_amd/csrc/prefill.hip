@@ -80,9 +80,11 @@ PARROT_DEV void write_row_meta(const PrefillArgs& a, int t) {
         chain[nlev++] = x;
         x = a.parents ? a.parents[x] : -1;
       }
+      // at most seg_p chunks per level (none when no prefix items run, as
+      // when max_group_rows is 0), so the merge never reads past the row's slots
 #pragma unroll
       for (int i = 0; i < kMaxDepth; ++i)
-        if (i < nlev) np[nlev - 1 - i] = (clampi(a.plen[chain[i]], 0, a.max_p) + a.cp - 1) / a.cp;
+        if (i < nlev) np[nlev - 1 - i] = min((clampi(a.plen[chain[i]], 0, a.max_p) + a.cp - 1) / a.cp, a.seg_p);
       m = int4{pos / a.co + 1, nlev, (int)((unsigned)np[0] | ((unsigned)np[1] << 16)),
                (int)((unsigned)np[2] | ((unsigned)np[3] << 16))};
     }
