@@ -82,6 +82,32 @@ def algorithmic_bytes(plan):
                 prefix_flops=prefix_flops)
 
 
+def host_info() -> dict:
+    """The host CPU model and the BLAS numpy / torch link against."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        import numpy as np
+        deps = np.show_config(mode="dicts").get("Build Dependencies", {})
+        blas = deps.get("blas", {}).get("name")
+    except Exception:
+        pass
+    try:
+        import torch
+        threads = torch.get_num_threads()
+    except Exception:
+        threads = None
+    return {"cpu_model": model, "numpy_blas": blas, "torch_threads": threads}
+
+
 def cpu_baseline(plan, layer_dev, budget_s: float):
     """The oracle on host copies of one layer, request by request, for ~budget_s."""
     import numpy as np
@@ -110,6 +136,7 @@ def cpu_baseline(plan, layer_dev, budget_s: float):
         "unit": "req/s per layer",
         "cores": max(1, int(round(cpu / wall))),
         "cores_available": len(os.sched_getaffinity(0)),
+        **host_info(),
         "kind": "oracle",
         "sample": f"{done} requests of one layer of the same workload, one oracle call each, "
                   f"{wall:.1f} s wall, {cpu:.1f} s CPU",
@@ -159,6 +186,7 @@ def cpu_prefill_baseline(plan, q_rows, offsets, layer_dev, budget_s: float):
         "unit": "rows/s per layer",
         "cores": max(1, int(round(cpu / wall))),
         "cores_available": len(os.sched_getaffinity(0)),
+        **host_info(),
         "kind": "oracle",
         "sample": f"{done} random query rows of one layer of the same workload, one oracle "
                   f"call each, {wall:.1f} s wall, {cpu:.1f} s CPU",
@@ -423,13 +451,18 @@ def main():
             suffix_table_stride=flat.suffix_tables.shape[1],
             num_prefix_blocks=flat.num_blocks, num_suffix_blocks=flat.num_blocks), device=dev)
 
-    def run(shared: bool, trace: bool, flat_baseline: bool = False, append: bool = False):
+    def run(shared: bool, trace: bool, flat_baseline: bool = False, append: bool = False,
+            inputs=None, steps=None, every=None):
         """W untimed steps, then K timed steps; every `trace_every`-th timed step
         carries per-kernel (start, stop) event pairs when `trace` is set.  For
         nested groups, `flat_baseline` runs the flat entry points on the
         flattened groups; `append` times decode with append (this step's K/V
-        written into every request's last own slot)."""
-        if nested and (flat_baseline or not shared):
+        written into every request's last own slot).  `inputs` replaces the
+        per-layer input dicts (their count sets the layers cycled)."""
+        K = steps or args.steps
+        if inputs is not None:
+            calls = [dec.bind(t, shared=shared, stream=stream, nested=nested) for t in inputs]
+        elif nested and (flat_baseline or not shared):
             calls = [flat_dec.bind(flat_layers[l], shared=shared, stream=stream) for l in range(L)]
         elif append:
             calls = [dec.bind(dict(layers[l], k_new=new_kv[l][0], v_new=new_kv[l][1]),
@@ -437,7 +470,7 @@ def main():
         else:
             calls = [dec.bind(layers[l], shared=shared, stream=stream, nested=nested)
                      for l in range(L)]
-        every = max(1, args.trace_every)
+        every = max(1, every or args.trace_every)
         traced = list(range(0, K, every)) if trace else []
         events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in traced}
         for evs in events.values():       # materialise the events outside the timed region
@@ -445,20 +478,22 @@ def main():
                 e.record(stream)
         torch.cuda.synchronize()
         traces = {i: ParrotTrace(*[e.cuda_event for e in evs]) for i, evs in events.items()}
+        n = len(calls)
         for i in range(W):
-            calls[i % L]()
+            calls[i % n]()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for i in range(K):
-            calls[i % L](traces.get(i))
+            calls[i % n](traces.get(i))
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         per = None
         if trace:
             per = {}
             for k, name in enumerate(names):
-                per[name + "_us"] = sum(evs[2 * k].elapsed_time(evs[2 * k + 1])
-                                        for evs in events.values()) * 1e3 / len(events)
+                us = np.array([evs[2 * k].elapsed_time(evs[2 * k + 1]) * 1e3 for evs in events.values()])
+                per[name + "_us"] = float(us.mean())
+                per[name + "_pct"] = [round(float(x), 3) for x in np.percentile(us, [10, 50, 90])]
             per["traced_steps"] = len(events)
         return wall, per
 
@@ -506,6 +541,8 @@ def main():
             "avg_us": round(per["partials_us"], 3),
         }
         result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
+        result["kernels_us"].update({k.replace("_pct", "_p10_p50_p90_us"): v
+                                     for k, v in per.items() if k.endswith("_pct")})
         result["kernels_us"]["traced_steps"] = per["traced_steps"]
         result["ceilings"] = {
             "copy_gbps": round(copy_gbps, 1),
@@ -523,6 +560,55 @@ def main():
                 "util_ceiling_at_hbm_peak": round(min(1.0, intensity * HBM_PEAK_GBPS / 1e3
                                                       / MFMA_F16_PEAK_TFLOPS), 5),
             }
+    if not args.no_baselines and per is not None and int(plan.suffix_lens.min()) > 0:
+        # The roles one at a time, on the same blocks (the kernel runs both
+        # roles side by side, so its events cannot split them):
+        #  * suffix + merge: every request ungrouped, so the partial-result
+        #    kernel streams only the own tokens, then the merge;
+        #  * prefix: grouped requests with no own tokens (ungrouped ones keep
+        #    one), so the kernel is the prefix-group role.
+        R_ = plan.num_requests
+        ungrouped = torch.full((R_,), -1, dtype=torch.int32, device=dev)
+        slen_p = torch.from_numpy(np.where(plan.group_ids >= 0, 0, 1).astype(np.int32)).to(dev)
+        n_roles = min(args.steps, 400)
+        wall_s, per_s = run(shared=True, trace=True, steps=n_roles, every=4,
+                            inputs=[dict(t, group_ids=ungrouped) for t in layers])
+        wall_p, per_p = run(shared=True, trace=True, steps=n_roles, every=4,
+                            inputs=[dict(t, suffix_lens=slen_p) for t in layers])
+        suffix_bytes = ab["suffix_kv"] + ab["q"] + ab["out"] + ab["lse"]
+        sm_us = per_s["partials_us"] + per_s["merge_us"]
+        pre_us = per_p["partials_us"]
+        roles = {
+            "suffix_merge": {
+                "partials_us": round(per_s["partials_us"], 3), "merge_us": round(per_s["merge_us"], 3),
+                "algorithmic_bytes": suffix_bytes,
+                "gbps": round(suffix_bytes / (sm_us * 1e-6) / 1e9, 1),
+                "frac_of_hbm_peak": round(suffix_bytes / (sm_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                "partials_frac_of_hbm_peak": round((ab["suffix_kv"] + ab["q"]) / (per_s["partials_us"] * 1e-6)
+                                                   / 1e9 / HBM_PEAK_GBPS, 4),
+                "note": "the same call with every request ungrouped (own tokens only): "
+                        "partial-result kernel + merge, kernel events",
+            },
+        }
+        if ab["prefix_flops"] > 0:
+            roles["prefix"] = {
+                "partials_us": round(pre_us, 3),
+                "algorithmic_bytes": ab["prefix_kv"] + ab["q"],
+                "gbps": round((ab["prefix_kv"] + ab["q"]) / (pre_us * 1e-6) / 1e9, 1),
+                "mfma_util": round(ab["prefix_flops"] / (pre_us * 1e-6) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+                "mfma_util_ceiling_at_hbm_peak": round(min(1.0, ab["prefix_flops"] / ab["prefix_kv"]
+                                                           * HBM_PEAK_GBPS / 1e3 / MFMA_F16_PEAK_TFLOPS), 5),
+                "note": "the same call with grouped requests holding no own tokens: the "
+                        "prefix-group role alone, kernel events",
+            }
+        result["roles"] = roles
+        # warm: one layer's KV reused by every call (it stays partly in the
+        # 256 MB Infinity Cache); the headline cycles distinct-KV layers
+        wall_w, _ = run(shared=True, trace=False, steps=n_roles, inputs=[layers[0]])
+        result["warm"] = {"ms_per_step": round(wall_w / n_roles * 1e3, 5),
+                          "value": round(R_ / (wall_w / n_roles), 1),
+                          "note": "one layer's KV reused by every call"}
+
     if not args.no_baselines:
         if nested:
             wall_f, _ = run(shared=True, trace=False, flat_baseline=True)
