@@ -368,7 +368,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU: run with --gpus 1 "
+        print(json.dumps({"error": "this benchmark measures one GPU: run with --gpus 1 "
                                    "(no multi-GPU path exists)"}))
         sys.exit(2)
 

@@ -1,6 +1,6 @@
 """CPU oracle for shared-prefix decode attention -- TEST INFRASTRUCTURE ONLY.
 
-This package is the checker, not the product.  Only the test suite, the smoke
+This package is test infrastructure, not the product.  Only the test suite, the smoke
 check of the entry module and the CPU-baseline leg of the benchmark may import
 it; the library path never calls it and has no CPU fallback.
 

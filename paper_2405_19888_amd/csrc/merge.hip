@@ -76,7 +76,7 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
     }
   };
 
-  // round 1: every lane's lse slot and the first batch of outputs together
+  // first pass: every lane's lse slot and the first batch of outputs together
   const float l_lane = lane < n ? a.lse_part[base + slot_lane] : -INFINITY;
   float v[kBatch][EPL];
 #pragma unroll
