@@ -216,3 +216,24 @@ def test_prefill_contexts_from_store(chunked):
     out, lse = run_prefill(plan, device_dict(data, q, off), off)
     ref = oracle_prefill_for(data, plan, q, off)
     assert_close(*to_np(out, lse), *ref, "bfloat16", f"store prefill chunked={chunked}")
+
+
+@pytest.mark.parametrize("dtype,D", [("float16", 128), ("bfloat16", 64)])
+def test_prefill_long_prefix_max_chunks(dtype, D):
+    """A 9000-token prefix read by enough row tiles that the prefix chunk is
+    the largest one (8192 tokens, a 512-block table) and the prefix splits in
+    two; own prompts of 256 rows.  Sampled rows against the oracle."""
+    say("prefill long prefix", dtype, D)
+    rng = np.random.default_rng(3)
+    plan = build_plan(heads=32, head_dim=D, block_size=16, dtype=dtype,
+                      group_of_request=[0] * 8, prefix_lens=[9000], suffix_lens=[256] * 8,
+                      sm_scale=1.0 / math.sqrt(D), shuffle=True, rng=rng)
+    batch = make_batch(plan, seed=4)
+    q, off = make_prefill_queries(plan, [256] * 8, seed=4)
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off)
+    o, l = to_np(out, lse)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    rows = sorted({0, 1, 127, 128, 255, 256, 1000, 1023, 1024, 2047} |
+                  set(rng.integers(0, 2048, size=6).tolist()))
+    ref = oracle_prefill_for(batch, plan, q, off, rows=rows)
+    assert_close(o[rows], l[rows], *ref, dtype, f"long prefix {dtype} D={D}")
