@@ -45,7 +45,8 @@ KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/partials.hip", "paper_2405_19888_am
                   "paper_2405_19888_amd/csrc/splitkv_role.h", "paper_2405_19888_amd/csrc/common.h"]
 PREFILL_COUNTERS_FILE = os.path.join(ROOT, "profiles", "prefill_counters.json")
 PREFILL_SOURCES = ["paper_2405_19888_amd/csrc/prefill.hip", "paper_2405_19888_amd/csrc/prefill_tile.h",
-                   "paper_2405_19888_amd/csrc/prefix_role.h", "paper_2405_19888_amd/csrc/common.h"]
+                   "paper_2405_19888_amd/csrc/prefill_shape.h", "paper_2405_19888_amd/csrc/prefix_role.h",
+                   "paper_2405_19888_amd/csrc/common.h"]
 
 
 def kernel_source_hash(sources=KERNEL_SOURCES) -> str:

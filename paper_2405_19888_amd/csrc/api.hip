@@ -11,6 +11,7 @@
 #include "parrot_attn.h"
 #include "common.h"
 #include "errors.h"
+#include "prefill_shape.h"
 
 namespace {
 
@@ -415,7 +416,7 @@ parrot_status check_prefill(const parrot_problem* p, const parrot_prefill_rows* 
     return fail(PARROT_ERR_UNSUPPORTED, "num_query_rows * num_heads > 2^31 - 1");
   const int H = p->num_heads;
   pl->depth = p->num_groups > 0 ? (nested ? std::max(1, (int)p->max_prefix_depth) : 1) : 0;
-  const int rows_per_tile = p->dtype == PARROT_DTYPE_F32 ? 64 : 128;   // the kernel's tile height
+  const int rows_per_tile = p->dtype == PARROT_DTYPE_F32 ? 64 : parrot::kWideRows;   // the kernel's tile height
   pl->qtiles_p = (int)ceil_div(mg, rows_per_tile);
   pl->qtiles_o = (int)ceil_div(mq, rows_per_tile);
   if (p->num_groups > 0 && pl->qtiles_p > 0) {

@@ -5,9 +5,9 @@
 // a bandwidth-bound prefix stream cheap, but a prefill tile is bound by the
 // matrix cores, and with 16 queries per wave the LDS reads of K and V, the
 // online softmax and the per-stage bookkeeping cost more than the MFMAs.  Here
-// each wave owns 32 queries as two 16-query column sets that share every K
-// and V fragment read from LDS, so one K read feeds two QK^T MFMAs and one
-// transposed V read feeds two PV MFMAs.  The rest follows tile_core:
+// each wave owns kWideSets (2) 16-query column sets that share every K and V
+// fragment read from LDS, so one K read feeds kWideSets QK^T MFMAs and one
+// transposed V read feeds kWideSets PV MFMAs.  The rest follows tile_core:
 //   * K/V stages of 16 KiB (K and V of 32 tokens for D = 128, 64 for D = 64)
 //     fill a ring of three LDS buffers through direct-to-LDS loads, two stages
 //     ahead; the loads take a scalar base (pool + block * stride) and a
@@ -27,6 +27,7 @@
 
 #include <type_traits>
 
+#include "prefill_shape.h"
 #include "prefix_role.h"
 
 namespace parrot {
@@ -45,7 +46,6 @@ PARROT_DEV int swz_wide(int t) {
   else return (t & 6) | ((t >> 3) & 1);
 }
 
-constexpr int kWideRows = 128;   // query rows per tile: 4 waves x 2 sets x 16
 constexpr int kWideRing = prefix_detail::kRing;   // stage buffers (two stages in flight)
 
 template <int DT, int D, bool CAUSAL>
@@ -77,12 +77,13 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
   const float scale = fmaxf(fabsf(a.scale_log2), 1e-30f);
   const unsigned qsign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
 
-  int qi[2], lim[2];
-  bool q_ok[2];
-  u32x4 qf[2][KS];
+  constexpr int NS = kWideSets;
+  int qi[NS], lim[NS];
+  bool q_ok[NS];
+  u32x4 qf[NS][KS];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    qi[c] = wave * 32 + c * 16 + (lane & 15);
+  for (int c = 0; c < NS; ++c) {
+    qi[c] = wave * 16 * NS + c * 16 + (lane & 15);
     q_ok[c] = qi[c] < nq;
     const int rq = q_ok[c] ? tl.rows[qi[c]] : 0;
     lim[c] = CAUSAL ? (q_ok[c] ? tl.lim[qi[c]] : -1) : 0;
@@ -93,8 +94,8 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       qf[c][ks] = v ^ u32x4{qsign, qsign, qsign, qsign};
     }
   }
-  const bool has_q = wave * 32 < nq;                  // wave-uniform (set 1 may be empty:
-                                                      // it is computed on zero queries)
+  const bool has_q = wave * 16 * NS < nq;             // wave-uniform (the wave's last sets may
+                                                      // be empty: they run on zero queries)
 
   // Direct-to-LDS stage loads: wave w issues chunks w, w + W, ... (1 KiB each);
   // lane l of a chunk fills LDS bytes [16 l, 16 l + 16) of it, i.e. block
@@ -131,11 +132,12 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
     }
   };
 
-  float mref[2] = {-INFINITY, -INFINITY};   // reference max of the exponentials
-  float lsum[2] = {0.f, 0.f};
-  f32x4 o[2][DT16];
+  float mref[NS], lsum[NS];   // reference max of the exponentials, running sum
+  f32x4 o[NS][DT16];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < NS; ++c) { mref[c] = -INFINITY; lsum[c] = 0.f; }
+#pragma unroll
+  for (int c = 0; c < NS; ++c)
 #pragma unroll
     for (int i = 0; i < DT16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -161,22 +163,22 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       for (int ks = 0; ks < KS; ++ks)
         kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz_wide<GRAN>(kt_row)) << 4));
     }
-    f32x4 s[2][2];
+    f32x4 s[NS][2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < NS; ++c)
 #pragma unroll
       for (int b = 0; b < 2; ++b) s[c][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        s[0][b] = Mfma<DT>::qk(kf[b][ks], qf[0][ks], s[0][b]);
-        s[1][b] = Mfma<DT>::qk(kf[b][ks], qf[1][ks], s[1][b]);
+#pragma unroll
+        for (int c = 0; c < NS; ++c) s[c][b] = Mfma<DT>::qk(kf[b][ks], qf[c][ks], s[c][b]);
       }
 
-    unsigned long long pk[2][2];
+    unsigned long long pk[NS][2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < NS; ++c) {
       float x[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) { x[i] = s[c][0][i]; x[4 + i] = s[c][1][i]; }
@@ -214,8 +216,8 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
       const int off = ((2 * dt + vt_pair) ^ swz_wide<GRAN>(vt_row)) << 4;
       const unsigned long long va = Mfma<DT>::tr_read(vrow + off);
       const unsigned long long vb2 = Mfma<DT>::tr_read(vrow + BLK_B + off);
-      o[0][dt] = Mfma<DT>::pv2(va, vb2, pk[0][0], pk[0][1], o[0][dt]);
-      o[1][dt] = Mfma<DT>::pv2(va, vb2, pk[1][0], pk[1][1], o[1][dt]);
+#pragma unroll
+      for (int c = 0; c < NS; ++c) o[c][dt] = Mfma<DT>::pv2(va, vb2, pk[c][0], pk[c][1], o[c][dt]);
     }
   };
 
@@ -228,7 +230,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
   }
   table(min(kRing - 1, last), tb);
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < NS; ++c)
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) asm volatile("" : : "v"(qf[c][ks]));
   wait_vmcnt<0>();
@@ -282,7 +284,7 @@ __device__ __forceinline__ void wide_tile(const TileJob& a, const TileLds& tl, i
 
   if (!has_q) return;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NS; ++c) {
     float lt = sum_xor16(lsum[c]);
     lt = sum_xor32(lt);
     if (q_ok[c]) {
