@@ -45,8 +45,8 @@ KERNEL_SOURCES = ["paper_2405_19888_amd/csrc/partials.hip", "paper_2405_19888_am
                   "paper_2405_19888_amd/csrc/splitkv_role.h", "paper_2405_19888_amd/csrc/common.h"]
 PREFILL_COUNTERS_FILE = os.path.join(ROOT, "profiles", "prefill_counters.json")
 PREFILL_SOURCES = ["paper_2405_19888_amd/csrc/prefill.hip", "paper_2405_19888_amd/csrc/prefill_tile.h",
-                   "paper_2405_19888_amd/csrc/prefill_shape.h", "paper_2405_19888_amd/csrc/prefix_role.h",
-                   "paper_2405_19888_amd/csrc/common.h"]
+                   "paper_2405_19888_amd/csrc/prefill_shape.h", "paper_2405_19888_amd/csrc/prefill_args.h",
+                   "paper_2405_19888_amd/csrc/prefix_role.h", "paper_2405_19888_amd/csrc/common.h"]
 
 
 def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
@@ -201,7 +201,8 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
     distinct-KV layers.  Returns the leg's JSON object."""
     import numpy as np
     import torch
-    from paper_2405_19888_amd import ParrotTrace, Prefiller, parrot_validate_prefill_inputs
+    from paper_2405_19888_amd import (ParrotTrace, Prefiller, parrot_prefill_single_pass,
+                                      parrot_validate_prefill_inputs)
     from paper_2405_19888_amd import prefill_rows_from_host, problem_from_host
     from workloads import (get_config, make_device_layer, make_device_prefill_queries, make_plan,
                            one_group_per_request, prefill_rows)
@@ -240,6 +241,7 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
                                    t0["prefix_lens"], t0["prefix_parents"] if plan.nested else None,
                                    t0["suffix_tables"], t0["suffix_lens"], t0["group_ids"], scratch)
     pre = Prefiller(prob, rows, device=dev)
+    single = parrot_prefill_single_pass(prob, rows, nested=plan.nested)
     stream = torch.cuda.current_stream()
 
     def timed(calls, trace: bool):
@@ -260,8 +262,9 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
         wall = time.perf_counter() - w0
         per = None
         if trace:
-            per = {"prefill_us": sum(e[0].elapsed_time(e[1]) for e in events) * 1e3 / steps,
-                   "merge_us": sum(e[2].elapsed_time(e[3]) for e in events) * 1e3 / steps}
+            per = {"prefill_us": sum(e[0].elapsed_time(e[1]) for e in events) * 1e3 / steps}
+            if not single:
+                per["merge_us"] = sum(e[2].elapsed_time(e[3]) for e in events) * 1e3 / steps
         return wall, per
 
     calls = [pre.bind(t, stream=stream, nested=plan.nested) for t in layers]
@@ -282,8 +285,12 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
                    "rows_per_request_mean": round(float(np.mean(qr)), 1),
                    "own_len_mean": round(float(plan.suffix_lens.mean()), 1),
                    "layers_cycled": n_layers},
+        "plan": ("single pass: one kernel, no partial results, no merge" if single else
+                 "split: prefix and own partial results, then the merge kernel"),
         "roofline": {
-            "kernel": "k_prefill (prefix items + causal own items, MFMA)",
+            "kernel": ("k_prefill single pass (group tiles: the prefix, then their rows' own "
+                       "tokens; MFMA)" if single else
+                       "k_prefill (prefix items + causal own items, MFMA)"),
             "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / MFMA_F16_PEAK_TFLOPS, 4),
             "traffic": traffic_from_counters(cfg.name, PREFILL_COUNTERS_FILE, PREFILL_SOURCES),

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 3
+#define PARROT_ABI_VERSION 4
 
 typedef enum {
   PARROT_OK = 0,
@@ -275,11 +275,24 @@ parrot_status parrot_validate_nested_inputs(
  * prefill).  Per row and head the result is the decode formula over those
  * keys.
  *
- * Two kernels run on `stream`: the partial-result kernel (prefix items: the
- * rows of all requests reading a group's prefix, 64 per tile, against one
- * prefix chunk staged in LDS; own items: 64 rows of one request against one
- * chunk of its own tokens with a per-row causal limit; both on MFMA), then the
- * merge kernel per (row, head).
+ * Rows are computed in tiles of 128 (fp16 / bf16 caches) or 64 (fp32) on
+ * MFMA, with K/V staged in LDS.  Two plans, chosen per call:
+ *   single pass (flat groups, 16-bit caches, prefix and own lengths that fit
+ *     one chunk of 8192 tokens and enough tiles to fill the device): one
+ *     kernel; a tile of the rows of a group's members (all requests reading
+ *     the prefix, stacked) sees the whole prefix and then, request by
+ *     request, its rows' own tokens up to their positions; ungrouped
+ *     requests' tiles see their own tokens; the output is written directly
+ *     and the workspace is not used;
+ *   split: prefix items (stacked rows against one prefix chunk) and own
+ *     items (one request's rows against one chunk of its own tokens, per-row
+ *     causal limit) write partial results to the workspace, then the merge
+ *     kernel combines them per (row, head).
+ * parrot_prefill_single_pass tells which one a call takes.  The environment
+ * variable PARROT_PREFILL_SINGLE_PASS=0 forces the split plan; =1 takes the
+ * single pass wherever the groups are flat, the caches 16-bit and the lengths
+ * at most 8192 (even when the split plan would cut them into chunks to fill
+ * the device).  Both plans give the same results to rounding.
  *
  *   rows                 (host) row counts; see parrot_prefill_rows
  *   q                    [T][H][D] dtype, 16-byte aligned
@@ -305,6 +318,12 @@ typedef struct {
  * depends on the current device's compute-unit count like
  * parrot_workspace_bytes.  (size_t)-1 if the arguments are invalid. */
 size_t parrot_prefill_workspace_bytes(const parrot_problem* p, const parrot_prefill_rows* rows);
+
+/* 1 when parrot_shared_prefix_prefill takes the single pass for these
+ * arguments on the current device, 0 when it takes the split plan, -1 if the
+ * arguments are invalid.  `nested` is nonzero when prefix_parents will be
+ * non-NULL (nested groups always take the split plan). */
+int parrot_prefill_single_pass(const parrot_problem* p, const parrot_prefill_rows* rows, int nested);
 
 parrot_status parrot_shared_prefix_prefill(
     const parrot_problem* p, const parrot_prefill_rows* rows,

@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     parrot_last_error,
     parrot_nested_prefix_decode,
     parrot_per_request_decode,
+    parrot_prefill_single_pass,
     parrot_prefill_workspace_bytes,
     parrot_shared_prefix_decode,
     parrot_shared_prefix_decode_append,

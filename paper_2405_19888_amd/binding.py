@@ -72,7 +72,7 @@ EXPORTED = (
     "parrot_workspace_bytes", "parrot_shared_prefix_decode", "parrot_per_request_decode",
     "parrot_nested_prefix_decode", "parrot_shared_prefix_decode_append",
     "parrot_validate_inputs", "parrot_validate_nested_inputs",
-    "parrot_prefill_workspace_bytes", "parrot_shared_prefix_prefill",
+    "parrot_prefill_workspace_bytes", "parrot_prefill_single_pass", "parrot_shared_prefix_prefill",
     "parrot_validate_prefill_inputs", "parrot_last_error", "parrot_abi_version",
 )
 
@@ -121,6 +121,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         lib.parrot_validate_prefill_inputs.argtypes = [prob_p, rows_p, i32p, i32p, i32p, i32p,
                                                        i32p, i32p, i32p, vp, vp]
         lib.parrot_validate_prefill_inputs.restype = ctypes.c_int
+    if hasattr(lib, "parrot_prefill_single_pass"):       # absent from ABI 1-3 builds
+        lib.parrot_prefill_single_pass.argtypes = [prob_p, rows_p, ctypes.c_int]
+        lib.parrot_prefill_single_pass.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []
@@ -283,6 +286,17 @@ def parrot_prefill_workspace_bytes(problem: ParrotProblem, rows: ParrotPrefillRo
     if n == ctypes.c_size_t(-1).value:
         raise ParrotError(PARROT_ERR_INVALID_ARGUMENT, parrot_last_error())
     return int(n)
+
+
+def parrot_prefill_single_pass(problem: ParrotProblem, rows: ParrotPrefillRows,
+                               nested: bool = False) -> bool:
+    """Whether the prefill entry point takes the single pass for these
+    arguments (else partial results and the merge kernel)."""
+    r = load_library().parrot_prefill_single_pass(ctypes.byref(problem), ctypes.byref(rows),
+                                                  1 if nested else 0)
+    if r < 0:
+        raise ParrotError(PARROT_ERR_INVALID_ARGUMENT, parrot_last_error())
+    return bool(r)
 
 
 def parrot_shared_prefix_prefill(problem, rows, q, query_offsets, prefix_k, prefix_v, suffix_k,

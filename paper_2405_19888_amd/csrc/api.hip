@@ -5,12 +5,14 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <algorithm>
 #include <string>
 
 #include "parrot_attn.h"
 #include "common.h"
 #include "errors.h"
+#include "prefill_args.h"
 #include "prefill_shape.h"
 
 namespace {
@@ -374,8 +376,20 @@ constexpr int kPrefillChunkMin = 256;
 struct PrefillPlan {
   int depth, cp, co, seg_p, seg_pre, seg_s, seg, qtiles_p, qtiles_o;
   long n_pre, n_own;
+  bool single;   // single-pass items: no partial results, no merge
   size_t o_bytes, lse_bytes, info_bytes, total_bytes;
 };
+
+// The single-pass prefill runs when the groups are flat, the caches 16-bit and
+// the prefix and own ranges each fit one chunk of the split plan.
+// PARROT_PREFILL_SINGLE_PASS=0 turns it off; =1 takes it whenever the ranges
+// fit the tile's block table (8192 tokens), even where the split plan would
+// cut them into chunks to fill the device (for tests and tuning).
+int single_pass_setting() {
+  const char* e = std::getenv("PARROT_PREFILL_SINGLE_PASS");
+  if (!e || !*e) return -1;
+  return e[0] == '0' ? 0 : 1;
+}
 
 // Chunk of a key range of at most `len` tokens: the whole range up to 8192
 // tokens (fewest partial results), halved while the items of that chunk size
@@ -437,6 +451,14 @@ parrot_status check_prefill(const parrot_problem* p, const parrot_prefill_rows* 
   // per XCD)
   pl->n_pre = (long)p->num_groups * pl->seg_p * pl->qtiles_p;
   pl->n_own = (long)p->num_requests * pl->seg_s * pl->qtiles_o;
+  const int setting = single_pass_setting();
+  const bool fits = p->max_prefix_len <= kPrefillChunkMax && p->max_suffix_len <= kPrefillChunkMax;
+  pl->single = p->dtype != PARROT_DTYPE_F32 && !nested && fits &&
+               (setting == 1 || (setting == -1 && pl->seg_p <= 1 && pl->seg_s == 1));
+  if (pl->single) {   // one item per group tile (whole prefix), one per own tile
+    pl->n_pre = pl->seg_p > 0 ? (long)p->num_groups * pl->qtiles_p : 0;
+    pl->n_own = (long)p->num_requests * pl->qtiles_o;
+  }
   const long grid = 8L * ceil_div(H, 8) * (pl->n_pre + pl->n_own);
   if (grid > 0x7fffffffL)
     return fail(PARROT_ERR_UNSUPPORTED, "prefill needs %ld workgroups (at most 2^31 - 1)", grid);
@@ -504,13 +526,19 @@ parrot_status prefill(const parrot_problem* p, const parrot_prefill_rows* rows, 
     a.seg = pl.seg; a.seg_p = pl.seg_p; a.seg_pre = pl.seg_pre; a.seg_s = pl.seg_s;
     a.cp = pl.cp; a.co = pl.co; a.qtiles_p = pl.qtiles_p; a.qtiles_o = pl.qtiles_o;
     a.n_pre = (int)pl.n_pre; a.n_own = (int)pl.n_own;
-    a.meta_wgs = (T + 255) / 256;
+    a.meta_wgs = pl.single ? 0 : (T + 255) / 256;
     a.scale_log2 = p->sm_scale * parrot::kLog2e;
+    a.single = pl.single ? 1 : 0;
+    a.out = out; a.lse = lse;
     PARROT_TRY(launched(parrot::launch_prefill(a, (int)p->dtype, p->head_dim, s, ev(tr.partials_start),
                                                ev(tr.partials_stop)),
                         "prefill kernel"));
   }
-  {
+  if (pl.single) {
+    // no merge: its trace events, if asked for, bracket nothing
+    if (tr.merge_start) PARROT_TRY(hip_ok(hipEventRecord(ev(tr.merge_start), s), "hipEventRecord"));
+    if (tr.merge_stop) PARROT_TRY(hip_ok(hipEventRecord(ev(tr.merge_stop), s), "hipEventRecord"));
+  } else {
     parrot::MergeArgs a{};
     a.o_part = o_part; a.lse_part = lse_part; a.merge_meta = merge_meta;
     a.out = out; a.lse = lse;
@@ -534,6 +562,13 @@ size_t parrot_prefill_workspace_bytes(const parrot_problem* p, const parrot_pref
   if (check_prefill(p, rows, true, &pl) != PARROT_OK) return (size_t)-1;
   g_err.clear();
   return pl.total_bytes;
+}
+
+int parrot_prefill_single_pass(const parrot_problem* p, const parrot_prefill_rows* rows, int nested) {
+  PrefillPlan pl;
+  if (check_prefill(p, rows, nested != 0, &pl) != PARROT_OK) return -1;
+  g_err.clear();
+  return pl.single ? 1 : 0;
 }
 
 parrot_status parrot_shared_prefix_prefill(

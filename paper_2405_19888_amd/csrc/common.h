@@ -89,30 +89,6 @@ struct MergeArgs {
   int seg, seg_p, seg_pre;   // slots per sequence, per prefix level, before the pieces
 };
 
-// Prefill of the new rows of forked contexts.  Rows [qoff[r], qoff[r+1]) of
-// q are request r's last Q_r own tokens.  Partial results use the decode
-// layout with rows in place of requests: o_part [T][H][seg][D], slots
-// [l*seg_p, (l+1)*seg_p) for prefix level l, [seg_pre, seg) for own-token
-// chunks of co tokens; merge_meta [T][4].
-struct PrefillArgs {
-  const void* q;         // [T][H][D]
-  const void* pk; const void* pv;
-  const void* sk; const void* sv;
-  const int* ptab; const int* plen; const int* stab; const int* slen; const int* gid;
-  const int* parents;    // nested groups (NULL: flat)
-  const int* qoff;       // [R + 1]
-  float* o_part; float* lse_part;
-  int* merge_meta;
-  int T, R, H, NG, depth;
-  int pstride, sstride, max_p, max_s, max_q, npblk, nsblk;
-  int seg, seg_p, seg_pre, seg_s;
-  int cp, co;            // prefix and own chunk tokens
-  int qtiles_p, qtiles_o;   // 64-row tiles per group, per request
-  int n_pre, n_own;      // prefix-chunk and own-chunk work items per head
-  int meta_wgs;          // workgroups that also write the row descriptors (256 rows each)
-  float scale_log2;
-};
-
 struct ValidateArgs {
   const int* ptab; const int* plen; const int* stab; const int* slen; const int* gid;
   const int* parents;    // nested groups (NULL: flat)
@@ -138,7 +114,6 @@ struct PartialsArgs {
 // Each launcher attaches the optional (start, stop) timing events to its kernel.
 // a.skv.k_new != NULL selects the kernel that also appends this step's token
 hipError_t launch_partials(const PartialsArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_prefill(const PrefillArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
 

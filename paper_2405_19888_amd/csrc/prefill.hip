@@ -21,11 +21,17 @@
 // then combines them per row, reading the row descriptors that the first
 // workgroups write.
 //
+// When the prefix and the own tokens each fit one chunk and the groups are
+// flat, one pass does it all (single-pass items, no partial results, no
+// merge): a group tile's rows see the prefix and then, run by run, their own
+// requests' tokens; ungrouped requests' tiles see only their own tokens.
+//
 // Work items are placed per XCD (workgroup b runs on XCD b mod 8): XCD x takes
 // every item of heads x, x + 8, ..., one head after another, prefix items
 // before own items and row tiles fastest.  Each XCD then holds the same share
 // of the work, and the workgroups that run together on it read the same head's
 // key chunk, which stays in that XCD's L2.
+#include "prefill_args.h"
 #include "prefill_tile.h"
 
 namespace parrot {
@@ -34,7 +40,9 @@ constexpr int kPrefillMaxBlocks = 512;                       // chunk <= 8192 to
 // query rows per tile: the wide tile for 16-bit caches, decode's tile for fp32
 template <int DT> constexpr int kTileRows = DT == kF32 ? kPrefixWaves * 16 : kWideRows;
 template <int DT> constexpr int kTileRing = DT == kF32 ? prefix_detail::kRing : kWideRing;
-constexpr int kPrefillLds = tile_lds_bytes(kPrefillMaxBlocks, kWideRows, kWideRing);
+constexpr int kPrefillTileLds = tile_lds_bytes(kPrefillMaxBlocks, kWideRows, kWideRing);
+// single-pass tiles also keep their runs of rows per request after the tile's view
+constexpr int kPrefillLds = kPrefillTileLds + kWideRows * (int)sizeof(int2);
 constexpr int kPrefillLdsF32 = tile_lds_bytes(kPrefillMaxBlocks);
 
 // The one LDS view of a prefill tile: its stage ring, rows, block table and
@@ -43,6 +51,9 @@ template <int DT>
 PARROT_DEV TileLds prefill_lds(char* lds) {
   return TileLds(lds, kPrefillMaxBlocks, kTileRows<DT>, kTileRing<DT>);
 }
+// The single-pass tile's runs: (request, first tile row) per run of rows.
+PARROT_DEV int2* prefill_runs(char* lds) { return reinterpret_cast<int2*>(lds + kPrefillTileLds); }
+static_assert(kPrefillTileLds % 8 == 0, "runs are 8-byte aligned");
 constexpr int kXcds = 8;                                     // workgroups go round-robin over XCDs
 
 
@@ -202,16 +213,120 @@ __device__ __forceinline__ void prefill_own_item(const PrefillArgs& a, char* lds
     wide_tile<DT, D, true>(j, tl, nq);
 }
 
+// Single-pass group tile (g, row tile qt, head h) of flat groups: rows of the
+// requests in group g, stacked as for the prefix items, against the whole
+// prefix and then each run's own tokens; writes the rows' output.
+template <int DT, int D>
+__device__ __forceinline__ void prefill_single_group_item(const PrefillArgs& a, char* lds, int h,
+                                                          int item) {
+  const int qt = item % a.qtiles_p;
+  const int g = item / a.qtiles_p;
+  if (g >= a.NG) return;
+  const int P = clampi(a.plen[g], 0, a.max_p);
+  constexpr int ROWS = kWideRows;
+  const TileLds tl = prefill_lds<DT>(lds);
+  int2* runs = prefill_runs(lds);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const long qbase = (long)qt * ROWS;
+  const int nb = (P + kBlock - 1) / kBlock;
+  if (wave == 0) {
+    // rows of g's members in request order: this tile takes rows [qbase,
+    // qbase + ROWS) of that list, with their own positions and one run per
+    // request that has rows in it
+    long base = 0;
+    int nruns = 0;
+    for (int b = 0; b < a.R && base < qbase + ROWS; b += kWave) {
+      const int r = b + lane;
+      ReqRows rw = {0, 0, 0};
+      if (r < a.R && a.gid[r] == g) rw = req_rows(a, r);
+      long inc = rw.count;                             // inclusive scan over lanes
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) {
+        const long v = __shfl_up(inc, d);
+        if (lane >= d) inc += v;
+      }
+      const long first = base + inc - rw.count;
+      const long lo = first > qbase ? first : qbase;
+      const long hi = min(first + rw.count, qbase + ROWS);
+      for (long x = lo; x < hi; ++x) {
+        tl.rows[x - qbase] = rw.start + (int)(x - first);
+        tl.lim[x - qbase] = rw.S - rw.count + (int)(x - first);
+      }
+      const unsigned long long has = __builtin_amdgcn_ballot_w64(hi > lo);
+      if (hi > lo) {
+        const int k = nruns + __builtin_popcountll(has & ((1ull << lane) - 1ull));
+        runs[k] = int2{r, (int)(lo - qbase)};
+      }
+      nruns += __builtin_popcountll(has);
+      base += __shfl(inc, kWave - 1);
+    }
+    if (lane == 0) {
+      tl.count[0] = (int)(base - qbase > ROWS ? ROWS : (base - qbase < 0 ? 0 : base - qbase));
+      tl.count[1] = nruns;
+    }
+  } else if (wave == 1) {
+    const int* tbl = a.ptab + (long)g * a.pstride;
+    for (int i = lane; i < nb; i += kWave) tl.tbl[i] = clampi(tbl[i], 0, a.npblk - 1);
+  }
+  __syncthreads();
+  const int nq = tl.count[0];
+  if (nq <= 0) return;                                 // uniform over the workgroup
+  TileJob j;
+  j.q = a.q; j.pk = a.pk; j.pv = a.pv; j.npool = a.npblk; j.H = a.H; j.h = h;
+  j.t0 = 0; j.t1 = P; j.o_part = nullptr; j.lse_part = nullptr;
+  j.seg = 0; j.slot = 0; j.scale_log2 = a.scale_log2; j.lim_min = 0;
+  const WideSingle sg{a.sk, a.sv, a.stab, a.sstride, a.nsblk, runs, tl.count[1], a.out, a.lse};
+  wide_tile_single<DT, D>(j, tl, nq, sg);
+}
+
+// Single-pass own tile (request r, row tile t, head h) of a request outside
+// the groups: its rows against its own tokens, causal; writes their output.
+// Grouped requests' rows belong to their group's tiles.
+template <int DT, int D>
+__device__ __forceinline__ void prefill_single_own_item(const PrefillArgs& a, char* lds, int h,
+                                                        int item) {
+  const int t = item % a.qtiles_o;
+  const int r = item / a.qtiles_o;
+  if (r >= a.R) return;
+  const int g = a.gid[r];
+  if (g >= 0 && g < a.NG) return;
+  constexpr int ROWS = kWideRows;
+  const ReqRows rw = req_rows(a, r);
+  const int row0 = t * ROWS;
+  if (row0 >= rw.count) return;
+  const int nq = min(ROWS, rw.count - row0);
+  const int pos0 = rw.S - rw.count + row0;             // position of the tile's first row
+  const TileLds tl = prefill_lds<DT>(lds);
+  int2* runs = prefill_runs(lds);
+  const int tid = threadIdx.x;
+  if (tid < nq) {
+    tl.rows[tid] = rw.start + row0 + tid;
+    tl.lim[tid] = pos0 + tid;
+  }
+  if (tid == 0) runs[0] = int2{r, 0};
+  __syncthreads();
+  TileJob j;
+  j.q = a.q; j.pk = a.sk; j.pv = a.sv; j.npool = a.nsblk; j.H = a.H; j.h = h;
+  j.t0 = 0; j.t1 = 0; j.o_part = nullptr; j.lse_part = nullptr;  // no prefix range
+  j.seg = 0; j.slot = 0; j.scale_log2 = a.scale_log2; j.lim_min = 0;
+  const WideSingle sg{a.sk, a.sv, a.stab, a.sstride, a.nsblk, runs, 1, a.out, a.lse};
+  wide_tile_single<DT, D>(j, tl, nq, sg);
+}
+
 // Occupancy: three waves per SIMD (three workgroups per CU: 3 x 51 KiB of
 // LDS, at most 168 registers per lane), for either tile core.
-template <int DT, int D>
+// SINGLE: single-pass items (16-bit caches); otherwise prefix and own items
+// with partial results and row descriptors for the merge.
+template <int DT, int D, bool SINGLE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 void k_prefill(PrefillArgs a) {
+  static_assert(!SINGLE || DT != kF32, "single-pass tiles are the 16-bit wide tiles");
   __shared__ __attribute__((aligned(1024))) char lds[DT == kF32 ? kPrefillLdsF32 : kPrefillLds];
   static_assert(sizeof(lds) >= tile_lds_bytes(kPrefillMaxBlocks, kTileRows<DT>, kTileRing<DT>),
                 "the LDS array holds the tile's layout");
   const int bid = blockIdx.x;
-  if (bid < a.meta_wgs) {
+  if (!SINGLE && bid < a.meta_wgs) {
     const int t = bid * 256 + (int)threadIdx.x;
     if (t < a.T) write_row_meta(a, t);
   }
@@ -221,10 +336,17 @@ void k_prefill(PrefillArgs a) {
   const int j = l / per, item = l % per;
   const int h = x + kXcds * j;
   if (h >= a.H) return;
-  if (item < a.n_pre)
-    prefill_prefix_item<DT, D>(a, lds, h, item);
-  else
-    prefill_own_item<DT, D>(a, lds, h, item - a.n_pre);
+  if constexpr (SINGLE) {
+    if (item < a.n_pre)
+      prefill_single_group_item<DT, D>(a, lds, h, item);
+    else
+      prefill_single_own_item<DT, D>(a, lds, h, item - a.n_pre);
+  } else {
+    if (item < a.n_pre)
+      prefill_prefix_item<DT, D>(a, lds, h, item);
+    else
+      prefill_own_item<DT, D>(a, lds, h, item - a.n_pre);
+  }
 }
 
 template <int DT, int D>
@@ -232,7 +354,13 @@ static hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t s, hipEvent
   const long items = (long)kXcds * ((a.H + kXcds - 1) / kXcds) * ((long)a.n_pre + a.n_own);
   const long blocks = items > a.meta_wgs ? items : a.meta_wgs;
   if (blocks <= 0) return hipSuccess;
-  hipExtLaunchKernelGGL((k_prefill<DT, D>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+  if constexpr (DT != kF32) {
+    if (a.single) {
+      hipExtLaunchKernelGGL((k_prefill<DT, D, true>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
+      return hipGetLastError();
+    }
+  }
+  hipExtLaunchKernelGGL((k_prefill<DT, D, false>), dim3((unsigned)blocks), dim3(256), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 
@@ -243,7 +371,9 @@ hipError_t launch_prefill(const PrefillArgs& a, int dtype, int D, hipStream_t s,
   if (a.cp % 32 != 0 || a.co % 32 != 0 || a.cp > kPrefillMaxBlocks * kBlock ||
       a.co > kPrefillMaxBlocks * kBlock || a.cp < 32 || a.co < 32)
     return hipErrorInvalidValue;
-  if (a.meta_wgs != (a.T + 255) / 256 || a.n_pre < 0 || a.n_own < 1 ||
+  if (a.single && (dtype == kF32 || a.parents || a.depth != 1 || !a.out || !a.lse))
+    return hipErrorInvalidValue;
+  if (a.meta_wgs != (a.single ? 0 : (a.T + 255) / 256) || a.n_pre < 0 || a.n_own < 1 ||
       (long)kXcds * ((a.H + kXcds - 1) / kXcds) * ((long)a.n_pre + a.n_own) > 0x7fffffffL)
     return hipErrorInvalidValue;
   switch (dtype * 1000 + D) {

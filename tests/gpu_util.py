@@ -90,9 +90,11 @@ def prefill_rows_for(plan, offsets):
 
 
 def run_prefill(plan, dev: dict, offsets, problem=None, rows=None, poison: bool = True,
-                nested: bool = None):
+                nested: bool = None, keep: list = None):
     """Validate the prefill inputs on the device, poison outputs and
-    workspace, run the prefill entry point, sync."""
+    workspace, run the prefill entry point, sync.  `keep` (a list) receives
+    the Prefiller, whose workspace shows which path ran: the single pass
+    writes none of it."""
     from paper_2405_19888_amd import Prefiller, parrot_validate_prefill_inputs
     nested = plan.nested if nested is None else nested
     prob = problem or problem_for(plan)
@@ -109,7 +111,14 @@ def run_prefill(plan, dev: dict, offsets, problem=None, rows=None, poison: bool 
         pre.workspace.fill_(0xFF)
     out, lse = pre(dev, nested=nested)
     torch.cuda.synchronize()
+    if keep is not None:
+        keep.append(pre)
     return out, lse
+
+
+def workspace_untouched(pre) -> bool:
+    """True when no byte of the prefill workspace changed from the 0xFF poison."""
+    return bool(torch.all(pre.workspace.view(torch.uint8) == 0xFF).item())
 
 
 def oracle_prefill_for(batch, plan, q_rows, offsets, rows=None, pools=None):

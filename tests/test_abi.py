@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 3
+    assert B.parrot_abi_version() == 4
 
 
 def base_problem(**over):
@@ -214,6 +214,35 @@ def test_prefill_workspace_sizes(parrot_lib):
                                                                max_group_rows=32 * 128)) < w
     # nested groups need a slot range per level
     assert B.parrot_prefill_workspace_bytes(base_problem(max_prefix_depth=3), prefill_rows()) > w
+
+
+def test_prefill_single_pass_choice(parrot_lib, monkeypatch):
+    """The single pass needs flat groups, 16-bit caches and lengths within one
+    8192-token chunk; by default it also needs tiles enough to fill the device
+    without cutting the ranges into chunks (256 CUs assumed without a GPU)."""
+    monkeypatch.delenv("PARROT_PREFILL_SINGLE_PASS", raising=False)
+    prob, rows = base_problem(), prefill_rows()
+    assert B.parrot_prefill_single_pass(prob, rows)                   # 64 row tiles x 32 heads
+    assert not B.parrot_prefill_single_pass(prob, rows, nested=True)
+    assert not B.parrot_prefill_single_pass(base_problem(dtype=0), rows)
+    assert B.parrot_prefill_single_pass(base_problem(dtype=2), rows)
+    few = prefill_rows(num_query_rows=32 * 16, max_query_rows=16, max_group_rows=32 * 16)
+    assert not B.parrot_prefill_single_pass(prob, few)                # 4 tiles: chunked
+    long_prefix = base_problem(max_prefix_len=9000, prefix_table_stride=563)
+    assert not B.parrot_prefill_single_pass(long_prefix, rows)        # two 8192-token chunks
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "1")
+    assert B.parrot_prefill_single_pass(prob, few)
+    assert not B.parrot_prefill_single_pass(long_prefix, rows)
+    assert not B.parrot_prefill_single_pass(prob, rows, nested=True)
+    assert not B.parrot_prefill_single_pass(base_problem(dtype=0), few)
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "0")
+    assert not B.parrot_prefill_single_pass(prob, rows)
+    # the workspace bound does not depend on the plan
+    w = B.parrot_prefill_workspace_bytes(prob, rows)
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "1")
+    assert B.parrot_prefill_workspace_bytes(prob, rows) == w
+    with pytest.raises(B.ParrotError, match="max_query_rows"):
+        B.parrot_prefill_single_pass(prob, prefill_rows(max_query_rows=0))
 
 
 @pytest.mark.parametrize("over,msg", [

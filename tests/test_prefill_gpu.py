@@ -14,7 +14,8 @@ import pytest
 import torch
 
 from gpu_util import (assert_close, oracle_prefill_for, prefill_rows_for, problem_for,
-                      run_prefill, to_np)
+                      run_prefill, to_np, workspace_untouched)
+from paper_2405_19888_amd import parrot_prefill_single_pass
 from workloads import build_plan, make_batch, make_prefill_queries
 
 pytestmark = pytest.mark.gpu
@@ -100,6 +101,44 @@ def test_prefill_parity(kind, dtype, D):
     assert_close(*to_np(out, lse), *ref, dtype, f"prefill {kind} {dtype} D={D}")
 
 
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
+@pytest.mark.parametrize("kind", ["mixed", "wide_group", "long_rows", "single"])
+def test_prefill_single_pass_parity(kind, dtype, D, monkeypatch):
+    """The single-pass path (each group tile sees the whole prefix, then its
+    rows' own tokens run by run; ungrouped requests' tiles their own tokens)
+    on the same cases, forced where the split plan would cut the ranges into
+    chunks.  It writes no partial results: the poisoned workspace stays as it
+    was, which shows that this path ran."""
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "1")
+    say("prefill single pass", kind, dtype, D)
+    plan, qr = prefill_case(kind, dtype, D)
+    batch = make_batch(plan, seed=5)
+    q, off = make_prefill_queries(plan, qr, seed=5)
+    keep = []
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off, keep=keep)
+    assert workspace_untouched(keep[0]), "the split path ran"
+    assert parrot_prefill_single_pass(problem_for(plan), prefill_rows_for(plan, off))
+    ref = oracle_prefill_for(batch, plan, q, off)
+    assert_close(*to_np(out, lse), *ref, dtype, f"single pass {kind} {dtype} D={D}")
+
+
+@pytest.mark.parametrize("kind,dtype", [("nested", "float16"), ("mixed", "float32")])
+def test_prefill_single_pass_not_taken(kind, dtype, monkeypatch):
+    """Nested groups and fp32 caches keep the split path (partial results and
+    the merge) even when the single pass is asked for."""
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "1")
+    say("prefill single pass not taken", kind, dtype)
+    plan, qr = prefill_case(kind, dtype, 64)
+    batch = make_batch(plan, seed=6)
+    q, off = make_prefill_queries(plan, qr, seed=6)
+    keep = []
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off, keep=keep)
+    assert not workspace_untouched(keep[0])
+    ref = oracle_prefill_for(batch, plan, q, off)
+    assert_close(*to_np(out, lse), *ref, dtype, f"split {kind} {dtype}")
+
+
 def test_prefill_rows_as_decode():
     """One row per request at its last own token is a decode step: the prefill
     result equals the decode entry point's on the same queries."""
@@ -155,11 +194,18 @@ def test_prefill_validation_catches_bad_rows():
                                  rows.max_group_rows - 1), msg="max_group_rows")
 
 
-@pytest.mark.parametrize("name", ["prefill", "prefill_q16"])
-def test_prefill_workload_sampled(name):
+@pytest.mark.parametrize("name,path", [("prefill", "auto"), ("prefill", "split"),
+                                       ("prefill_q16", "auto")])
+def test_prefill_workload_sampled(name, path, monkeypatch):
     """The benchmark's prefill workloads at full size, in the launch the
-    benchmark times: sampled rows (first and last rows of requests, rows at
-    row-tile edges, random rows) against the oracle, and every row finite."""
+    benchmark times (whole prompts: the single pass; 16 rows per request: the
+    split plan, whose chunks fill the device), and whole prompts on the split
+    path too: sampled rows (first and last rows of requests, rows at row-tile
+    edges, random rows) against the oracle, and every row finite."""
+    if path == "split":
+        monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "0")
+    else:
+        monkeypatch.delenv("PARROT_PREFILL_SINGLE_PASS", raising=False)
     from workloads import (get_config, make_device_layer, make_device_prefill_queries,
                            make_plan, prefill_rows)
     cfg = get_config(name)
@@ -169,7 +215,11 @@ def test_prefill_workload_sampled(name):
     dev = make_device_layer(plan, 0, "cuda", seed=cfg.seed)
     dev["q_rows"], dev["query_offsets"] = make_device_prefill_queries(plan, qr, "cuda", cfg.seed, 0)
     off = dev["query_offsets"].cpu().numpy()
-    out, lse = run_prefill(plan, dev, off)
+    keep = []
+    out, lse = run_prefill(plan, dev, off, keep=keep)
+    single = name == "prefill" and path == "auto"
+    assert workspace_untouched(keep[0]) == single, "unexpected prefill path"
+    assert parrot_prefill_single_pass(problem_for(plan), prefill_rows_for(plan, off)) == single
     o, l = to_np(out, lse)
     assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
     rng = np.random.default_rng(1)
@@ -237,3 +287,30 @@ def test_prefill_long_prefix_max_chunks(dtype, D):
                   set(rng.integers(0, 2048, size=6).tolist()))
     ref = oracle_prefill_for(batch, plan, q, off, rows=rows)
     assert_close(o[rows], l[rows], *ref, dtype, f"long prefix {dtype} D={D}")
+
+
+@pytest.mark.parametrize("dtype,D", [("float16", 128), ("bfloat16", 64)])
+def test_prefill_single_pass_longest_ranges(dtype, D, monkeypatch):
+    """The single pass at its largest ranges: an 8192-token prefix (a
+    512-block table) and own prompts of up to 8192 tokens whose last 300 and
+    1000 tokens are rows; one group and one ungrouped request.  Sampled rows
+    against the oracle."""
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "1")
+    say("prefill single pass longest ranges", dtype, D)
+    rng = np.random.default_rng(11)
+    sl = [8192, 5000, 300, 8000]
+    plan = build_plan(heads=8, head_dim=D, block_size=16, dtype=dtype,
+                      group_of_request=[0, 0, 0, -1], prefix_lens=[8192], suffix_lens=sl,
+                      sm_scale=1.0 / math.sqrt(D), rng=rng)
+    qr = [1000, 300, 300, 1000]
+    batch = make_batch(plan, seed=12)
+    q, off = make_prefill_queries(plan, qr, seed=12)
+    keep = []
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off, keep=keep)
+    assert workspace_untouched(keep[0]), "the split path ran"
+    o, l = to_np(out, lse)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(l))
+    rows = sorted({0, 127, 128, 999, 1000, 1299, 1300, 1599, 1600, 2599} |
+                  set(rng.integers(0, int(off[-1]), size=6).tolist()))
+    ref = oracle_prefill_for(batch, plan, q, off, rows=rows)
+    assert_close(o[rows], l[rows], *ref, dtype, f"single pass longest {dtype} D={D}")
