@@ -25,6 +25,7 @@
 //     stages that need it.
 #pragma once
 
+#include <cfloat>
 #include <type_traits>
 
 #include "prefill_shape.h"
@@ -168,11 +169,14 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
   }
 
   // reference max of the exponentials, running sum of the probabilities, and
-  // of the probabilities as rounded for the PV products
+  // of the probabilities as rounded for the PV products.  Before a row's
+  // first visible key its reference is -FLT_MAX, finite: every finite logit
+  // moves it, and exp2(logit * scale - reference) needs no guard (a masked
+  // logit, -inf, gives 0)
   float mref[NS], lsum[NS], lsr[NS];
   f32x4 o[NS][DT16];
 #pragma unroll
-  for (int c = 0; c < NS; ++c) { mref[c] = -INFINITY; lsum[c] = 0.f; lsr[c] = 0.f; }
+  for (int c = 0; c < NS; ++c) { mref[c] = -FLT_MAX; lsum[c] = 0.f; lsr[c] = 0.f; }
 #pragma unroll
   for (int c = 0; c < NS; ++c)
 #pragma unroll
@@ -256,26 +260,24 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
         // The row's reference only has to move when some lane's own logits
         // exceed it by more than kLazy: that test needs no cross-lane max, and
         // the cross-lane max is taken only in the (rare) branch that moves it.
+        // (scale > 0: the scaled max of a masked lane stays -inf, no NaN)
         const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-        if (__builtin_amdgcn_ballot_w64(lm * scale > mref[c] + kLazy) != 0) {
-          const float bm = max_xor32(max_xor16(lm));
-          const float bms = bm == -INFINITY ? -INFINITY : bm * scale;
-          const float mn = fmaxf(mref[c], bms);
-          const float alpha = mn == -INFINITY ? 1.f : fast_exp2(mref[c] - mn);
+        if (__builtin_amdgcn_ballot_w64(__builtin_fmaf(lm, scale, -mref[c]) > kLazy) != 0) {
+          const float mn = fmaxf(mref[c], max_xor32(max_xor16(lm)) * scale);
+          const float alpha = fast_exp2(mref[c] - mn);      // 0 after -FLT_MAX, 1 if unmoved
           lsum[c] *= alpha;
           lsr[c] *= alpha;
 #pragma unroll
           for (int dt = 0; dt < DT16; ++dt) o[c][dt] *= alpha;
           mref[c] = mn;
         }
-        const float nm = mref[c] == -INFINITY ? 0.f : -mref[c];
         float p[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(x[i], scale, nm));   // masked: 0
+        for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(x[i], scale, -mref[c]));   // masked: 0
         lsum[c] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
         pk2[c][0] = Mfma<DT>::pack_p(p);
         pk2[c][1] = Mfma<DT>::pack_p(p + 4);
-        lsr[c] += add_packed<DT>(pk2[c][1], add_packed<DT>(pk2[c][0], 0.f));
+        lsr[c] = add_packed<DT>(pk2[c][1], add_packed<DT>(pk2[c][0], lsr[c]));
       }
       const char* vrow = vb + vt_row * ROW_B + vt_half;
 #pragma unroll

@@ -63,6 +63,14 @@ def prefill_case(kind, dtype, D, seed=0):
                           group_of_request=[0, 0], prefix_lens=[300], suffix_lens=[1000, 3],
                           sm_scale=scale, rng=rng)
         return plan, [1000, 3]
+    if kind == "many_runs":
+        # 160 requests of one group with one row each (at the last own token):
+        # the first row tile holds 128 requests' rows, one run per request
+        sl = [int(x) for x in rng.integers(1, 50, size=160)]
+        plan = build_plan(heads=2, head_dim=D, block_size=16, dtype=dtype,
+                          group_of_request=[0] * 160, prefix_lens=[300], suffix_lens=sl,
+                          sm_scale=scale, shuffle=True, rng=rng)
+        return plan, [1] * 160
     if kind == "single":
         plan = build_plan(heads=1, head_dim=D, block_size=16, dtype=dtype, group_of_request=[-1],
                           prefix_lens=[], suffix_lens=[1], sm_scale=scale, rng=rng)
@@ -90,7 +98,8 @@ def device_dict(batch, q, off):
 
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("kind", ["mixed", "wide_group", "nested", "long_rows", "single"])
+@pytest.mark.parametrize("kind", ["mixed", "wide_group", "nested", "long_rows", "many_runs",
+                                  "single"])
 def test_prefill_parity(kind, dtype, D):
     say("prefill", kind, dtype, D)
     plan, qr = prefill_case(kind, dtype, D)
@@ -103,7 +112,7 @@ def test_prefill_parity(kind, dtype, D):
 
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
-@pytest.mark.parametrize("kind", ["mixed", "wide_group", "long_rows", "single"])
+@pytest.mark.parametrize("kind", ["mixed", "wide_group", "long_rows", "many_runs", "single"])
 def test_prefill_single_pass_parity(kind, dtype, D, monkeypatch):
     """The single-pass path (each group tile sees the whole prefix, then its
     rows' own tokens run by run; ungrouped requests' tiles their own tokens)
