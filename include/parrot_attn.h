@@ -292,7 +292,8 @@ parrot_status parrot_validate_nested_inputs(
  * variable PARROT_PREFILL_SINGLE_PASS=0 forces the split plan; =1 takes the
  * single pass wherever the groups are flat, the caches 16-bit and the lengths
  * at most 8192 (even when the split plan would cut them into chunks to fill
- * the device).  Both plans give the same results to rounding.
+ * the device); other values leave the choice to the plan.  Both plans give
+ * the same results to rounding.
  *
  *   rows                 (host) row counts; see parrot_prefill_rows
  *   q                    [T][H][D] dtype, 16-byte aligned

@@ -385,10 +385,12 @@ struct PrefillPlan {
 // PARROT_PREFILL_SINGLE_PASS=0 turns it off; =1 takes it whenever the ranges
 // fit the tile's block table (8192 tokens), even where the split plan would
 // cut them into chunks to fill the device (for tests and tuning).
+// Any other value (or none) leaves the choice to the plan.
 int single_pass_setting() {
   const char* e = std::getenv("PARROT_PREFILL_SINGLE_PASS");
-  if (!e || !*e) return -1;
-  return e[0] == '0' ? 0 : 1;
+  if (e && e[0] == '0' && e[1] == 0) return 0;
+  if (e && e[0] == '1' && e[1] == 0) return 1;
+  return -1;
 }
 
 // Chunk of a key range of at most `len` tokens: the whole range up to 8192

@@ -3,7 +3,8 @@
 // causally, against its own tokens (Section 7: Fill with a parent context
 // fills only the new tokens on top of the parent's KV cache).
 //
-// The work splits the same way as decode, with many query rows per request:
+// Split plan: the work splits the same way as decode, with many query rows
+// per request:
 //
 //   prefix items (g, chunk c, head h, row tile qt): the rows of every request
 //     that reads g's prefix, stacked in request order, one tile of rows at a
@@ -17,14 +18,16 @@
 //
 // Tiles hold 128 rows on fp16 / bf16 caches (wide_tile) and 64 on fp32 caches
 // (decode's tile_core); both run QK^T and PV on MFMA over LDS-staged 16-token
-// blocks and write one partial result per (row, head, item); the decode merge kernel
-// then combines them per row, reading the row descriptors that the first
-// workgroups write.
+// blocks and write one partial result per (row, head, item); the decode merge
+// kernel then combines them per row, reading the row descriptors that the
+// first workgroups write.
 //
-// When the prefix and the own tokens each fit one chunk and the groups are
-// flat, one pass does it all (single-pass items, no partial results, no
-// merge): a group tile's rows see the prefix and then, run by run, their own
-// requests' tokens; ungrouped requests' tiles see only their own tokens.
+// Single pass (16-bit caches, flat groups, prefix and own tokens within one
+// chunk each; the host decides): no partial results and no merge.  A group
+// tile (g, head h, row tile qt) takes the same stacked rows as a prefix item,
+// sees the whole prefix and then, run by run, each of its requests' own
+// tokens up to its rows' positions, and writes the rows' output; tiles of
+// ungrouped requests see only their own tokens.
 //
 // Work items are placed per XCD (workgroup b runs on XCD b mod 8): XCD x takes
 // every item of heads x, x + 8, ..., one head after another, prefix items

@@ -1,5 +1,6 @@
 // The prefill query tile on MFMA (gfx950, fp16 / bf16 caches): 128 query rows
-// against one range of a paged key sequence.
+// against one range of a paged key sequence (a partial result per row), or
+// against a prefix and then each row's own tokens (the output itself).
 //
 // Decode's prefix tile (tile_core) gives each wave 16 queries: enough to make
 // a bandwidth-bound prefix stream cheap, but a prefill tile is bound by the

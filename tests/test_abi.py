@@ -235,6 +235,8 @@ def test_prefill_single_pass_choice(parrot_lib, monkeypatch):
     assert not B.parrot_prefill_single_pass(long_prefix, rows)
     assert not B.parrot_prefill_single_pass(prob, rows, nested=True)
     assert not B.parrot_prefill_single_pass(base_problem(dtype=0), few)
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "yes")                # not 0 or 1: the plan decides
+    assert not B.parrot_prefill_single_pass(prob, few)
     monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", "0")
     assert not B.parrot_prefill_single_pass(prob, rows)
     # the workspace bound does not depend on the plan
