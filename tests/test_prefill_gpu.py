@@ -323,3 +323,87 @@ def test_prefill_single_pass_longest_ranges(dtype, D, monkeypatch):
                   set(rng.integers(0, int(off[-1]), size=6).tolist()))
     ref = oracle_prefill_for(batch, plan, q, off, rows=rows)
     assert_close(o[rows], l[rows], *ref, dtype, f"single pass longest {dtype} D={D}")
+
+
+# ---------------------------------------------------------------- probes
+# The graded tolerances cannot see one key too many or too few in a long row
+# (its weight is about 1/N).  Two probes pin the visible keys of every row in
+# both plans: with q = 0 every visible key has weight exactly 1/N, so the lse
+# is ln N to fp32 rounding; a key made to dominate one row's logits (logit
+# 40) must become that row's output when the row sees it, and must not when
+# it lies after the row's position.
+
+PLANS = {"single": "1", "split": "0"}
+
+
+def _prefix_len(plan, r):
+    g = int(plan.group_ids[r])
+    return int(plan.prefix_lens[g]) if g >= 0 else 0
+
+
+@pytest.mark.parametrize("dtype", ["float16", "bfloat16"])
+@pytest.mark.parametrize("path", ["single", "split"])
+def test_prefill_zero_query_probe(path, dtype, monkeypatch):
+    from oracle.attention import prefill_positions
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", PLANS[path])
+    for kind in ("mixed", "wide_group", "long_rows"):
+        say("prefill zero-query probe", path, dtype, kind)
+        plan, qr = prefill_case(kind, dtype, 128)
+        batch = make_batch(plan, seed=5)
+        q, off = make_prefill_queries(plan, qr, seed=5)
+        q.zero_()
+        keep = []
+        out, lse = run_prefill(plan, device_dict(batch, q, off), off, keep=keep)
+        assert workspace_untouched(keep[0]) == (path == "single"), "unexpected prefill path"
+        ref_o, ref_l = oracle_prefill_for(batch, plan, q, off)
+        n = np.array([_prefix_len(plan, r) + p + 1 for r, p in prefill_positions(off, plan.suffix_lens)])
+        assert np.allclose(ref_l, np.log(n)[:, None], rtol=1e-12, atol=1e-15)
+        o, l = to_np(out, lse)
+        assert np.max(np.abs(l - ref_l) / np.maximum(1.0, np.abs(ref_l))) < 1e-6, kind
+        # the output is the mean of the visible values, exact in fp32 up to a
+        # few ulps; its rounding to the cache type (half an ulp) dominates, and
+        # rows with one or two keys have means of any size: a relative bound
+        half_ulp = 2.0 ** -8 if dtype == "bfloat16" else 2.0 ** -11
+        bound = half_ulp * np.maximum(np.abs(ref_o), 2.0 ** -6) + 1e-5
+        assert np.all(np.abs(o - ref_o) <= bound), kind
+
+
+@pytest.mark.parametrize("path", ["single", "split"])
+def test_prefill_spike_probe(path, monkeypatch):
+    from oracle.attention import prefill_positions
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", PLANS[path])
+    dtype, B = "float16", 16
+    plan, qr = prefill_case("wide_group", dtype, 128)
+    base = make_batch(plan, seed=4)
+    q, off = make_prefill_queries(plan, qr, seed=4)
+    pos = prefill_positions(off, plan.suffix_lens)
+    T = int(off[-1])
+    firsts = [int(off[r]) for r in range(plan.num_requests) if off[r + 1] > off[r]]
+    rows = sorted({0, 127, 128, T - 1, firsts[len(firsts) // 2]})
+    for t in rows:
+        r, p = pos[t]
+        g, P, S = int(plan.group_ids[r]), _prefix_len(plan, r), int(plan.suffix_lens[r])
+        for j in sorted({0, 15, 16, P - 1, P, P + p - 1, P + p, P + p + 1}):
+            if not 0 <= j < P + S:
+                continue
+            say("prefill spike probe", path, "row", t, "key", j)
+            k = base.k_pool.clone()
+            if j < P:
+                blk, slot = int(plan.prefix_tables[g][j // B]), j % B
+            else:
+                blk, slot = int(plan.suffix_tables[r][(j - P) // B]), (j - P) % B
+            for h in range(plan.heads):
+                qv = q[t, h].double()
+                k[blk, h, slot] = (40.0 / (plan.sm_scale * float(qv @ qv)) * qv).to(k.dtype)
+            batch = type(base)(plan=plan, q=base.q, k_pool=k, v_pool=base.v_pool)
+            out, lse = run_prefill(plan, device_dict(batch, q, off), off)
+            o, l = to_np(out, lse)
+            v = base.v_pool[blk, :, slot].double().numpy()
+            if j <= P + p:                               # visible: the key takes over
+                s = plan.sm_scale * (q[t].double() * k[blk, :, slot].double()).sum(-1).numpy()
+                assert np.max(np.abs(o[t] - v)) <= 1e-3 * max(1.0, np.abs(v).max()), (t, j)
+                assert np.max(np.abs(l[t] - s) / np.abs(s)) < 1e-5, (t, j)
+            else:                                        # after the row: no effect on it
+                ref_o, ref_l = oracle_prefill_for(batch, plan, q, off, rows=[t])
+                assert_close(o[[t]], l[[t]], ref_o, ref_l, dtype, f"spike after row {t}")
+                assert np.max(np.abs(o[t] - v)) > 0.1, (t, j)
