@@ -101,9 +101,11 @@ typedef struct {
  * stream.  Attaching events still costs a few microseconds of stream time per
  * kernel, so time throughput on calls without them. */
 typedef struct {
-  void* partials_start;  /* the partial-result kernel (split-KV + prefix-group roles) */
+  void* partials_start;  /* the partial-result kernel (split-KV + prefix-group roles;
+                            for prefill, the prefill kernel) */
   void* partials_stop;
-  void* merge_start;     /* the log-sum-exp merge kernel */
+  void* merge_start;     /* the log-sum-exp merge kernel (a prefill call on the single
+                            pass has none: both events are recorded back to back) */
   void* merge_stop;
 } parrot_trace;
 
