@@ -95,11 +95,21 @@ int num_cus() {
 //  * CUs < n(1024) <= 2 CUs: c = 512, so that the workgroups that start late
 //    (once the own-token stream drains) are short;
 //  * otherwise c = 1024 (many rounds anyway; fewest partial results).
+// The smallest chunk is 256 tokens, unless the own-token stream is too short to
+// cover a 256-token chunk: a chunk costs about one memory round trip (taken as
+// 1.5 us) per 32-token stage, and the stream about its bytes at 5 TB/s, so the
+// chunk then shrinks to the stages the stream covers (down to one stage: 32
+// tokens).  Measured: a 4-request, 128-token fp32 group (own tokens ~100)
+// 16.3 -> 10.7 us per call; the benchmark workloads keep their chunks.
 int prefix_chunk(const parrot_problem* p, int qtiles) {
   if (p->num_groups <= 0) return kPrefixChunk;
   const double work = (double)p->max_prefix_len * p->num_groups * p->num_heads * qtiles;
   const double cus = num_cus();
+  const double elt = p->dtype == PARROT_DTYPE_F32 ? 4.0 : 2.0;
+  const double own_bytes = (double)p->num_requests * p->max_suffix_len * 2.0 * p->num_heads * p->head_dim * elt;
+  const double stream_stages = own_bytes / 5e12 / 1.5e-6;
   int cp = kPrefixChunk;
+  while (cp > 32 && cp / 32 > stream_stages) cp /= 2;
   if (work / kPrefixChunkMax <= cus) {
     while (cp < kPrefixChunkMax && work / cp > cus) cp *= 2;
   } else if (work / kPrefixChunkMax <= 2 * cus) {
