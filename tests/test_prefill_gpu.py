@@ -407,3 +407,18 @@ def test_prefill_spike_probe(path, monkeypatch):
                 ref_o, ref_l = oracle_prefill_for(batch, plan, q, off, rows=[t])
                 assert_close(o[[t]], l[[t]], ref_o, ref_l, dtype, f"spike after row {t}")
                 assert np.max(np.abs(o[t] - v)) > 0.1, (t, j)
+
+
+@pytest.mark.parametrize("path", ["single", "split"])
+def test_prefill_bitwise_reproducible(path, monkeypatch):
+    """The same inputs and plan give bitwise-identical output and lse (no
+    atomics or order-dependent sums in either plan)."""
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", PLANS[path])
+    say("prefill reproducibility", path)
+    plan, qr = prefill_case("mixed", "bfloat16", 128)
+    batch = make_batch(plan, seed=8)
+    q, off = make_prefill_queries(plan, qr, seed=8)
+    dev = device_dict(batch, q, off)
+    a = [t.clone() for t in run_prefill(plan, dev, off)]
+    b = run_prefill(plan, dev, off)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
