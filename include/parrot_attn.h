@@ -113,8 +113,10 @@ typedef struct {
  * (0 when R = 0).  The prefix chunk, and with it the workspace size, depends
  * on the compute-unit count of the current HIP device, so ask with the device
  * current that the calls will run on (a call with a smaller workspace fails
- * with PARROT_ERR_WORKSPACE_TOO_SMALL).  Returns (size_t)-1 if `p` is invalid;
- * the reason is then in parrot_last_error(). */
+ * with PARROT_ERR_WORKSPACE_TOO_SMALL).  The size never decreases when
+ * num_requests or max_suffix_len grow, so a workspace sized for the largest
+ * batch serves every smaller one with the other fields unchanged.  Returns
+ * (size_t)-1 if `p` is invalid; the reason is then in parrot_last_error(). */
 size_t parrot_workspace_bytes(const parrot_problem* p);
 
 /*

@@ -101,13 +101,16 @@ int num_cus() {
 // chunk then shrinks to the stages the stream covers (down to one stage: 32
 // tokens).  Measured: a 4-request, 128-token fp32 group (own tokens ~100)
 // 16.3 -> 10.7 us per call; the benchmark workloads keep their chunks.
-int prefix_chunk(const parrot_problem* p, int qtiles) {
+// `any_stream`: the chunk for the shortest own-token stream (the smallest the
+// rule can give for these prefix sizes), which sizes the workspace so that it
+// does not shrink when requests or own tokens are added.
+int prefix_chunk(const parrot_problem* p, int qtiles, bool any_stream = false) {
   if (p->num_groups <= 0) return kPrefixChunk;
   const double work = (double)p->max_prefix_len * p->num_groups * p->num_heads * qtiles;
   const double cus = num_cus();
   const double elt = p->dtype == PARROT_DTYPE_F32 ? 4.0 : 2.0;
   const double own_bytes = (double)p->num_requests * p->max_suffix_len * 2.0 * p->num_heads * p->head_dim * elt;
-  const double stream_stages = own_bytes / 5e12 / 1.5e-6;
+  const double stream_stages = any_stream ? 0.0 : own_bytes / 5e12 / 1.5e-6;
   int cp = kPrefixChunk;
   while (cp > 32 && cp / 32 > stream_stages) cp /= 2;
   if (work / kPrefixChunkMax <= cus) {
@@ -179,13 +182,18 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   const long seg = std::max<long>(pl->seg_pre + pieces_shared, pieces_naive);
   pl->seg = (int)seg;
   pl->skv_waves = 0;   // set at launch from the device's CU count
+  // the workspace holds the slots of the smallest prefix chunk any own-token
+  // stream could select (at least this call's): its size never drops when
+  // num_requests or max_suffix_len grow
+  const long seg_p_ws = p->num_groups > 0 ? ceil_div(p->max_prefix_len, prefix_chunk(p, pl->prefix_qtiles, true)) : 0;
+  const long seg_ws = std::max<long>(std::max<long>(pl->depth * seg_p_ws + pieces_shared, pieces_naive), seg);
 
-  const double slots = (double)p->num_requests * p->num_heads * seg;
+  const double slots = (double)p->num_requests * p->num_heads * seg_ws;
   const double flat = (double)p->num_requests * (double)(nbp_max + nbs_max);
   const double grid_b = (double)p->num_groups * pl->seg_p * p->num_heads * pl->prefix_qtiles;
   if (flat > 2e9 || grid_b > 2e9 || slots * p->head_dim * 4.0 > 9e18)
     return fail(PARROT_ERR_UNSUPPORTED, "problem too large for one launch (%.3g blocks)", flat);
-  const size_t n_slots = (size_t)p->num_requests * p->num_heads * seg;
+  const size_t n_slots = (size_t)p->num_requests * p->num_heads * seg_ws;
   auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
   pl->lse_bytes = align256(n_slots * sizeof(float));

@@ -66,6 +66,31 @@ def test_workspace_sizes(parrot_lib):
     assert B.parrot_workspace_bytes(base_problem(head_dim=64)) < w0
 
 
+@pytest.mark.parametrize("base", [
+    dict(num_requests=4, num_heads=4, head_dim=64, dtype=0, max_group_size=4, max_prefix_len=128,
+         prefix_table_stride=8, max_suffix_len=32, suffix_table_stride=2),     # tiny: small chunks
+    dict(num_requests=4, num_heads=1, head_dim=64, dtype=0, max_group_size=4, max_prefix_len=1024,
+         prefix_table_stride=64, max_suffix_len=32, suffix_table_stride=2),     # many small chunks
+    dict(),                                                                      # LLaMA-7B, 1 x 32
+])
+def test_workspace_monotone_in_batch(parrot_lib, base):
+    """A workspace sized for the largest batch serves every smaller one: the
+    size never drops as requests or own tokens are added (the prefix chunk,
+    which can grow with the own-token stream, does not shrink the slots)."""
+    prev = 0
+    g = base.get("max_group_size", 32)                   # requests >= the largest group
+    for R in (g, g + 1, g + 3, 2 * g, 4 * g, 8 * g, 16 * g):
+        w = B.parrot_workspace_bytes(base_problem(**dict(base, num_requests=R)))
+        assert w >= prev, R
+        prev = w
+    prev = 0
+    for S in (1, 2, 16, 32, 64, 100, 256, 512, 1024, 4096, 8192, 16384):
+        w = B.parrot_workspace_bytes(base_problem(**dict(base, max_suffix_len=S,
+                                                         suffix_table_stride=-(-S // 16))))
+        assert w >= prev, S
+        prev = w
+
+
 @pytest.mark.parametrize("over,status,msg", [
     (dict(head_dim=96), B.PARROT_ERR_UNSUPPORTED, "head_dim"),
     (dict(block_size=32), B.PARROT_ERR_UNSUPPORTED, "block_size"),
