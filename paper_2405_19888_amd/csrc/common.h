@@ -159,22 +159,12 @@ PARROT_DEV float group_sum(float x) {
   return x;
 }
 
-// Workgroup barrier that orders LDS traffic only.  __syncthreads() is a
-// release/acquire fence on all address spaces, and on gfx9 loads and stores
-// share one counter, so it would wait for every global load still in flight
-// (register prefetches included).  Fencing only the local address space keeps
-// those loads in flight across the barrier.
-PARROT_DEV void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // Workgroup barrier for kernels that manage their own memory counters: this
 // wave's LDS operations complete (lgkmcnt 0), then s_barrier.  No hardware
 // fence and no wait on vector-memory loads, so direct-to-LDS loads issued
-// earlier stay in flight; the empty asm statements keep the compiler from
-// moving memory accesses across the barrier.
+// earlier stay in flight (a __syncthreads() would wait for every global load
+// still in flight: on gfx9 loads and stores share one counter); the empty asm
+// statements keep the compiler from moving memory accesses across the barrier.
 PARROT_DEV void lds_sync() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt untouched
