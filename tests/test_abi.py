@@ -31,6 +31,33 @@ def test_exports_every_declared_symbol(parrot_lib):
         assert hasattr(parrot_lib, n), f"{n} not exported"
 
 
+def declared_arities():
+    """Parameter count of every function declared in include/*.h."""
+    out = {}
+    for h in sorted(os.listdir(INCLUDE)):
+        if not h.endswith(".h"):
+            continue
+        text = open(os.path.join(INCLUDE, h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"\b(parrot_\w+)\s*\(([^;{]*?)\)\s*;", text):
+            params = " ".join(m.group(2).split())
+            out[m.group(1)] = 0 if params in ("", "void") else params.count(",") + 1
+    return out
+
+
+def test_binding_matches_header_arity(parrot_lib):
+    """Every function of the C header is bound with as many arguments as it
+    declares (argument lists drift silently through ctypes otherwise)."""
+    from paper_2405_19888_amd import context
+    context._lib()                       # binds the context-store functions
+    arity = declared_arities()
+    assert set(arity) == set(declared_functions()), "declarations the parser missed"
+    for name, n in arity.items():
+        f = getattr(parrot_lib, name)
+        assert f.argtypes is not None, f"{name} has no argtypes"
+        assert len(f.argtypes) == n, f"{name}: header {n} arguments, binding {len(f.argtypes)}"
+
+
 def test_abi_version(parrot_lib):
     assert B.parrot_abi_version() == 4
 
