@@ -29,4 +29,6 @@ from .binding import (  # noqa: F401
     parrot_workspace_bytes,
     prefill_rows_from_host,
     problem_from_host,
+    shared_prefix_decode,
+    shared_prefix_prefill,
 )

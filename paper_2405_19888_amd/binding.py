@@ -458,3 +458,58 @@ class Prefiller:
     def __call__(self, t: dict, stream=None, trace=None, nested: bool = False):
         self.bind(t, stream=stream, nested=nested)(trace)
         return self.out, self.lse
+
+
+def _sizes_from_tensors(q, prefix_k, suffix_k, prefix_tables, suffix_tables, group_ids,
+                        prefix_lens, suffix_lens, sm_scale, prefix_parents):
+    """ParrotProblem of a call given as torch tensors (one device-to-host copy
+    of the group ids and lengths, for the maxima and group sizes)."""
+    return problem_from_host(
+        num_heads=q.shape[-2], head_dim=q.shape[-1], block_size=suffix_k.shape[2],
+        dtype=q.dtype, sm_scale=sm_scale, group_ids=group_ids.cpu().numpy(),
+        prefix_lens=prefix_lens.cpu().numpy(), suffix_lens=suffix_lens.cpu().numpy(),
+        prefix_table_stride=prefix_tables.shape[1] if prefix_tables.dim() == 2 else 0,
+        suffix_table_stride=suffix_tables.shape[1],
+        num_prefix_blocks=prefix_k.shape[0], num_suffix_blocks=suffix_k.shape[0],
+        prefix_parents=None if prefix_parents is None else prefix_parents.cpu().numpy())
+
+
+def shared_prefix_decode(q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_tables, prefix_lens,
+                         suffix_tables, suffix_lens, group_ids, *, sm_scale, prefix_parents=None,
+                         per_request=False, stream=None):
+    """One decode call on torch tensors laid out as the C entry points take
+    them (q [R, H, D]; pools [blocks, H, 16, D]; int32 tables, lengths, group
+    ids and, for nested groups, parents).  Sizes the problem from host copies
+    of the group ids and lengths, allocates out, lse and the workspace, and
+    runs on ``stream`` (default: the current stream).  Returns (out, lse).
+    ``per_request`` runs the baseline that reads each request's prefix itself.
+    Engines that know the maxima on the host should build a ParrotProblem and
+    reuse a Decoder instead (no copy, no allocation per call)."""
+    prob = _sizes_from_tensors(q, prefix_k, suffix_k, prefix_tables, suffix_tables, group_ids,
+                               prefix_lens, suffix_lens, sm_scale, prefix_parents)
+    dec = Decoder(prob, device=q.device)
+    t = dict(q=q, prefix_k=prefix_k, prefix_v=prefix_v, suffix_k=suffix_k, suffix_v=suffix_v,
+             prefix_tables=prefix_tables, prefix_lens=prefix_lens, suffix_tables=suffix_tables,
+             suffix_lens=suffix_lens, group_ids=group_ids, prefix_parents=prefix_parents)
+    return dec(t, shared=not per_request, stream=stream, nested=prefix_parents is not None)
+
+
+def shared_prefix_prefill(q_rows, query_offsets, prefix_k, prefix_v, suffix_k, suffix_v,
+                          prefix_tables, prefix_lens, suffix_tables, suffix_lens, group_ids, *,
+                          sm_scale, prefix_parents=None, stream=None):
+    """One prefill call on torch tensors: rows [query_offsets[r],
+    query_offsets[r+1]) of q_rows [T, H, D] are request r's last own tokens.
+    Sizes the problem and the row counts from host copies of the int arrays,
+    allocates out, lse and the workspace, and runs on ``stream``.  Returns
+    (out, lse)."""
+    prob = _sizes_from_tensors(q_rows, prefix_k, suffix_k, prefix_tables, suffix_tables, group_ids,
+                               prefix_lens, suffix_lens, sm_scale, prefix_parents)
+    rows = prefill_rows_from_host(query_offsets.cpu().numpy(), group_ids.cpu().numpy(),
+                                  prob.num_groups,
+                                  None if prefix_parents is None else prefix_parents.cpu().numpy())
+    pre = Prefiller(prob, rows, device=q_rows.device)
+    t = dict(q_rows=q_rows, query_offsets=query_offsets, prefix_k=prefix_k, prefix_v=prefix_v,
+             suffix_k=suffix_k, suffix_v=suffix_v, prefix_tables=prefix_tables,
+             prefix_lens=prefix_lens, suffix_tables=suffix_tables, suffix_lens=suffix_lens,
+             group_ids=group_ids, prefix_parents=prefix_parents)
+    return pre(t, stream=stream, nested=prefix_parents is not None)

@@ -307,3 +307,21 @@ def test_trace_events_time_each_kernel():
     times = [evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(2)]
     assert all(t > 0 for t in times), times
     assert evs[1].elapsed_time(evs[2]) >= 0        # the merge runs after the partials
+
+
+@pytest.mark.parametrize("per_request", [False, True])
+def test_one_call_torch_api(per_request):
+    """shared_prefix_decode on plain torch tensors sizes the problem itself and
+    matches the oracle (flat groups, ungrouped requests, separate pools)."""
+    from paper_2405_19888_amd import shared_prefix_decode
+    say("one-call torch API, per_request =", per_request)
+    plan = edge_plan("boundaries", "float16", 128)
+    batch = make_batch(plan, seed=2)
+    dev = batch.to("cuda")
+    out, lse = shared_prefix_decode(
+        dev["q"], dev["k_pool"], dev["v_pool"], dev["k_pool"], dev["v_pool"], dev["prefix_tables"],
+        dev["prefix_lens"], dev["suffix_tables"], dev["suffix_lens"], dev["group_ids"],
+        sm_scale=plan.sm_scale, per_request=per_request)
+    torch.cuda.synchronize()
+    ref = oracle_for(batch, plan)
+    assert_close(*to_np(out, lse), *ref, "float16", f"one-call per_request={per_request}")

@@ -422,3 +422,21 @@ def test_prefill_bitwise_reproducible(path, monkeypatch):
     a = [t.clone() for t in run_prefill(plan, dev, off)]
     b = run_prefill(plan, dev, off)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_prefill_one_call_torch_api():
+    """shared_prefix_prefill on plain torch tensors sizes the problem and the
+    row counts itself and matches the oracle."""
+    from paper_2405_19888_amd import shared_prefix_prefill
+    say("prefill one-call torch API")
+    plan, qr = prefill_case("mixed", "bfloat16", 64)
+    batch = make_batch(plan, seed=9)
+    q, off = make_prefill_queries(plan, qr, seed=9)
+    dev = device_dict(batch, q, off)
+    out, lse = shared_prefix_prefill(
+        dev["q_rows"], dev["query_offsets"], dev["k_pool"], dev["v_pool"], dev["k_pool"],
+        dev["v_pool"], dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
+        dev["suffix_lens"], dev["group_ids"], sm_scale=plan.sm_scale)
+    torch.cuda.synchronize()
+    ref = oracle_prefill_for(batch, plan, q, off)
+    assert_close(*to_np(out, lse), *ref, "bfloat16", "prefill one-call")
