@@ -30,10 +30,11 @@
 // ungrouped requests see only their own tokens.
 //
 // Work items are placed per XCD (workgroup b runs on XCD b mod 8): XCD x takes
-// every item of heads x, x + 8, ..., one head after another, prefix items
-// before own items and row tiles fastest.  Each XCD then holds the same share
-// of the work, and the workgroups that run together on it read the same head's
-// key chunk, which stays in that XCD's L2.
+// every item of heads x, x + 8, ..., one head after another (split plan: a
+// head's own items after the next head's prefix items), prefix items before
+// own items and row tiles fastest.  Each XCD then holds the same share of the
+// work, and the workgroups that run together on it read the same head's key
+// chunk, which stays in that XCD's L2.
 #include "prefill_args.h"
 #include "prefill_tile.h"
 
@@ -333,22 +334,41 @@ void k_prefill(PrefillArgs a) {
     const int t = bid * 256 + (int)threadIdx.x;
     if (t < a.T) write_row_meta(a, t);
   }
-  // XCD x, its l-th workgroup: head x + 8 (l / per), item l % per of that head
+  // XCD x takes heads x, x + 8, ... (J of them); l is its workgroup index
   const int x = bid % kXcds, l = bid / kXcds;
-  const int per = a.n_pre + a.n_own;                   // items per head
-  const int j = l / per, item = l % per;
-  const int h = x + kXcds * j;
-  if (h >= a.H) return;
   if constexpr (SINGLE) {
+    // head after head: head x + 8 (l / per), item l % per of that head
+    const int per = a.n_pre + a.n_own;                 // items per head
+    const int j = l / per, item = l % per;
+    const int h = x + kXcds * j;
+    if (h >= a.H) return;
     if (item < a.n_pre)
       prefill_single_group_item<DT, D>(a, lds, h, item);
     else
       prefill_single_own_item<DT, D>(a, lds, h, item - a.n_pre);
   } else {
-    if (item < a.n_pre)
-      prefill_prefix_item<DT, D>(a, lds, h, item);
+    // prefix items of head 0, then of head 1 with the own items of head 0,
+    // and so on: the own-token streams (bandwidth-bound) of one head run
+    // beside the prefix tiles (MFMA-bound) of the next, and each head's
+    // prefix items still run together (its prefix chunk stays in the L2)
+    const int J = (a.H - x + kXcds - 1) / kXcds;
+    int rem = l, j = -1, own = 0;
+    for (int k = 0; k <= J; ++k) {
+      if (k < J) {
+        if (rem < a.n_pre) { j = k; break; }
+        rem -= a.n_pre;
+      }
+      if (k >= 1) {
+        if (rem < a.n_own) { j = k - 1; own = 1; break; }
+        rem -= a.n_own;
+      }
+    }
+    if (j < 0) return;
+    const int h = x + kXcds * j;
+    if (own)
+      prefill_own_item<DT, D>(a, lds, h, rem);
     else
-      prefill_own_item<DT, D>(a, lds, h, item - a.n_pre);
+      prefill_prefix_item<DT, D>(a, lds, h, rem);
   }
 }
 
