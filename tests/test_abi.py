@@ -160,15 +160,20 @@ def call(lib, prob, fn="parrot_shared_prefix_decode", **ptrs):
     return getattr(lib, fn)(ctypes.byref(prob), *[vals[n] for n in names], ws_bytes, None, None)
 
 
-@pytest.mark.parametrize("fn", ["parrot_shared_prefix_decode", "parrot_per_request_decode",
-                                "parrot_nested_prefix_decode", "parrot_shared_prefix_decode_append"])
-@pytest.mark.parametrize("field", ["q", "sk", "sv", "stab", "slen", "gid", "out", "lse", "ws",
-                                   "pk", "pv", "ptab", "plen", "parents", "k_new", "v_new"])
+_COMMON_FIELDS = ["q", "sk", "sv", "stab", "slen", "gid", "out", "lse", "ws", "pk", "pv", "ptab",
+                  "plen"]
+_NULL_CASES = [(fn, f) for fn in ("parrot_shared_prefix_decode", "parrot_per_request_decode",
+                                  "parrot_nested_prefix_decode",
+                                  "parrot_shared_prefix_decode_append")
+               for f in _COMMON_FIELDS] + \
+    [("parrot_nested_prefix_decode", "parents"), ("parrot_shared_prefix_decode_append", "k_new"),
+     ("parrot_shared_prefix_decode_append", "v_new")]
+
+
+@pytest.mark.parametrize("fn,field", _NULL_CASES)
 def test_null_pointer_rejected(parrot_lib, fn, field):
-    if field == "parents" and fn != "parrot_nested_prefix_decode":
-        pytest.skip("only the nested entry point takes prefix_parents")
-    if field in ("k_new", "v_new") and fn != "parrot_shared_prefix_decode_append":
-        pytest.skip("only the appending entry point takes k_new / v_new")
+    """Every pointer argument an entry point takes (prefix_parents only the
+    nested one, k_new / v_new only the appending one) is checked for NULL."""
     st = call(parrot_lib, base_problem(max_prefix_depth=2), fn, **{field: None})
     assert st == B.PARROT_ERR_INVALID_ARGUMENT
     assert "NULL" in B.parrot_last_error()
