@@ -241,7 +241,9 @@ parrot_status parrot_nested_prefix_decode(
  * Checks the device-side contents against `p` (a debugging aid; it
  * synchronises `stream`): group ids in [-1, NG), prefix lengths in
  * [1, max_prefix_len], suffix lengths in [0, max_suffix_len], P + S >= 1,
- * and every block id a length reaches in [0, pool size).  Returns
+ * every block id a length reaches in [0, pool size), and no group's prefix
+ * read by more than max_group_size requests (the decode launch sizes its
+ * prefix query tiles from that bound).  Returns
  * PARROT_ERR_INVALID_ARGUMENT with a message naming the first bad entry.
  * `scratch` is >= 64 bytes of device memory, 4-byte aligned.
  */

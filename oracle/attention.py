@@ -40,7 +40,6 @@ All inputs are upcast exactly to float64 before any arithmetic.
 """
 from __future__ import annotations
 
-import math
 from typing import Iterable, Optional, Sequence
 
 import numpy as np
@@ -241,8 +240,3 @@ def shared_prefix_prefill(q, query_offsets, prefix_k, prefix_v, suffix_k, suffix
         out[i], lse[i] = attend(qf[t], K[:n], V[:n], sm_scale)
     return out, lse
 
-
-def lse_natural(values: Sequence[float]) -> float:
-    """ln sum exp(values) for a short Python list (used by worked examples)."""
-    m = max(values)
-    return m + math.log(sum(math.exp(v - m) for v in values))

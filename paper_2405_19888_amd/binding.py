@@ -98,32 +98,27 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = dec_args
         f.restype = ctypes.c_int
-    if hasattr(lib, "parrot_shared_prefix_decode_append"):   # absent from ABI 1 builds
-        lib.parrot_shared_prefix_decode_append.argtypes = dec_args[:2] + [vp, vp] + dec_args[2:]
-        lib.parrot_shared_prefix_decode_append.restype = ctypes.c_int
-    if hasattr(lib, "parrot_nested_prefix_decode"):      # absent from ABI 1 builds
-        lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
-        lib.parrot_nested_prefix_decode.restype = ctypes.c_int
+    lib.parrot_shared_prefix_decode_append.argtypes = dec_args[:2] + [vp, vp] + dec_args[2:]
+    lib.parrot_shared_prefix_decode_append.restype = ctypes.c_int
+    lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
+    lib.parrot_nested_prefix_decode.restype = ctypes.c_int
     lib.parrot_validate_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, vp, vp]
     lib.parrot_validate_inputs.restype = ctypes.c_int
-    if hasattr(lib, "parrot_validate_nested_inputs"):
-        lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p,
-                                                      vp, vp]
-        lib.parrot_validate_nested_inputs.restype = ctypes.c_int
+    lib.parrot_validate_nested_inputs.argtypes = [prob_p, i32p, i32p, i32p, i32p, i32p, i32p,
+                                                  vp, vp]
+    lib.parrot_validate_nested_inputs.restype = ctypes.c_int
     rows_p = ctypes.POINTER(ParrotPrefillRows)
-    if hasattr(lib, "parrot_shared_prefix_prefill"):     # absent from ABI 1-2 builds
-        lib.parrot_prefill_workspace_bytes.argtypes = [prob_p, rows_p]
-        lib.parrot_prefill_workspace_bytes.restype = sz
-        lib.parrot_shared_prefix_prefill.argtypes = [
-            prob_p, rows_p, vp, i32p, vp, vp, vp, vp, i32p, i32p, i32p, i32p, i32p, i32p, vp, vp,
-            vp, sz, vp, ctypes.POINTER(ParrotTrace)]
-        lib.parrot_shared_prefix_prefill.restype = ctypes.c_int
-        lib.parrot_validate_prefill_inputs.argtypes = [prob_p, rows_p, i32p, i32p, i32p, i32p,
-                                                       i32p, i32p, i32p, vp, vp]
-        lib.parrot_validate_prefill_inputs.restype = ctypes.c_int
-    if hasattr(lib, "parrot_prefill_single_pass"):       # absent from ABI 1-3 builds
-        lib.parrot_prefill_single_pass.argtypes = [prob_p, rows_p, ctypes.c_int]
-        lib.parrot_prefill_single_pass.restype = ctypes.c_int
+    lib.parrot_prefill_workspace_bytes.argtypes = [prob_p, rows_p]
+    lib.parrot_prefill_workspace_bytes.restype = sz
+    lib.parrot_shared_prefix_prefill.argtypes = [
+        prob_p, rows_p, vp, i32p, vp, vp, vp, vp, i32p, i32p, i32p, i32p, i32p, i32p, vp, vp,
+        vp, sz, vp, ctypes.POINTER(ParrotTrace)]
+    lib.parrot_shared_prefix_prefill.restype = ctypes.c_int
+    lib.parrot_validate_prefill_inputs.argtypes = [prob_p, rows_p, i32p, i32p, i32p, i32p,
+                                                   i32p, i32p, i32p, vp, vp]
+    lib.parrot_validate_prefill_inputs.restype = ctypes.c_int
+    lib.parrot_prefill_single_pass.argtypes = [prob_p, rows_p, ctypes.c_int]
+    lib.parrot_prefill_single_pass.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []

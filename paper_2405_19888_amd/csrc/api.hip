@@ -84,6 +84,14 @@ int num_cus() {
   return v;
 }
 
+// Split-KV workgroups of a decode launch: a fixed number per CU, and at least
+// one wave per head.
+long splitkv_workgroups(int heads) {
+  long n = (long)num_cus() * kSplitkvWgsPerCu;
+  if (n * parrot::kSkvWaves < heads) n = ceil_div(heads, parrot::kSkvWaves);
+  return n;
+}
+
 // Prefix chunk length.  One prefix-group workgroup streams one chunk of one
 // head for up to 64 members, about two 16 KiB stages in flight, so its run time
 // grows with the chunk; every chunk also costs each member one partial result
@@ -168,11 +176,15 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   pl->skv_min_q = kSplitkvMinBlocks;
   // slots: shared path = prefix chunks + split-KV pieces of the own tokens;
   // per-request path = split-KV pieces of prefix + own tokens.  One stride
-  // serves both.
+  // serves both.  A sequence of n block columns touches at most
+  // ceil(n / min_q) + 1 runs of the flat column list, and never more than the
+  // G column groups the role has (its piece index is its group minus the
+  // group of its first column).
   const long nbp_max = p->num_groups > 0 ? ceil_div(p->max_prefix_len, B) : 0;
   const long nbs_max = ceil_div(p->max_suffix_len, B);
-  const long pieces_shared = nbs_max > 0 ? ceil_div(nbs_max, pl->skv_min_q) + 1 : 0;
-  const long pieces_naive = ceil_div(nbp_max + nbs_max, pl->skv_min_q) + 1;
+  const long groups = splitkv_workgroups(p->num_heads) * parrot::kSkvWaves / p->num_heads;
+  const long pieces_shared = nbs_max > 0 ? std::min(ceil_div(nbs_max, pl->skv_min_q) + 1, groups) : 0;
+  const long pieces_naive = std::min(ceil_div(nbp_max + nbs_max, pl->skv_min_q) + 1, groups);
   pl->seg_p = p->num_groups > 0 ? (int)ceil_div(p->max_prefix_len, pl->cp) : 0;
   if (pl->seg_p > 0xFFFF)
     return fail(PARROT_ERR_UNSUPPORTED, "max_prefix_len %d needs %d prefix chunks (at most 65535)",
@@ -287,9 +299,8 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.seg = pl.seg; a.seg_pre = shared ? pl.seg_pre : 0; a.cp = pl.cp;
     a.with_prefix = shared ? 0 : 1;
     // a fixed grid of split-KV workgroups per CU, at least one wave per head
-    pa.n_skv = num_cus() * kSplitkvWgsPerCu;
-    if (pa.n_skv * 4 < a.H) pa.n_skv = (int)ceil_div(a.H, 4);
-    a.nwaves = pa.n_skv * 4;
+    pa.n_skv = (int)splitkv_workgroups(a.H);
+    a.nwaves = pa.n_skv * parrot::kSkvWaves;
     a.min_q = pl.skv_min_q;
     a.scale_log2 = scale_log2;
     if (run_prefix) {
@@ -644,6 +655,8 @@ parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tabl
   if (rows) {
     a.qoff = query_offsets; a.T = rows->num_query_rows;
     a.max_q = rows->max_query_rows; a.max_grp = rows->max_group_rows;
+  } else {
+    a.max_grp = p->max_group_size;
   }
   PARROT_TRY(launched(parrot::launch_validate(a, s), "validation kernel"));
   int32_t res[3] = {0, 0, 0};
@@ -658,10 +671,12 @@ parrot_status validate(const parrot_problem* p, const int32_t* prefix_block_tabl
                                "prefix chain deeper than max_prefix_depth",
                                "query_offsets not 0 = offsets[0] <= ... <= offsets[R] = num_query_rows",
                                "query rows of a request > min(suffix length, max_query_rows)",
-                               "rows reading a group's prefix > max_group_rows"};
+                               "rows reading a group's prefix > max_group_rows",
+                               "requests reading a group's prefix > max_group_size"};
+  constexpr int kCodes = (int)(sizeof what / sizeof what[0]) - 1;
   if (res[0] != 0)
     return fail(PARROT_ERR_INVALID_ARGUMENT, "%s at entry %d (value %d)",
-                (res[0] > 0 && res[0] <= 11) ? what[res[0]] : "unknown", res[1], res[2]);
+                (res[0] > 0 && res[0] <= kCodes) ? what[res[0]] : "unknown", res[1], res[2]);
   g_err.clear();
   return PARROT_OK;
 }

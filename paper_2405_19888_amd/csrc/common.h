@@ -39,6 +39,7 @@ struct Plan {
 };
 
 constexpr int kMaxRequests = 1024;   // per call (split-KV keeps per-request data in LDS)
+constexpr int kSkvWaves = 4;         // waves per split-KV workgroup
 constexpr int kMaxDepth = 4;         // prefix levels of nested groups
 constexpr int kMetaInts = 4;         // merge_meta ints per request
 

@@ -159,8 +159,10 @@ hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hip
 // 2 bad prefix length, 3 bad suffix length, 4 empty context, 5 prefix block id
 // out of the pool, 6 suffix block id out of the pool, 7 bad parent, 8 chain
 // too deep; prefill rows: 9 bad row offsets, 10 too many rows for a request,
-// 11 too many rows reading a group.  result[1] is the entry index, result[2]
-// the offending value.
+// 11 too many rows reading a group; decode: 12 more requests read a group's
+// prefix than max_group_size (the prefix role sizes its query tiles from that
+// bound, so readers past it would get no prefix partial).  result[1] is the
+// entry index, result[2] the offending value.
 PARROT_DEV void report(int* res, int code, int idx, int val) {
   if (atomicCAS(res, 0, code) == 0) { res[1] = idx; res[2] = val; }
 }
@@ -195,24 +197,27 @@ __global__ __launch_bounds__(256) void k_validate(ValidateArgs a) {
       if (id < 0 || id >= a.nsblk) report(a.result, 6, r * a.sstride + b, id);
     }
   }
-  if (!a.qoff) return;                       // uniform: decode inputs only
-  if (threadIdx.x == 0) {
-    if (a.qoff[0] != 0) report(a.result, 9, 0, a.qoff[0]);
-    if (a.qoff[a.R] != a.T) report(a.result, 9, a.R, a.qoff[a.R]);
+  if (a.qoff) {
+    if (threadIdx.x == 0) {
+      if (a.qoff[0] != 0) report(a.result, 9, 0, a.qoff[0]);
+      if (a.qoff[a.R] != a.T) report(a.result, 9, a.R, a.qoff[a.R]);
+    }
+    for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
+      const long n = (long)a.qoff[r + 1] - a.qoff[r];
+      if (n < 0) { report(a.result, 9, r + 1, a.qoff[r + 1]); continue; }
+      if (n > a.slen[r] || n > a.max_q) report(a.result, 10, r, (int)n);
+    }
   }
-  for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-    const long n = (long)a.qoff[r + 1] - a.qoff[r];
-    if (n < 0) { report(a.result, 9, r + 1, a.qoff[r + 1]); continue; }
-    if (n > a.slen[r] || n > a.max_q) report(a.result, 10, r, (int)n);
-  }
-  // rows reading each group: its members' rows and its descendants', summed
-  // in LDS for 1024 groups at a time
+  // readers of each group's prefix: its members and its descendants' members
+  // (decode: one per request; prefill: the request's rows), summed in LDS for
+  // 1024 groups at a time and compared with the bound the launch was sized for
   __shared__ unsigned long long cnt[1024];
+  const int code = a.qoff ? 11 : 12;
   for (int g0 = 0; g0 < a.NG; g0 += 1024) {
     for (int i = threadIdx.x; i < 1024; i += blockDim.x) cnt[i] = 0;
     __syncthreads();
     for (int r = threadIdx.x; r < a.R; r += blockDim.x) {
-      const long n = (long)a.qoff[r + 1] - a.qoff[r];
+      const long n = a.qoff ? (long)a.qoff[r + 1] - a.qoff[r] : 1;
       const unsigned long long add = n > 0 ? (unsigned long long)n : 0ull;
       int x = a.gid[r];
       for (int d = 0; d < a.depth && x >= 0 && x < a.NG; ++d) {
@@ -223,7 +228,7 @@ __global__ __launch_bounds__(256) void k_validate(ValidateArgs a) {
     __syncthreads();
     for (int i = threadIdx.x; i < 1024 && g0 + i < a.NG; i += blockDim.x)
       if (cnt[i] > (unsigned long long)a.max_grp)
-        report(a.result, 11, g0 + i, cnt[i] > 0x7fffffffull ? 0x7fffffff : (int)cnt[i]);
+        report(a.result, code, g0 + i, cnt[i] > 0x7fffffffull ? 0x7fffffff : (int)cnt[i]);
     __syncthreads();
   }
 }

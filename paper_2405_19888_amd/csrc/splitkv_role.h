@@ -27,7 +27,6 @@
 
 namespace parrot {
 
-constexpr int kSkvWaves = 4;   // waves per split-KV workgroup
 // LDS bytes the split-KV role needs: six per-request arrays and a total.
 constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 

@@ -91,9 +91,10 @@ def test_nested_entry_with_flat_groups_matches_flat_entry():
 
 
 def test_nested_system_prompt_workload():
-    """The two-level workload at full size: sampled requests against the
-    oracle; every request against the flat entry points run on the same
+    """The two-level workload at full size: every request against the oracle;
+    as an extra, every request against the flat entry points run on the same
     blocks with each sub-group's chain laid end to end."""
+    from oracle_pool import oracle_decode
     cfg = get_config("nested")
     plan = make_plan(cfg)
     say(cfg.name, "requests", plan.num_requests)
@@ -101,11 +102,8 @@ def test_nested_system_prompt_workload():
     dev = batch.to("cuda")
     out, lse = run_gpu(plan, dev)
     o, l = to_np(out, lse)
-    rng = np.random.default_rng(0)
-    reqs = sorted(set(rng.choice(plan.num_requests, size=10, replace=False).tolist()) |
-                  {0, plan.num_requests - 1})
-    assert_close(o[reqs], l[reqs], *oracle_for(batch, plan, requests=reqs), plan.dtype,
-                 "nested workload sampled")
+    ref = oracle_decode(batch.q, (batch.k_pool, batch.v_pool, batch.k_pool, batch.v_pool), plan)
+    assert_close(o, l, *ref, plan.dtype, "nested workload, every request")
     flat = flatten_nested(plan)
     fdev = dict(dev)
     for k, v in (("prefix_tables", flat.prefix_tables), ("prefix_lens", flat.prefix_lens),

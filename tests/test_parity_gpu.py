@@ -2,7 +2,7 @@
 
 Every case prints its name before touching the GPU, validates the device-side
 inputs with parrot_validate_inputs, NaN-poisons the outputs and the workspace,
-and compares element by element (sampled requests at the largest sizes).
+and compares element by element.
 """
 import math
 import sys
@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from gpu_util import assert_close, oracle_for, problem_for, run_gpu, to_np
-from workloads import build_plan, get_config, make_batch, make_device_layer, make_plan
+from workloads import build_plan, get_config, make_batch, make_plan
 
 pytestmark = pytest.mark.gpu
 
@@ -22,16 +22,6 @@ DTYPES = ["float16", "bfloat16", "float32"]
 def say(*a):
     print("[case]", *a, flush=True)
     sys.stdout.flush()
-
-
-def sample_requests(plan, k=12, seed=0):
-    R = plan.num_requests
-    rng = np.random.default_rng(seed)
-    ctx = plan.context_lens()
-    pick = {0, R - 1, int(np.argmax(ctx)), int(np.argmin(ctx)),
-            int(np.argmax(plan.suffix_lens)), int(np.argmin(plan.suffix_lens))}
-    pick |= set(rng.choice(R, size=min(k, R), replace=False).tolist())
-    return sorted(pick)
 
 
 # ------------------------------------------------------------------ workloads
@@ -47,50 +37,8 @@ def test_config_full_parity(name, shared):
     assert_close(*to_np(out, lse), *ref, plan.dtype, f"{cfg.name} shared={shared}")
 
 
-@pytest.mark.parametrize("name", ["c3", "c4"])
-def test_config_sampled_parity(name):
-    cfg = get_config(name)
-    say(name, cfg.name)
-    plan = make_plan(cfg)
-    batch = make_batch(plan)
-    dev = batch.to("cuda")
-    out, lse = run_gpu(plan, dev, shared=True)
-    out_s, lse_s = to_np(out, lse)
-    reqs = sample_requests(plan)
-    ref = oracle_for(batch, plan, requests=reqs)
-    assert_close(out_s[reqs], lse_s[reqs], *ref, plan.dtype, f"{cfg.name} sampled")
-    # every request: finite, and the unshared path agrees within the same bar
-    out2, lse2 = run_gpu(plan, dev, shared=False)
-    o2, l2 = to_np(out2, lse2)
-    assert np.all(np.isfinite(out_s)) and np.all(np.isfinite(lse_s))
-    assert np.max(np.abs(out_s - o2)) <= 2e-3
-    assert np.max(np.abs(lse_s - l2) / np.maximum(1, np.abs(l2))) <= 1e-4
-
-
-def test_mixed_32_layer_serving_step():
-    """32 layers resident on the device (about 4 GB of bf16 KV each); every
-    layer is decoded, layers 0, 15 and 31 are checked on sampled requests."""
-    cfg = get_config("c5")
-    plan = make_plan(cfg)
-    say(cfg.name, "layers", cfg.layers, "blocks", plan.num_blocks)
-    layers = [make_device_layer(plan, l, "cuda") for l in range(cfg.layers)]
-    from paper_2405_19888_amd import Decoder
-    prob = problem_for(plan)
-    dec = Decoder(prob)
-    results = {}
-    for l, dev in enumerate(layers):
-        out, lse = dec(dev, shared=True)
-        if l in (0, 15, 31):
-            results[l] = (out.clone(), lse.clone())
-    torch.cuda.synchronize()
-    reqs = sample_requests(plan, k=6)
-    for l, (out, lse) in results.items():
-        say(cfg.name, "check layer", l, "requests", reqs)
-        o, s = to_np(out, lse)
-        assert np.all(np.isfinite(o)) and np.all(np.isfinite(s))
-        ref = oracle_for(layers[l], plan, requests=reqs,
-                         pools=(layers[l]["k_pool"], layers[l]["v_pool"]))
-        assert_close(o[reqs], s[reqs], *ref, plan.dtype, f"layer {l}")
+# The shared-system-prompt, map-reduce and 32-layer mixed workloads are
+# compared request by request with the oracle in test_fullsize_gpu.py.
 
 
 # ----------------------------------------------------------------- edge cases
@@ -289,6 +237,29 @@ def test_validate_inputs_reports_bad_entries():
     with pytest.raises(ParrotError, match="group id"):
         parrot_validate_inputs(prob, dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"],
                                dev["suffix_lens"], badg, scratch)
+
+
+def test_validate_inputs_reports_group_above_max_group_size():
+    """A group read by 65 requests under max_group_size = 64: the prefix role
+    sizes its query tiles from the bound, so the validator must refuse it."""
+    say("validate max_group_size")
+    from paper_2405_19888_amd import ParrotError, parrot_validate_inputs
+    rng = np.random.default_rng(11)
+    plan = build_plan(heads=2, head_dim=128, block_size=16, dtype="float16",
+                      group_of_request=[0] * 65 + [-1], prefix_lens=[40],
+                      suffix_lens=rng.integers(1, 30, size=66).tolist(),
+                      sm_scale=1 / math.sqrt(128), shuffle=True, rng=rng)
+    dev = make_batch(plan).to("cuda")
+    prob = problem_for(plan)
+    scratch = torch.zeros(16, dtype=torch.int32, device="cuda")
+    args = (dev["prefix_tables"], dev["prefix_lens"], dev["suffix_tables"], dev["suffix_lens"],
+            dev["group_ids"], scratch)
+    assert prob.max_group_size == 65
+    parrot_validate_inputs(prob, *args)
+    prob.max_group_size = 64
+    with pytest.raises(ParrotError, match="max_group_size") as e:
+        parrot_validate_inputs(prob, *args)
+    assert e.value.status == 1
 
 
 def test_trace_events_time_each_kernel():
