@@ -85,8 +85,10 @@ def oracle_decode(q, pools, plan, requests=None):
     ctx = tmp.get_context("spawn")
     with ctx.Pool(min(workers(), max(1, len(reqs))), initializer=_init,
                   initargs=(_state(q, pools, plan),)) as pool:
-        for r, o, l in pool.imap_unordered(_decode_one, order):
+        for i, (r, o, l) in enumerate(pool.imap_unordered(_decode_one, order)):
             out[pos[r]], lse[pos[r]] = o, l
+            if (i + 1) % 64 == 0:
+                print(f"[oracle] {i + 1}/{len(reqs)} requests", flush=True)
     return out, lse
 
 
@@ -111,7 +113,9 @@ def oracle_prefill(q_rows, offsets, pools, plan, rows=None):
     ctx = tmp.get_context("spawn")
     with ctx.Pool(min(workers(), max(1, len(order))), initializer=_init,
                   initargs=(_state(q_rows, pools, plan, qoff=off),)) as pool:
-        for rs, o, l in pool.imap_unordered(_prefill_rows, order):
+        for k, (rs, o, l) in enumerate(pool.imap_unordered(_prefill_rows, order)):
             for i, t in enumerate(rs):
                 out[pos[t]], lse[pos[t]] = o[i], l[i]
+            if (k + 1) % 32 == 0:
+                print(f"[oracle] {k + 1}/{len(order)} row tasks", flush=True)
     return out, lse

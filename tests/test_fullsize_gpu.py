@@ -174,6 +174,8 @@ def spike_sweep(plan, dev, what, paths=(True, False), max_calls=None):
         finally:
             k_dev[bi, :, si] = saved
         checked += len(reqs)
+        if (i + 1) % 100 == 0:
+            say(what, "spike call", i + 1, "of", calls)
     torch.cuda.synchronize()
     return calls, checked
 
@@ -218,7 +220,11 @@ def mixed_workload():
     from paper_2405_19888_amd import Decoder
     dec = Decoder(problem_for(plan))
     kept, outs = {}, {}
-    layers = [make_device_layer(plan, l, "cuda", seed=cfg.seed) for l in range(cfg.layers)]
+    layers = []
+    for l in range(cfg.layers):
+        layers.append(make_device_layer(plan, l, "cuda", seed=cfg.seed))
+        if l % 8 == 7:
+            say(cfg.name, "layers resident:", l + 1)
     run_gpu(plan, layers[0], decoder=dec)            # validates the inputs once
     for shared in (True, False):
         for l, dev in enumerate(layers):
