@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 4
+#define PARROT_ABI_VERSION 5
 
 typedef enum {
   PARROT_OK = 0,
@@ -159,6 +159,35 @@ parrot_status parrot_shared_prefix_decode(
     const int32_t* group_ids,
     void* out, float* lse,
     void* workspace, size_t workspace_bytes,
+    void* stream, const parrot_trace* trace);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * parrot_shared_prefix_decode without a workspace argument.  The partial
+ * results go to a fixed array inside the library, PARROT_STATIC_SCRATCH_BYTES
+ * (64 MiB) per device, which each device the library runs on holds until the
+ * process ends.  The call allocates nothing (no hipMalloc, no library
+ * allocation); the caller still owns q, the pools, the tables, out and lse.
+ * A call whose partial results need more than the array holds (about
+ * R * H * (prefix chunks + split-KV pieces) * (D + 1) * 4 bytes, so larger
+ * batches) returns PARROT_ERR_WORKSPACE_TOO_SMALL before any launch.  Calls
+ * that overlap on one device share the array and race: serialise them (one
+ * stream, or events).  The array keeps the last call's contents; every call
+ * writes each partial result before reading it, so it needs no clearing.
+ * Results equal parrot_shared_prefix_decode's on the same inputs.  Other
+ * arguments as parrot_shared_prefix_decode.
+ */
+#define PARROT_STATIC_SCRATCH_BYTES (64u << 20)
+parrot_status parrot_shared_prefix_decode_noalloc(
+    const parrot_problem* p,
+    const void* q,
+    const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v,
+    const int32_t* prefix_block_tables, const int32_t* prefix_lens,
+    const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids,
+    void* out, float* lse,
     void* stream, const parrot_trace* trace);
 
 /*

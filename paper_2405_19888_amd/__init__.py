@@ -22,6 +22,7 @@ from .binding import (  # noqa: F401
     parrot_prefill_workspace_bytes,
     parrot_shared_prefix_decode,
     parrot_shared_prefix_decode_append,
+    parrot_shared_prefix_decode_noalloc,
     parrot_shared_prefix_prefill,
     parrot_validate_inputs,
     parrot_validate_nested_inputs,

@@ -74,7 +74,10 @@ EXPORTED = (
     "parrot_validate_inputs", "parrot_validate_nested_inputs",
     "parrot_prefill_workspace_bytes", "parrot_prefill_single_pass", "parrot_shared_prefix_prefill",
     "parrot_validate_prefill_inputs", "parrot_last_error", "parrot_abi_version",
+    "parrot_shared_prefix_decode_noalloc",
 )
+
+STATIC_SCRATCH_BYTES = 64 << 20   # PARROT_STATIC_SCRATCH_BYTES
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -98,6 +101,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = dec_args
         f.restype = ctypes.c_int
+    lib.parrot_shared_prefix_decode_noalloc.argtypes = dec_args[:13] + dec_args[15:]
+    lib.parrot_shared_prefix_decode_noalloc.restype = ctypes.c_int
     lib.parrot_shared_prefix_decode_append.argtypes = dec_args[:2] + [vp, vp] + dec_args[2:]
     lib.parrot_shared_prefix_decode_append.restype = ctypes.c_int
     lib.parrot_nested_prefix_decode.argtypes = dec_args[:8] + [i32p] + dec_args[8:]
@@ -196,6 +201,20 @@ def parrot_shared_prefix_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix
     _decode("parrot_shared_prefix_decode", problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
             prefix_block_tables, prefix_lens, suffix_block_tables, suffix_lens, group_ids,
             out, lse, workspace, stream, trace)
+
+
+def parrot_shared_prefix_decode_noalloc(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,
+                                        prefix_block_tables, prefix_lens, suffix_block_tables,
+                                        suffix_lens, group_ids, out, lse, stream=None,
+                                        trace=None):
+    """Shared-prefix decode attention with the library's fixed partial-result
+    array instead of a workspace (allocates nothing; see the C header)."""
+    lib = load_library()
+    _check(lib.parrot_shared_prefix_decode_noalloc(
+        ctypes.byref(problem), _ptr(q), _ptr(prefix_k), _ptr(prefix_v), _ptr(suffix_k),
+        _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(suffix_block_tables),
+        _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse), _stream_handle(stream),
+        ctypes.byref(trace) if trace is not None else None))
 
 
 def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,

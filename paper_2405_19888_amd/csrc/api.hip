@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "parrot_attn.h"
@@ -214,6 +215,21 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   return PARROT_OK;
 }
 
+// The workspace layout of one shared-path call sized for that call alone: the
+// prefix chunks of this call's chunk size and its split-KV pieces, with no
+// slots reserved for the per-request path or for smaller chunks (used where
+// the workspace is the library's own fixed array and is laid out afresh on
+// every call).
+void exact_shared_layout(const parrot_problem* p, parrot::Plan* pl) {
+  pl->seg = pl->seg_pre + pl->seg_s;
+  const size_t n_slots = (size_t)p->num_requests * p->num_heads * pl->seg;
+  auto align256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  pl->o_bytes = align256(n_slots * p->head_dim * sizeof(float));
+  pl->lse_bytes = align256(n_slots * sizeof(float));
+  pl->info_bytes = align256((size_t)p->num_requests * parrot::kMetaInts * sizeof(int32_t));
+  pl->total_bytes = p->num_requests > 0 ? pl->o_bytes + pl->lse_bytes + pl->info_bytes : 0;
+}
+
 hipEvent_t ev(void* p) { return reinterpret_cast<hipEvent_t>(p); }
 
 parrot_status hip_ok(hipError_t e, const char* what) {
@@ -238,9 +254,10 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
                      const int32_t* stab, const int32_t* slen, const int32_t* gid, void* out,
                      float* lse, void* workspace, size_t workspace_bytes, void* stream,
                      const parrot_trace* trace, const void* k_new = nullptr,
-                     const void* v_new = nullptr) {
+                     const void* v_new = nullptr, bool exact = false) {
   parrot::Plan pl;
   PARROT_TRY(check_problem(p, &pl));
+  if (exact) exact_shared_layout(p, &pl);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const parrot_trace none = {nullptr, nullptr, nullptr, nullptr};
   const parrot_trace& tr = trace ? *trace : none;
@@ -392,6 +409,71 @@ parrot_status parrot_nested_prefix_decode(
                 prefix_lens, p && p->num_groups > 0 ? prefix_parents : nullptr,
                 suffix_block_tables, suffix_lens, group_ids, out, lse, workspace,
                 workspace_bytes, stream, trace);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------ allocation-free decode
+// The partial-result workspace of parrot_shared_prefix_decode_noalloc: one
+// fixed array per device, held from the library's load on that device until
+// the process ends.  Every call lays its partial results out afresh and
+// writes each slot before the merge reads it, so nothing in it has to start
+// at zero; calls that overlap on one device share it and race.
+static __device__ __align__(256) char scratch[PARROT_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of `scratch` on the current device, looked up once per
+// device with that device current.  The array's name in host code is only a
+// host-side handle; kernels get this address.
+parrot_status static_scratch(void** out) {
+  static std::atomic<void*> addr[64];
+  static std::mutex mu;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(PARROT_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(PARROT_ERR_UNSUPPORTED, "device %d (at most 64 devices)", dev);
+  void* ptr = addr[dev].load(std::memory_order_acquire);
+  if (!ptr) {
+    std::lock_guard<std::mutex> lock(mu);
+    ptr = addr[dev].load(std::memory_order_relaxed);
+    if (!ptr) {
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !ptr)
+        return fail(PARROT_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      addr[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return PARROT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+parrot_status parrot_shared_prefix_decode_noalloc(
+    const parrot_problem* p, const void* q, const void* prefix_k, const void* prefix_v,
+    const void* suffix_k, const void* suffix_v, const int32_t* prefix_block_tables,
+    const int32_t* prefix_lens, const int32_t* suffix_block_tables, const int32_t* suffix_lens,
+    const int32_t* group_ids, void* out, float* lse, void* stream, const parrot_trace* trace) {
+  parrot::Plan pl;
+  PARROT_TRY(check_problem(p, &pl));
+  if (p->num_requests == 0) {
+    g_err.clear();
+    return PARROT_OK;
+  }
+  exact_shared_layout(p, &pl);
+  if (pl.total_bytes > (size_t)PARROT_STATIC_SCRATCH_BYTES)
+    return fail(PARROT_ERR_WORKSPACE_TOO_SMALL,
+                "this call needs %zu bytes of partial results; the library's fixed array holds %zu "
+                "(use parrot_shared_prefix_decode with a workspace)",
+                pl.total_bytes, (size_t)PARROT_STATIC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  PARROT_TRY(static_scratch(&ws));
+  return decode(true, p, q, prefix_k, prefix_v, suffix_k, suffix_v, prefix_block_tables,
+                prefix_lens, nullptr, suffix_block_tables, suffix_lens, group_ids, out, lse, ws,
+                (size_t)PARROT_STATIC_SCRATCH_BYTES, stream, trace, nullptr, nullptr, true);
 }
 
 }  // extern "C"

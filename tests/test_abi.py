@@ -59,7 +59,24 @@ def test_binding_matches_header_arity(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 4
+    assert B.parrot_abi_version() == 5
+
+
+def test_noalloc_refuses_batches_above_its_array_without_a_device(parrot_lib):
+    """The allocation-free entry point sizes the call on the host and refuses
+    one whose partial results exceed the library's fixed array before it
+    touches the device (pointers are never read)."""
+    big = base_problem(num_requests=512, num_groups=8, max_group_size=64, max_prefix_len=4096,
+                       prefix_table_stride=256, max_suffix_len=4096, suffix_table_stride=256)
+    st = parrot_lib.parrot_shared_prefix_decode_noalloc(
+        ctypes.byref(big), *([None] * 12), None, None)
+    assert st == B.PARROT_ERR_WORKSPACE_TOO_SMALL
+    assert "fixed array" in B.parrot_last_error()
+    st = parrot_lib.parrot_shared_prefix_decode_noalloc(
+        ctypes.byref(base_problem(num_requests=0)), *([None] * 12), None, None)
+    assert st == B.PARROT_OK
+    st = parrot_lib.parrot_shared_prefix_decode_noalloc(None, *([None] * 12), None, None)
+    assert st == B.PARROT_ERR_INVALID_ARGUMENT
 
 
 def base_problem(**over):
