@@ -2,34 +2,36 @@
 
 One step is one call of parrot_shared_prefix_decode (partial-result kernel
 with its prefix-group and split-KV roles, then the merge kernel) for one layer
-of a decode batch.  The default
-workload is the LLaMA-7B layer shape: 32 heads x 128, fp16 KV in 16-token
-blocks with permuted block tables, one prefix group of 32 requests sharing a
-2048-token prefix, own lengths U[64,512].  Steps cycle through `--layers`
-layers with distinct KV values, all resident in HBM, so a layer's KV is not
-still in the 256 MB Infinity Cache when it is read again.  A multi-layer
-workload (`--config c5`: 32 LLaMA-7B layers) cycles through all of its own
-layers instead, and a step is one layer of it.
+of a decode batch.  The headline workload is the full-depth mixed serving
+step: 32 LLaMA-7B layers (32 heads x 128, bf16 KV in 16-token blocks with
+permuted block tables), 256 requests in 8 Zipf(1.1) prefix groups plus 32
+ungrouped requests.  All 32 layers are resident in HBM with their own KV and
+the steps cycle through them, so a layer's KV is never still in the 256 MB
+Infinity Cache when it is read again.  A one-layer workload cycles `--layers`
+distinct-KV copies instead.
 
-After the decode line's measurements, a prefill leg (`--prefill`, default the
-Fill of 64 contexts forked from a 6000-token system prompt) times
-parrot_shared_prefix_prefill and reports it under "prefill" with an MFMA
-roofline; `--mode prefill` prints only that leg as the line.
+The line carries, besides the headline: the same measurements for the other
+decode workloads (`workloads`), the prefix-length sweep of the shared path
+against the per-request path (`sweep`), a prefill leg (`prefill`: the Fill of
+64 contexts forked from a 6000-token system prompt, with an MFMA roofline),
+the device's read-bandwidth ceiling measured in the same process by the
+library's read probe (`ceilings`), and the float64 CPU oracle timed on a
+bounded sample of the headline workload (`cpu_baseline`).  `--mode prefill`
+prints only the prefill leg as the line.
 
-Prints one JSON line.  `value` is requests per second per layer
-(R / seconds per step).  The `roofline` object describes the dominant kernel
-(the partial-result kernel) from HIP events attached to its launches on the
-launch stream during the timed steps, and `ceilings` holds a plain device copy
-measured in the same process; `cpu_baseline` times the float64 CPU oracle on a
-bounded sample of the same workload.
+`value` is requests per second per layer (R / seconds per step).  The
+`roofline` object describes the dominant kernel (the partial-result kernel)
+from HIP events attached to its launches on the launch stream during the
+timed steps.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
-import re
 import json
 import os
+import re
+import subprocess
 import sys
 import time
 
@@ -47,6 +49,7 @@ PREFILL_COUNTERS_FILE = os.path.join(ROOT, "profiles", "prefill_counters.json")
 PREFILL_SOURCES = ["paper_2405_19888_amd/csrc/prefill.hip", "paper_2405_19888_amd/csrc/prefill_tile.h",
                    "paper_2405_19888_amd/csrc/prefill_shape.h", "paper_2405_19888_amd/csrc/prefill_args.h",
                    "paper_2405_19888_amd/csrc/prefix_role.h", "paper_2405_19888_amd/csrc/common.h"]
+SWEEP_DEFAULT = "256,512,1024,2048,4096,8192,16384"
 
 
 def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
@@ -60,6 +63,20 @@ def kernel_source_hash(sources=KERNEL_SOURCES) -> str:
         src = re.sub(r"//[^\n]*", " ", src)
         h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
+
+
+def traffic_from_counters(workload: str, path: str = COUNTERS_FILE, sources=KERNEL_SOURCES):
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3
+    counter runs on `workload`, only if they were taken on the current kernel
+    source."""
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != kernel_source_hash(sources):
+        return None
+    w = rec.get("workloads", {}).get(workload)
+    return None if w is None else w.get("bytes_per_launch")
 
 
 def algorithmic_bytes(plan):
@@ -83,17 +100,27 @@ def algorithmic_bytes(plan):
                 prefix_flops=prefix_flops)
 
 
-def host_info() -> dict:
-    """The host CPU model and the BLAS numpy / torch link against."""
-    model = None
+# ------------------------------------------------------------------ CPU side
+def cpu_model() -> str | None:
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
                 if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
-                    break
+                    return line.split(":", 1)[1].strip()
     except OSError:
         pass
+    return None
+
+
+def host_info() -> dict:
+    """The host CPU model and the BLAS numpy links against."""
     blas = None
     try:
         import numpy as np
@@ -101,45 +128,61 @@ def host_info() -> dict:
         blas = deps.get("blas", {}).get("name")
     except Exception:
         pass
-    try:
+    return {"cpu_model": cpu_model(), "numpy_blas": blas}
+
+
+class pinned_host_threads:
+    """BLAS / OpenMP pools and torch's intra-op pool pinned to the CPUs this
+    process may run on, for the duration of the block."""
+
+    def __enter__(self):
         import torch
-        threads = torch.get_num_threads()
-    except Exception:
-        threads = None
-    return {"cpu_model": model, "numpy_blas": blas, "torch_threads": threads}
+        from threadpoolctl import threadpool_limits
+        self.n = len(os.sched_getaffinity(0))
+        self.prev = torch.get_num_threads()
+        self.limits = threadpool_limits(limits=self.n)
+        torch.set_num_threads(self.n)
+        return self.n
+
+    def __exit__(self, *exc):
+        import torch
+        torch.set_num_threads(self.prev)
+        self.limits.restore_original_limits()
+        return False
 
 
 def cpu_baseline(plan, layer_dev, budget_s: float):
     """The oracle on host copies of one layer, request by request, for ~budget_s."""
     import numpy as np
-    import torch
     import oracle
 
     q = layer_dev["q"].cpu()
     kp = layer_dev["k_pool"].cpu()
     vp = layer_dev["v_pool"].cpu()
-    t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
-    done = 0
     order = np.random.default_rng(0).permutation(plan.num_requests)
-    while True:
-        r = int(order[done % plan.num_requests])
-        oracle.shared_prefix_decode(q, kp, vp, kp, vp, plan.prefix_tables, plan.prefix_lens,
-                                    plan.suffix_tables, plan.suffix_lens, plan.group_ids,
-                                    plan.sm_scale, requests=[r],
-                                    prefix_parents=plan.prefix_parents if plan.nested else None)
-        done += 1
-        wall = time.perf_counter() - t_wall0
-        if wall >= budget_s:
-            break
-    cpu = time.process_time() - t_cpu0
+    with pinned_host_threads() as n:
+        t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
+        done = 0
+        while True:
+            r = int(order[done % plan.num_requests])
+            oracle.shared_prefix_decode(q, kp, vp, kp, vp, plan.prefix_tables, plan.prefix_lens,
+                                        plan.suffix_tables, plan.suffix_lens, plan.group_ids,
+                                        plan.sm_scale, requests=[r],
+                                        prefix_parents=plan.prefix_parents if plan.nested else None)
+            done += 1
+            wall = time.perf_counter() - t_wall0
+            if wall >= budget_s:
+                break
+        cpu = time.process_time() - t_cpu0
     return {
-        "value": done / wall,
+        "value": round(done / wall, 3),
         "unit": "req/s per layer",
-        "cores": max(1, int(round(cpu / wall))),
-        "cores_available": len(os.sched_getaffinity(0)),
+        "cores": n,
+        "threads_note": "BLAS/OpenMP and torch thread pools pinned to the process's CPU affinity",
+        "cpu_time_per_wall": round(cpu / wall, 2),
         **host_info(),
         "kind": "oracle",
-        "sample": f"{done} requests of one layer of the same workload, one oracle call each, "
+        "sample": f"{done} random requests of layer 0 of the same workload, one oracle call each, "
                   f"{wall:.1f} s wall, {cpu:.1f} s CPU",
     }
 
@@ -169,24 +212,25 @@ def cpu_prefill_baseline(plan, q_rows, offsets, layer_dev, budget_s: float):
     vp = layer_dev["v_pool"].cpu()
     T = int(offsets[-1])
     order = np.random.default_rng(0).permutation(T)
-    t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
-    done = 0
-    while True:
-        t = int(order[done % T])
-        oracle.shared_prefix_prefill(q, offsets, kp, vp, kp, vp, plan.prefix_tables,
-                                     plan.prefix_lens, plan.suffix_tables, plan.suffix_lens,
-                                     plan.group_ids, plan.sm_scale, rows=[t],
-                                     prefix_parents=plan.prefix_parents if plan.nested else None)
-        done += 1
-        wall = time.perf_counter() - t_wall0
-        if wall >= budget_s:
-            break
-    cpu = time.process_time() - t_cpu0
+    with pinned_host_threads() as n:
+        t_wall0, t_cpu0 = time.perf_counter(), time.process_time()
+        done = 0
+        while True:
+            t = int(order[done % T])
+            oracle.shared_prefix_prefill(q, offsets, kp, vp, kp, vp, plan.prefix_tables,
+                                         plan.prefix_lens, plan.suffix_tables, plan.suffix_lens,
+                                         plan.group_ids, plan.sm_scale, rows=[t],
+                                         prefix_parents=plan.prefix_parents if plan.nested else None)
+            done += 1
+            wall = time.perf_counter() - t_wall0
+            if wall >= budget_s:
+                break
+        cpu = time.process_time() - t_cpu0
     return {
-        "value": done / wall,
+        "value": round(done / wall, 3),
         "unit": "rows/s per layer",
-        "cores": max(1, int(round(cpu / wall))),
-        "cores_available": len(os.sched_getaffinity(0)),
+        "cores": n,
+        "cpu_time_per_wall": round(cpu / wall, 2),
         **host_info(),
         "kind": "oracle",
         "sample": f"{done} random query rows of one layer of the same workload, one oracle "
@@ -194,6 +238,361 @@ def cpu_prefill_baseline(plan, q_rows, offsets, layer_dev, budget_s: float):
     }
 
 
+# ------------------------------------------------------------------ ceilings
+def read_ceiling(torch, gib: int = 4, reps: int = 3) -> dict:
+    """Read-only HBM bandwidth from the library's read probe (16-byte
+    nontemporal loads over a buffer 16x the Infinity Cache), best over its
+    access orders and a few launch shapes."""
+    from paper_2405_19888_amd import parrot_hbm_read_ceiling
+    nbytes = gib << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    stream = torch.cuda.current_stream()
+    best, trials = None, []
+    for spans in (True, False):
+        for wpc in (1, 2, 4, 8):
+            for unroll in (4, 8, 16):
+                parrot_hbm_read_ceiling(buf, sink, cus * wpc, unroll, spans, stream=stream)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    parrot_hbm_read_ceiling(buf, sink, cus * wpc, unroll, spans, stream=stream)
+                e1.record(stream)
+                e1.synchronize()
+                gbps = reps * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9
+                trials.append({"order": "wave_spans" if spans else "grid_stride",
+                               "workgroups_per_cu": wpc, "loads_per_thread": unroll,
+                               "gbps": round(gbps, 1)})
+                if best is None or gbps > best["gbps"]:
+                    best = trials[-1]
+    del buf
+    torch.cuda.empty_cache()
+    return {"read_gbps": best["gbps"], "read_best_shape": best, "read_trials": trials,
+            "read_note": f"parrot_hbm_read_ceiling over {gib} GiB, {reps} passes per shape, "
+                         f"HIP events on the launch stream"}
+
+
+def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
+    """Read + write GB/s of a plain device-to-device copy (measured in the
+    same process; a copy both reads and writes, so it is not the read
+    ceiling)."""
+    src = torch.ones(mib << 19, dtype=torch.float16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    gbps = 2 * reps * src.numel() * 2 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
+# ------------------------------------------------------------------ decode
+def problem_of(plan, flat=None):
+    from paper_2405_19888_amd import problem_from_host
+    from workloads.gen import TORCH_DTYPES
+    p = flat or plan
+    return problem_from_host(
+        num_heads=p.heads, head_dim=p.head_dim, block_size=p.block_size,
+        dtype=TORCH_DTYPES[p.dtype], sm_scale=p.sm_scale, group_ids=p.group_ids,
+        prefix_lens=p.prefix_lens, suffix_lens=p.suffix_lens,
+        prefix_table_stride=p.prefix_tables.shape[1],
+        suffix_table_stride=p.suffix_tables.shape[1],
+        num_prefix_blocks=p.num_blocks, num_suffix_blocks=p.num_blocks,
+        prefix_parents=p.prefix_parents if (flat is None and p.nested) else None)
+
+
+def decode_leg(cfg_name: str, steps: int, warmup: int, one_layer_copies: int, trace_every: int,
+               baselines: bool, read_gbps: float | None, trace: bool = True, keep_layers=False):
+    """Time parrot_shared_prefix_decode on a decode workload.  Returns (the
+    leg's JSON object, the plan, the device layers if `keep_layers`)."""
+    import numpy as np
+    import torch
+    from paper_2405_19888_amd import (Decoder, ParrotTrace, parrot_validate_inputs,
+                                      parrot_validate_nested_inputs)
+    from workloads import get_config, make_device_layer, make_plan
+
+    cfg = get_config(cfg_name)
+    plan = make_plan(cfg)
+    dev = "cuda"
+    # A multi-layer workload cycles through all of its layers (each with its
+    # own KV, all resident); a one-layer workload cycles distinct-KV copies so
+    # that every call reads cold HBM.
+    n_layers = cfg.layers if cfg.layers > 1 else one_layer_copies
+    layers = [make_device_layer(plan, l, dev, seed=cfg.seed) for l in range(n_layers)]
+    prob = problem_of(plan)
+    scratch = torch.zeros(16, dtype=torch.int32, device=dev)
+    t0 = layers[0]
+    if plan.nested:
+        parrot_validate_nested_inputs(prob, t0["prefix_tables"], t0["prefix_lens"],
+                                      t0["prefix_parents"], t0["suffix_tables"], t0["suffix_lens"],
+                                      t0["group_ids"], scratch)
+    else:
+        parrot_validate_inputs(prob, t0["prefix_tables"], t0["prefix_lens"], t0["suffix_tables"],
+                               t0["suffix_lens"], t0["group_ids"], scratch)
+    dec = Decoder(prob, device=dev)
+    stream = torch.cuda.current_stream()
+    ab = algorithmic_bytes(plan)
+    K, W, L = steps, warmup, n_layers
+    names = ("partials", "merge")
+    nested = plan.nested
+    flat = flat_layers = flat_dec = None
+    new_kv = None
+    if nested:
+        # baselines for nested groups: the flat entry points on the same blocks,
+        # each group's chain of prefixes laid end to end as one flat prefix
+        from workloads.gen import flatten_nested
+        flat = flatten_nested(plan)
+        ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+                for k, v in (("prefix_tables", flat.prefix_tables), ("prefix_lens", flat.prefix_lens),
+                             ("group_ids", flat.group_ids))}
+        flat_layers = [dict(t, **ints) for t in layers]
+        flat_dec = Decoder(problem_of(plan, flat), device=dev)
+
+    def run(shared: bool, trace: bool, flat_baseline: bool = False, append: bool = False,
+            inputs=None, steps=None, every=None):
+        """W untimed steps, then K timed steps; every `every`-th timed step
+        carries per-kernel (start, stop) event pairs when `trace` is set."""
+        K = steps or K_default
+        if inputs is not None:
+            calls = [dec.bind(t, shared=shared, stream=stream, nested=nested) for t in inputs]
+        elif nested and (flat_baseline or not shared):
+            calls = [flat_dec.bind(flat_layers[l], shared=shared, stream=stream) for l in range(L)]
+        elif append:
+            calls = [dec.bind(dict(layers[l], k_new=new_kv[l][0], v_new=new_kv[l][1]),
+                              stream=stream, append=True) for l in range(L)]
+        else:
+            calls = [dec.bind(layers[l], shared=shared, stream=stream, nested=nested)
+                     for l in range(L)]
+        every = max(1, every or trace_every)
+        traced = list(range(0, K, every)) if trace else []
+        events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in traced}
+        for evs in events.values():       # materialise the events outside the timed region
+            for e in evs:
+                e.record(stream)
+        torch.cuda.synchronize()
+        traces = {i: ParrotTrace(*[e.cuda_event for e in evs]) for i, evs in events.items()}
+        n = len(calls)
+        for i in range(W):
+            calls[i % n]()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            calls[i % n](traces.get(i))
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per = None
+        if trace:
+            per = {}
+            for k, name in enumerate(names):
+                us = np.array([evs[2 * k].elapsed_time(evs[2 * k + 1]) * 1e3 for evs in events.values()])
+                per[name + "_us"] = float(us.mean())
+                per[name + "_pct"] = [round(float(x), 3) for x in np.percentile(us, [10, 50, 90])]
+            per["traced_steps"] = len(events)
+        return wall, per
+
+    K_default = K
+    wall, per = run(shared=True, trace=trace)
+    R = plan.num_requests
+    result = {
+        "value": round(R / (wall / K), 1),
+        "unit": "req/s",
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(wall / K * 1e3, 5),
+        "dtype": DTYPE_TAG[plan.dtype],
+        "config": {
+            "workload": cfg.name, "requests": R, "heads": plan.heads, "head_dim": plan.head_dim,
+            "prefix_groups": plan.num_groups, "group_sizes": plan.group_sizes(),
+            **({"prefix_parents": [int(x) for x in plan.prefix_parents]} if nested else {}),
+            "prefix_lens": [int(x) for x in plan.prefix_lens],
+            "suffix_len_mean": round(float(plan.suffix_lens.mean()), 1),
+            "ungrouped": int((plan.group_ids < 0).sum()),
+            "kv_block": plan.block_size, "kv_dtype": DTYPE_TAG[plan.dtype],
+            "layers": cfg.layers, "layers_cycled": L,
+            "timing": "HBM-resident inputs, distinct KV per cycled layer",
+        },
+        "algorithmic_bytes_per_step": ab["shared_total"],
+        "hbm_gbps": round(ab["shared_total"] / (wall / K) / 1e9, 1),
+    }
+    result["hbm_frac"] = round(result["hbm_gbps"] / HBM_PEAK_GBPS, 4)
+    if per is not None:
+        # dominant kernel: the partial-result kernel (prefix-group and split-KV roles)
+        part_bytes = ab["prefix_kv"] + ab["suffix_kv"] + ab["q"]
+        achieved = part_bytes / (per["partials_us"] * 1e-6) / 1e9
+        result["roofline"] = {
+            "kernel": "k_partials (prefix-group MFMA role + split-KV role)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic_from_counters(cfg.name),
+            "algorithmic_bytes": part_bytes,
+            "avg_us": round(per["partials_us"], 3),
+        }
+        if read_gbps:
+            result["roofline"]["frac_of_read_ceiling"] = round(achieved / read_gbps, 4)
+        result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
+        result["kernels_us"].update({k.replace("_pct", "_p10_p50_p90_us"): v
+                                     for k, v in per.items() if k.endswith("_pct")})
+        result["kernels_us"]["traced_steps"] = per["traced_steps"]
+        if ab["prefix_flops"] > 0:
+            intensity = ab["prefix_flops"] / ab["prefix_kv"]
+            result["prefix_mfma"] = {
+                "flops": ab["prefix_flops"],
+                "flop_per_byte": round(intensity, 2),
+                "util_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12
+                                                   / MFMA_F16_PEAK_TFLOPS, 5),
+                "util_ceiling_at_hbm_peak": round(min(1.0, intensity * HBM_PEAK_GBPS / 1e3
+                                                      / MFMA_F16_PEAK_TFLOPS), 5),
+            }
+    if baselines and per is not None and int(plan.suffix_lens.min()) > 0:
+        # The roles one at a time, on the same blocks (the kernel runs both
+        # roles side by side, so its events cannot split them):
+        #  * suffix + merge: every request ungrouped, so the partial-result
+        #    kernel streams only the own tokens, then the merge;
+        #  * prefix: grouped requests with no own tokens (ungrouped ones keep
+        #    one), so the kernel is the prefix-group role.
+        ungrouped = torch.full((R,), -1, dtype=torch.int32, device=dev)
+        slen_p = torch.from_numpy(np.where(plan.group_ids >= 0, 0, 1).astype(np.int32)).to(dev)
+        n_roles = min(K, 400)
+        _, per_s = run(shared=True, trace=True, steps=n_roles, every=4,
+                       inputs=[dict(t, group_ids=ungrouped) for t in layers])
+        _, per_p = run(shared=True, trace=True, steps=n_roles, every=4,
+                       inputs=[dict(t, suffix_lens=slen_p) for t in layers])
+        suffix_bytes = ab["suffix_kv"] + ab["q"] + ab["out"] + ab["lse"]
+        sm_us = per_s["partials_us"] + per_s["merge_us"]
+        sm_gbps = suffix_bytes / (sm_us * 1e-6) / 1e9
+        roles = {
+            "suffix_merge": {
+                "partials_us": round(per_s["partials_us"], 3), "merge_us": round(per_s["merge_us"], 3),
+                "algorithmic_bytes": suffix_bytes,
+                "gbps": round(sm_gbps, 1),
+                "frac_of_hbm_peak": round(sm_gbps / HBM_PEAK_GBPS, 4),
+                "partials_frac_of_hbm_peak": round((ab["suffix_kv"] + ab["q"]) / (per_s["partials_us"] * 1e-6)
+                                                   / 1e9 / HBM_PEAK_GBPS, 4),
+                "note": "the same call with every request ungrouped (own tokens only): "
+                        "partial-result kernel + merge, kernel events",
+            },
+        }
+        if read_gbps:
+            roles["suffix_merge"]["frac_of_read_ceiling"] = round(sm_gbps / read_gbps, 4)
+        if ab["prefix_flops"] > 0:
+            pre_us = per_p["partials_us"]
+            roles["prefix"] = {
+                "partials_us": round(pre_us, 3),
+                "algorithmic_bytes": ab["prefix_kv"] + ab["q"],
+                "gbps": round((ab["prefix_kv"] + ab["q"]) / (pre_us * 1e-6) / 1e9, 1),
+                "mfma_util": round(ab["prefix_flops"] / (pre_us * 1e-6) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+                "mfma_util_ceiling_at_hbm_peak": round(min(1.0, ab["prefix_flops"] / ab["prefix_kv"]
+                                                           * HBM_PEAK_GBPS / 1e3 / MFMA_F16_PEAK_TFLOPS), 5),
+                "note": "the same call with grouped requests holding no own tokens: the "
+                        "prefix-group role alone, kernel events",
+            }
+        result["roles"] = roles
+        # warm: one layer's KV reused by every call (it stays partly in the
+        # 256 MB Infinity Cache); the headline cycles distinct-KV layers
+        wall_w, _ = run(shared=True, trace=False, steps=n_roles, inputs=[layers[0]])
+        result["warm"] = {"ms_per_step": round(wall_w / n_roles * 1e3, 5),
+                          "value": round(R / (wall_w / n_roles), 1),
+                          "note": "one layer's KV reused by every call"}
+
+    if baselines:
+        if nested:
+            wall_f, _ = run(shared=True, trace=False, flat_baseline=True)
+            flat_bytes = (int(flat.prefix_lens.sum()) * 2 * plan.heads * plan.head_dim
+                          * ELT_BYTES[plan.dtype] + ab["shared_total"] - ab["prefix_kv"])
+            result["flat_sharing_baseline"] = {
+                "value": round(R / (wall_f / K), 1), "unit": "req/s",
+                "ms_per_step": round(wall_f / K * 1e3, 5),
+                "speedup_of_nested": round(wall_f / wall, 3),
+                "hbm_gbps": round(flat_bytes / (wall_f / K) / 1e9, 1),
+                "note": "parrot_shared_prefix_decode with each group's prefix chain as one flat prefix",
+            }
+        else:
+            # decode with append: the same step, with this step's K/V written
+            # into the cache by the partial-result kernel (the values equal
+            # what the slots already hold, so later steps see the same data)
+            last = [(r, int(plan.suffix_tables[r][(int(plan.suffix_lens[r]) - 1) // plan.block_size]),
+                     (int(plan.suffix_lens[r]) - 1) % plan.block_size)
+                    for r in range(R) if plan.suffix_lens[r] > 0]
+            rows = torch.tensor([x[0] for x in last], device=dev, dtype=torch.long)
+            blks = torch.tensor([x[1] for x in last], device=dev, dtype=torch.long)
+            slots = torch.tensor([x[2] for x in last], device=dev, dtype=torch.long)
+            new_kv = []
+            for t in layers:
+                pair = []
+                for name in ("k_pool", "v_pool"):
+                    x = torch.zeros((R, plan.heads, plan.head_dim), dtype=t["q"].dtype, device=dev)
+                    x[rows] = t[name][blks, :, slots]
+                    pair.append(x)
+                new_kv.append(pair)
+            wall_a, _ = run(shared=True, trace=False, append=True)
+            result["append_step"] = {
+                "ms_per_step": round(wall_a / K * 1e3, 5),
+                "overhead_vs_plain": round(wall_a / wall - 1.0, 4),
+                "note": "parrot_shared_prefix_decode_append on the same workload",
+            }
+            del new_kv
+        wall_n, _ = run(shared=False, trace=False)
+        result["per_request_baseline"] = {
+            "value": round(R / (wall_n / K), 1), "unit": "req/s",
+            "ms_per_step": round(wall_n / K * 1e3, 5),
+            "speedup_of_shared": round(wall_n / wall, 3),
+            "hbm_gbps": round(ab["naive_total"] / (wall_n / K) / 1e9, 1),
+            "byte_ratio": round(ab["naive_total"] / ab["shared_total"], 3),
+        }
+    kept = layers if keep_layers else None
+    del dec, flat_dec, flat_layers
+    if not keep_layers:
+        del layers
+        torch.cuda.empty_cache()
+    return result, plan, kept
+
+
+def sweep_leg(lens, steps: int, warmup: int, copies: int) -> dict:
+    """Shared path against the per-request path on the LLaMA-7B one-group
+    shape for each prefix length (speedup as a function of prefix length)."""
+    import torch
+    from paper_2405_19888_amd import Decoder
+    from workloads import get_config, make_device_layer, make_plan
+
+    out = {}
+    stream = torch.cuda.current_stream()
+    for P in lens:
+        cfg = get_config(f"sweep_p{P}")
+        plan = make_plan(cfg)
+        layers = [make_device_layer(plan, l, "cuda", seed=cfg.seed) for l in range(copies)]
+        dec = Decoder(problem_of(plan))
+        ab = algorithmic_bytes(plan)
+        times = {}
+        for shared in (True, False):
+            calls = [dec.bind(t, shared=shared, stream=stream) for t in layers]
+            for i in range(warmup):
+                calls[i % copies]()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(steps):
+                calls[i % copies]()
+            torch.cuda.synchronize()
+            times[shared] = (time.perf_counter() - t0) / steps
+        out[str(P)] = {"shared_us": round(times[True] * 1e6, 2),
+                       "per_request_us": round(times[False] * 1e6, 2),
+                       "speedup": round(times[False] / times[True], 3),
+                       "byte_ratio": round(ab["naive_total"] / ab["shared_total"], 3),
+                       "shared_hbm_frac": round(ab["shared_total"] / times[True] / 1e9 / HBM_PEAK_GBPS, 4)}
+        del layers, dec
+        torch.cuda.empty_cache()
+    sp = [out[str(P)]["speedup"] for P in lens]
+    return {"workload": "llama7b_g32_p<P>: 32 heads x 128, fp16, 1 group of 32, own U[64,512]",
+            "steps": steps, "layers_cycled": copies, "points": out,
+            "speedup_monotonic_in_prefix_len": all(b > a for a, b in zip(sp, sp[1:]))}
+
+
+# ------------------------------------------------------------------ prefill
 def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines: bool,
                 cpu_budget: float) -> dict:
     """Time parrot_shared_prefix_prefill on a prefill workload: `steps` calls,
@@ -203,10 +602,9 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
     import torch
     from paper_2405_19888_amd import (ParrotTrace, Prefiller, parrot_prefill_single_pass,
                                       parrot_validate_prefill_inputs)
-    from paper_2405_19888_amd import prefill_rows_from_host, problem_from_host
+    from paper_2405_19888_amd import prefill_rows_from_host
     from workloads import (get_config, make_device_layer, make_device_prefill_queries, make_plan,
                            one_group_per_request, prefill_rows)
-    from workloads.gen import TORCH_DTYPES
 
     cfg = get_config(cfg_name)
     if cfg.prefill_rows is None:
@@ -222,17 +620,9 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
     offsets = layers[0]["query_offsets"].cpu().numpy()
 
     def setup(p):
-        prob = problem_from_host(
-            num_heads=p.heads, head_dim=p.head_dim, block_size=p.block_size,
-            dtype=TORCH_DTYPES[p.dtype], sm_scale=p.sm_scale, group_ids=p.group_ids,
-            prefix_lens=p.prefix_lens, suffix_lens=p.suffix_lens,
-            prefix_table_stride=p.prefix_tables.shape[1],
-            suffix_table_stride=p.suffix_tables.shape[1],
-            num_prefix_blocks=p.num_blocks, num_suffix_blocks=p.num_blocks,
-            prefix_parents=p.prefix_parents if p.nested else None)
         rows = prefill_rows_from_host(offsets, p.group_ids, p.num_groups,
                                       p.prefix_parents if p.nested else None)
-        return prob, rows
+        return problem_of(p), rows
 
     prob, rows = setup(plan)
     scratch = torch.zeros(16, dtype=torch.int32, device=dev)
@@ -317,39 +707,17 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
             "note": "the same entry point with one group per request (prefix rows not stacked "
                     "across requests)",
         }
-        out["cpu_baseline"] = cpu_prefill_baseline(plan, layers[0]["q_rows"], offsets, layers[0],
-                                                   cpu_budget)
+        if cpu_budget > 0:
+            out["cpu_baseline"] = cpu_prefill_baseline(plan, layers[0]["q_rows"], offsets,
+                                                       layers[0], cpu_budget)
+    del layers, pre
+    torch.cuda.empty_cache()
     return out
 
 
-def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
-    """Read + write GB/s of a plain device-to-device copy (a ceiling for
-    bandwidth-bound kernels on this device, measured in the same process)."""
-    src = torch.ones(mib << 19, dtype=torch.float16, device="cuda")
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        dst.copy_(src)
-    e1.record()
-    e1.synchronize()
-    gbps = 2 * reps * src.numel() * 2 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del src, dst
-    torch.cuda.empty_cache()
-    return gbps
-
-
-def traffic_from_counters(plan_key: str, path: str = COUNTERS_FILE, sources=KERNEL_SOURCES):
-    """HBM bytes per launch of the dominant kernel from committed rocprofv3
-    counter runs, only if they were taken on the current kernel source."""
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        rec = json.load(f)
-    if rec.get("source_hash") != kernel_source_hash(sources) or rec.get("workload") != plan_key:
-        return None
-    return rec.get("bytes_per_launch")
+SUB_KEYS = ("value", "unit", "ms_per_step", "dtype", "hbm_gbps", "hbm_frac", "roofline",
+            "kernels_us", "prefix_mfma", "roles", "per_request_baseline", "flat_sharing_baseline",
+            "append_step", "warm", "algorithmic_bytes_per_step")
 
 
 def main():
@@ -357,10 +725,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--config", default="c2")
-    ap.add_argument("--layers", type=int, default=8, help="distinct-KV layers cycled by the steps")
+    ap.add_argument("--config", default="c5", help="headline decode workload (default: the "
+                                                   "32-layer mixed serving step)")
+    ap.add_argument("--layers", type=int, default=8,
+                    help="distinct-KV copies cycled by one-layer workloads")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle timing")
-    ap.add_argument("--no-baselines", action="store_true", help="skip the per-request and CPU legs")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the per-request, role, append and CPU legs")
     ap.add_argument("--no-trace", action="store_true", help="time without per-kernel events")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="first run three plain device copies of this many MiB (a known-size "
@@ -368,9 +739,15 @@ def main():
     ap.add_argument("--trace-every", type=int, default=16,
                     help="attach per-kernel HIP events to every N-th timed step (each traced "
                          "launch costs a few microseconds of stream time)")
+    ap.add_argument("--workloads", default="c2,c3,c4,nested",
+                    help="other decode workloads measured after the headline ('none' to skip)")
+    ap.add_argument("--sub-steps", type=int, default=400, help="timed steps per other workload")
+    ap.add_argument("--sweep", default=SWEEP_DEFAULT,
+                    help="prefix lengths of the sweep ('none' to skip)")
     ap.add_argument("--prefill", default="prefill",
-                    help="prefill workload timed after the decode line ('none' to skip)")
+                    help="prefill workload timed after the decode legs ('none' to skip)")
     ap.add_argument("--prefill-steps", type=int, default=20)
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the read and copy ceilings")
     ap.add_argument("--mode", choices=("decode", "prefill"), default="decode",
                     help="prefill: time only the prefill workload (--prefill) and print its line")
     args = ap.parse_args()
@@ -380,8 +757,8 @@ def main():
                                    "(no multi-GPU path exists)"}))
         sys.exit(2)
 
+    import torch
     if args.copy_mib > 0:
-        import torch
         n = args.copy_mib << 19                      # fp16 elements in that many MiB
         src = torch.ones(n, dtype=torch.float16, device="cuda")
         dst = torch.empty_like(src)
@@ -399,268 +776,42 @@ def main():
         print(json.dumps(leg), flush=True)
         return
 
-    import numpy as np
-    import torch
-    from paper_2405_19888_amd import (Decoder, ParrotTrace, parrot_validate_inputs,
-                                      parrot_validate_nested_inputs, problem_from_host)
-    from workloads import get_config, make_device_layer, make_plan
-    from workloads.gen import TORCH_DTYPES
+    ceilings = {}
+    if not args.no_ceilings:
+        ceilings = read_ceiling(torch)
+        ceilings["copy_gbps"] = round(copy_ceiling(torch), 1)
+        ceilings["copy_note"] = "device-to-device copy of 1 GiB, read + write bytes per second"
+    read_gbps = ceilings.get("read_gbps")
 
-    cfg = get_config(args.config)
-    plan = make_plan(cfg)
-    dev = "cuda"
-    # A multi-layer workload cycles through all of its layers (each with its
-    # own KV, all resident); a one-layer workload cycles --layers distinct-KV
-    # copies so that every call reads cold HBM.
-    n_layers = cfg.layers if cfg.layers > 1 else args.layers
-    layers = [make_device_layer(plan, l, dev, seed=cfg.seed) for l in range(n_layers)]
-    copy_gbps = copy_ceiling(torch)
-    prob = problem_from_host(
-        num_heads=plan.heads, head_dim=plan.head_dim, block_size=plan.block_size,
-        dtype=TORCH_DTYPES[plan.dtype], sm_scale=plan.sm_scale, group_ids=plan.group_ids,
-        prefix_lens=plan.prefix_lens, suffix_lens=plan.suffix_lens,
-        prefix_table_stride=plan.prefix_tables.shape[1],
-        suffix_table_stride=plan.suffix_tables.shape[1],
-        num_prefix_blocks=plan.num_blocks, num_suffix_blocks=plan.num_blocks,
-        prefix_parents=plan.prefix_parents if plan.nested else None)
-    scratch = torch.zeros(16, dtype=torch.int32, device=dev)
-    t0 = layers[0]
-    if plan.nested:
-        parrot_validate_nested_inputs(prob, t0["prefix_tables"], t0["prefix_lens"],
-                                      t0["prefix_parents"], t0["suffix_tables"], t0["suffix_lens"],
-                                      t0["group_ids"], scratch)
-    else:
-        parrot_validate_inputs(prob, t0["prefix_tables"], t0["prefix_lens"], t0["suffix_tables"],
-                               t0["suffix_lens"], t0["group_ids"], scratch)
-    dec = Decoder(prob, device=dev)
-    stream = torch.cuda.current_stream()
-    ab = algorithmic_bytes(plan)
-    K, W, L = args.steps, args.warmup, n_layers
-
-    names = ("partials", "merge")
-
-    nested = plan.nested
-    flat_layers = flat_dec = None
-    new_kv = None
-    if nested:
-        # baselines for nested groups: the flat entry points on the same blocks,
-        # each group's chain of prefixes laid end to end as one flat prefix
-        from workloads.gen import flatten_nested
-        flat = flatten_nested(plan)
-        ints = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
-                for k, v in (("prefix_tables", flat.prefix_tables), ("prefix_lens", flat.prefix_lens),
-                             ("group_ids", flat.group_ids))}
-        flat_layers = [dict(t, **ints) for t in layers]
-        flat_dec = Decoder(problem_from_host(
-            num_heads=flat.heads, head_dim=flat.head_dim, block_size=flat.block_size,
-            dtype=TORCH_DTYPES[flat.dtype], sm_scale=flat.sm_scale, group_ids=flat.group_ids,
-            prefix_lens=flat.prefix_lens, suffix_lens=flat.suffix_lens,
-            prefix_table_stride=flat.prefix_tables.shape[1],
-            suffix_table_stride=flat.suffix_tables.shape[1],
-            num_prefix_blocks=flat.num_blocks, num_suffix_blocks=flat.num_blocks), device=dev)
-
-    def run(shared: bool, trace: bool, flat_baseline: bool = False, append: bool = False,
-            inputs=None, steps=None, every=None):
-        """W untimed steps, then K timed steps; every `trace_every`-th timed step
-        carries per-kernel (start, stop) event pairs when `trace` is set.  For
-        nested groups, `flat_baseline` runs the flat entry points on the
-        flattened groups; `append` times decode with append (this step's K/V
-        written into every request's last own slot).  `inputs` replaces the
-        per-layer input dicts (their count sets the layers cycled)."""
-        K = steps or args.steps
-        if inputs is not None:
-            calls = [dec.bind(t, shared=shared, stream=stream, nested=nested) for t in inputs]
-        elif nested and (flat_baseline or not shared):
-            calls = [flat_dec.bind(flat_layers[l], shared=shared, stream=stream) for l in range(L)]
-        elif append:
-            calls = [dec.bind(dict(layers[l], k_new=new_kv[l][0], v_new=new_kv[l][1]),
-                              stream=stream, append=True) for l in range(L)]
-        else:
-            calls = [dec.bind(layers[l], shared=shared, stream=stream, nested=nested)
-                     for l in range(L)]
-        every = max(1, every or args.trace_every)
-        traced = list(range(0, K, every)) if trace else []
-        events = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)] for i in traced}
-        for evs in events.values():       # materialise the events outside the timed region
-            for e in evs:
-                e.record(stream)
-        torch.cuda.synchronize()
-        traces = {i: ParrotTrace(*[e.cuda_event for e in evs]) for i, evs in events.items()}
-        n = len(calls)
-        for i in range(W):
-            calls[i % n]()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(K):
-            calls[i % n](traces.get(i))
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        per = None
-        if trace:
-            per = {}
-            for k, name in enumerate(names):
-                us = np.array([evs[2 * k].elapsed_time(evs[2 * k + 1]) * 1e3 for evs in events.values()])
-                per[name + "_us"] = float(us.mean())
-                per[name + "_pct"] = [round(float(x), 3) for x in np.percentile(us, [10, 50, 90])]
-            per["traced_steps"] = len(events)
-        return wall, per
-
-    wall, per = run(shared=True, trace=not args.no_trace)
-    ms_per_step = wall / K * 1e3
-    R = plan.num_requests
-    value = R / (wall / K)
+    head, plan, layers = decode_leg(args.config, args.steps, args.warmup, args.layers,
+                                    args.trace_every, not args.no_baselines, read_gbps,
+                                    trace=not args.no_trace, keep_layers=True)
     result = {
         "metric": "decode-attention requests/sec per layer",
-        "value": round(value, 1),
-        "unit": "req/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
-        "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": DTYPE_TAG[plan.dtype],
-        "data": "synthetic",
-        "config": {
-            "workload": cfg.name, "requests": R, "heads": plan.heads, "head_dim": plan.head_dim,
-            "prefix_groups": plan.num_groups, "group_sizes": plan.group_sizes(),
-            **({"prefix_parents": [int(x) for x in plan.prefix_parents]} if nested else {}),
-            "prefix_lens": [int(x) for x in plan.prefix_lens],
-            "suffix_len_mean": round(float(plan.suffix_lens.mean()), 1),
-            "kv_block": plan.block_size, "kv_dtype": DTYPE_TAG[plan.dtype],
-            "layers": cfg.layers, "layers_cycled": L,
-            "timing": "HBM-resident inputs, distinct KV per cycled layer",
-        },
-        "hbm_gbps": round(ab["shared_total"] / (wall / K) / 1e9, 1),
+        "value": head["value"], "unit": "req/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": head["dtype"], "data": "synthetic", "config": head["config"],
     }
-    result["hbm_frac"] = round(result["hbm_gbps"] / HBM_PEAK_GBPS, 4)
-    if per is not None:
-        # dominant kernel: the partial-result kernel (prefix-group and split-KV roles)
-        part_bytes = ab["prefix_kv"] + ab["suffix_kv"] + ab["q"]
-        achieved = part_bytes / (per["partials_us"] * 1e-6) / 1e9
-        traffic = traffic_from_counters(cfg.name)
-        result["roofline"] = {
-            "kernel": "k_partials (prefix-group MFMA role + split-KV role)",
-            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
-            "algorithmic_bytes": part_bytes,
-            "avg_us": round(per["partials_us"], 3),
-        }
-        result["kernels_us"] = {k: round(v, 3) for k, v in per.items() if k.endswith("_us")}
-        result["kernels_us"].update({k.replace("_pct", "_p10_p50_p90_us"): v
-                                     for k, v in per.items() if k.endswith("_pct")})
-        result["kernels_us"]["traced_steps"] = per["traced_steps"]
-        result["ceilings"] = {
-            "copy_gbps": round(copy_gbps, 1),
-            "note": "device-to-device copy of 1 GiB in this process, read + write bytes per second",
-            "partials_frac_of_copy": round(achieved / copy_gbps, 4),
-        }
-        if ab["prefix_flops"] > 0:
-            intensity = ab["prefix_flops"] / ab["prefix_kv"]
-            result["prefix_mfma"] = {
-                "flops": ab["prefix_flops"],
-                "flop_per_byte": round(intensity, 2),
-                "tflops_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12, 2),
-                "util_over_partials_kernel": round(ab["prefix_flops"] / (per["partials_us"] * 1e-6) / 1e12
-                                                   / MFMA_F16_PEAK_TFLOPS, 5),
-                "util_ceiling_at_hbm_peak": round(min(1.0, intensity * HBM_PEAK_GBPS / 1e3
-                                                      / MFMA_F16_PEAK_TFLOPS), 5),
-            }
-    if not args.no_baselines and per is not None and int(plan.suffix_lens.min()) > 0:
-        # The roles one at a time, on the same blocks (the kernel runs both
-        # roles side by side, so its events cannot split them):
-        #  * suffix + merge: every request ungrouped, so the partial-result
-        #    kernel streams only the own tokens, then the merge;
-        #  * prefix: grouped requests with no own tokens (ungrouped ones keep
-        #    one), so the kernel is the prefix-group role.
-        R_ = plan.num_requests
-        ungrouped = torch.full((R_,), -1, dtype=torch.int32, device=dev)
-        slen_p = torch.from_numpy(np.where(plan.group_ids >= 0, 0, 1).astype(np.int32)).to(dev)
-        n_roles = min(args.steps, 400)
-        wall_s, per_s = run(shared=True, trace=True, steps=n_roles, every=4,
-                            inputs=[dict(t, group_ids=ungrouped) for t in layers])
-        wall_p, per_p = run(shared=True, trace=True, steps=n_roles, every=4,
-                            inputs=[dict(t, suffix_lens=slen_p) for t in layers])
-        suffix_bytes = ab["suffix_kv"] + ab["q"] + ab["out"] + ab["lse"]
-        sm_us = per_s["partials_us"] + per_s["merge_us"]
-        pre_us = per_p["partials_us"]
-        roles = {
-            "suffix_merge": {
-                "partials_us": round(per_s["partials_us"], 3), "merge_us": round(per_s["merge_us"], 3),
-                "algorithmic_bytes": suffix_bytes,
-                "gbps": round(suffix_bytes / (sm_us * 1e-6) / 1e9, 1),
-                "frac_of_hbm_peak": round(suffix_bytes / (sm_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-                "partials_frac_of_hbm_peak": round((ab["suffix_kv"] + ab["q"]) / (per_s["partials_us"] * 1e-6)
-                                                   / 1e9 / HBM_PEAK_GBPS, 4),
-                "note": "the same call with every request ungrouped (own tokens only): "
-                        "partial-result kernel + merge, kernel events",
-            },
-        }
-        if ab["prefix_flops"] > 0:
-            roles["prefix"] = {
-                "partials_us": round(pre_us, 3),
-                "algorithmic_bytes": ab["prefix_kv"] + ab["q"],
-                "gbps": round((ab["prefix_kv"] + ab["q"]) / (pre_us * 1e-6) / 1e9, 1),
-                "mfma_util": round(ab["prefix_flops"] / (pre_us * 1e-6) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
-                "mfma_util_ceiling_at_hbm_peak": round(min(1.0, ab["prefix_flops"] / ab["prefix_kv"]
-                                                           * HBM_PEAK_GBPS / 1e3 / MFMA_F16_PEAK_TFLOPS), 5),
-                "note": "the same call with grouped requests holding no own tokens: the "
-                        "prefix-group role alone, kernel events",
-            }
-        result["roles"] = roles
-        # warm: one layer's KV reused by every call (it stays partly in the
-        # 256 MB Infinity Cache); the headline cycles distinct-KV layers
-        wall_w, _ = run(shared=True, trace=False, steps=n_roles, inputs=[layers[0]])
-        result["warm"] = {"ms_per_step": round(wall_w / n_roles * 1e3, 5),
-                          "value": round(R_ / (wall_w / n_roles), 1),
-                          "note": "one layer's KV reused by every call"}
-
+    result.update({k: head[k] for k in SUB_KEYS if k in head and k not in result})
+    if ceilings:
+        result["ceilings"] = ceilings
     if not args.no_baselines:
-        if nested:
-            wall_f, _ = run(shared=True, trace=False, flat_baseline=True)
-            flat_bytes = (int(flat.prefix_lens.sum()) * 2 * plan.heads * plan.head_dim
-                          * ELT_BYTES[plan.dtype] + ab["shared_total"] - ab["prefix_kv"])
-            result["flat_sharing_baseline"] = {
-                "value": round(R / (wall_f / K), 1), "unit": "req/s",
-                "ms_per_step": round(wall_f / K * 1e3, 5),
-                "speedup_of_nested": round(wall_f / wall, 3),
-                "hbm_gbps": round(flat_bytes / (wall_f / K) / 1e9, 1),
-                "note": "parrot_shared_prefix_decode with each group's prefix chain as one flat prefix",
-            }
-        if not nested:
-            # decode with append: the same step, with this step's K/V written
-            # into the cache by the partial-result kernel (the values equal
-            # what the slots already hold, so later steps see the same data)
-            last = [(r, int(plan.suffix_tables[r][(int(plan.suffix_lens[r]) - 1) // plan.block_size]),
-                     (int(plan.suffix_lens[r]) - 1) % plan.block_size)
-                    for r in range(R) if plan.suffix_lens[r] > 0]
-            rows = torch.tensor([x[0] for x in last], device=dev, dtype=torch.long)
-            blks = torch.tensor([x[1] for x in last], device=dev, dtype=torch.long)
-            slots = torch.tensor([x[2] for x in last], device=dev, dtype=torch.long)
-            new_kv = []
-            for t in layers:
-                pair = []
-                for name in ("k_pool", "v_pool"):
-                    x = torch.zeros((R, plan.heads, plan.head_dim), dtype=t["q"].dtype, device=dev)
-                    x[rows] = t[name][blks, :, slots]
-                    pair.append(x)
-                new_kv.append(pair)
-            wall_a, _ = run(shared=True, trace=False, append=True)
-            result["append_step"] = {
-                "ms_per_step": round(wall_a / K * 1e3, 5),
-                "overhead_vs_plain": round(wall_a / wall - 1.0, 4),
-                "note": "parrot_shared_prefix_decode_append on the same workload",
-            }
-        wall_n, _ = run(shared=False, trace=False)
-        result["per_request_baseline"] = {
-            "value": round(R / (wall_n / K), 1), "unit": "req/s",
-            "ms_per_step": round(wall_n / K * 1e3, 5),
-            "speedup_of_shared": round(wall_n / wall, 3),
-            "hbm_gbps": round(ab["naive_total"] / (wall_n / K) / 1e9, 1),
-        }
         result["cpu_baseline"] = cpu_baseline(plan, layers[0], args.cpu_budget)
+    del layers
+    torch.cuda.empty_cache()
+
+    if args.workloads != "none":
+        result["workloads"] = {}
+        for name in [w for w in args.workloads.split(",") if w]:
+            leg, _, _ = decode_leg(name, args.sub_steps, min(args.warmup, 20), args.layers,
+                                   args.trace_every, not args.no_baselines, read_gbps,
+                                   trace=not args.no_trace)
+            sub = {k: leg[k] for k in SUB_KEYS if k in leg}
+            sub["config"] = leg["config"]
+            result["workloads"][leg["config"]["workload"]] = sub
+    if args.sweep != "none":
+        result["sweep"] = sweep_leg([int(x) for x in args.sweep.split(",")], 300, 20, args.layers)
     if args.prefill != "none":
         # the Fill step of the same kind of batch: every forked context's own
         # prompt rows against the shared prefix (its own line object)

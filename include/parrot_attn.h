@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 5
+#define PARROT_ABI_VERSION 6
 
 typedef enum {
   PARROT_OK = 0,
@@ -384,6 +384,30 @@ parrot_status parrot_validate_prefill_inputs(
     const int32_t* prefix_parents,
     const int32_t* suffix_block_tables, const int32_t* suffix_lens,
     const int32_t* group_ids, int32_t* scratch, void* stream);
+
+/*
+ * Measurement aid: the device's attainable HBM read bandwidth, the ceiling of
+ * the bandwidth-bound decode kernels (Section 8.3: token generation is bound
+ * by memory bandwidth).  Reads every byte of
+ *   src                  device buffer of `bytes` bytes (a multiple of 16),
+ *                        16-byte aligned; size it well above the 256 MB
+ *                        Infinity Cache so the reads come from HBM
+ * once, with 16-byte nontemporal loads (as the split-KV role streams KV
+ * blocks), `loads_per_thread` (4, 8 or 16) in flight per thread, over
+ * `workgroups` workgroups of 256 threads, and XOR-folds the data into
+ *   sink                 one uint32 of device memory (read-modify-written)
+ * so that no load can be dropped.  wave_spans = 0: grid-stride order
+ * (consecutive lanes of the whole grid read consecutive 16-byte pieces);
+ * 1: the buffer is cut into one contiguous span per wave, read front to back
+ * 1 KiB per instruction (the order of a KV stream).  Enqueued on `stream`;
+ * the caller times it (bytes / elapsed is the read bandwidth).  Errors: NULL
+ * or misaligned pointers, a size that is not a multiple of 16, workgroups < 1
+ * or wave_spans not 0 or 1 give PARROT_ERR_INVALID_ARGUMENT, another
+ * loads_per_thread PARROT_ERR_UNSUPPORTED; nothing is enqueued then.
+ */
+parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* sink,
+                                      int32_t workgroups, int32_t loads_per_thread,
+                                      int32_t wave_spans, void* stream);
 
 /* Message for the last failed call on this thread ("" if none).  Valid until
  * the next call of this library on the same thread. */

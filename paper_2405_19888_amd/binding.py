@@ -74,7 +74,7 @@ EXPORTED = (
     "parrot_validate_inputs", "parrot_validate_nested_inputs",
     "parrot_prefill_workspace_bytes", "parrot_prefill_single_pass", "parrot_shared_prefix_prefill",
     "parrot_validate_prefill_inputs", "parrot_last_error", "parrot_abi_version",
-    "parrot_shared_prefix_decode_noalloc",
+    "parrot_shared_prefix_decode_noalloc", "parrot_hbm_read_ceiling",
 )
 
 STATIC_SCRATCH_BYTES = 64 << 20   # PARROT_STATIC_SCRATCH_BYTES
@@ -124,6 +124,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.parrot_validate_prefill_inputs.restype = ctypes.c_int
     lib.parrot_prefill_single_pass.argtypes = [prob_p, rows_p, ctypes.c_int]
     lib.parrot_prefill_single_pass.restype = ctypes.c_int
+    lib.parrot_hbm_read_ceiling.argtypes = [vp, sz, vp, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32, vp]
+    lib.parrot_hbm_read_ceiling.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []
@@ -215,6 +218,16 @@ def parrot_shared_prefix_decode_noalloc(problem, q, prefix_k, prefix_v, suffix_k
         _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(suffix_block_tables),
         _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse), _stream_handle(stream),
         ctypes.byref(trace) if trace is not None else None))
+
+
+def parrot_hbm_read_ceiling(src, sink, workgroups: int, loads_per_thread: int = 8,
+                            wave_spans: bool = True, nbytes=None, stream=None):
+    """Enqueue the read-bandwidth probe over ``src`` (a device tensor; all of
+    it unless ``nbytes``) folding into ``sink`` (a device uint32/int32)."""
+    n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    _check(load_library().parrot_hbm_read_ceiling(_ptr(src), n, _ptr(sink), int(workgroups),
+                                                  int(loads_per_thread), 1 if wave_spans else 0,
+                                                  _stream_handle(stream)))
 
 
 def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,

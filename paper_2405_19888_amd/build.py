@@ -20,7 +20,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB_NAME = "libparrot_attn.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
-SOURCES = ["api.hip", "partials.hip", "prefill.hip", "merge.hip", "context_store.cpp"]
+SOURCES = ["api.hip", "partials.hip", "prefill.hip", "merge.hip", "ceiling.hip",
+           "context_store.cpp"]
 
 # Packed fp32 arithmetic is disabled: the kernels write only scalar float code.
 HIP_FLAGS = [

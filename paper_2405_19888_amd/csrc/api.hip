@@ -798,6 +798,26 @@ parrot_status parrot_validate_prefill_inputs(const parrot_problem* p, const parr
                   suffix_lens, group_ids, scratch, stream, rows, query_offsets);
 }
 
+parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* sink,
+                                      int32_t workgroups, int32_t loads_per_thread,
+                                      int32_t wave_spans, void* stream) {
+  if (!src || !sink) return fail(PARROT_ERR_INVALID_ARGUMENT, "src and sink must not be NULL");
+  if (!aligned(src, 16) || !aligned(sink, 4))
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "src must be 16-byte and sink 4-byte aligned");
+  if (bytes % 16 != 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "bytes %zu is not a multiple of 16", bytes);
+  if (workgroups < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "workgroups %d < 1", workgroups);
+  if (loads_per_thread != 4 && loads_per_thread != 8 && loads_per_thread != 16)
+    return fail(PARROT_ERR_UNSUPPORTED, "loads_per_thread %d (built for 4, 8 and 16)", loads_per_thread);
+  if (wave_spans != 0 && wave_spans != 1)
+    return fail(PARROT_ERR_INVALID_ARGUMENT, "wave_spans %d is not 0 or 1", wave_spans);
+  PARROT_TRY(launched(parrot::launch_read_ceiling(src, bytes, sink, workgroups, loads_per_thread,
+                                                  wave_spans != 0,
+                                                  reinterpret_cast<hipStream_t>(stream)),
+                      "read-ceiling kernel"));
+  g_err.clear();
+  return PARROT_OK;
+}
+
 const char* parrot_last_error(void) { return g_err.c_str(); }
 
 int parrot_abi_version(void) { return PARROT_ABI_VERSION; }
