@@ -796,7 +796,7 @@ def main():
     result.update({k: head[k] for k in SUB_KEYS if k in head and k not in result})
     if ceilings:
         result["ceilings"] = ceilings
-    if not args.no_baselines:
+    if not args.no_baselines and args.cpu_budget > 0:
         result["cpu_baseline"] = cpu_baseline(plan, layers[0], args.cpu_budget)
     del layers
     torch.cuda.empty_cache()

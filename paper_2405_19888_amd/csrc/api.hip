@@ -164,8 +164,6 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   if (p->num_requests > 0 && p->num_groups == 0 && p->max_suffix_len == 0)
     return fail(PARROT_ERR_INVALID_ARGUMENT, "no request can have a non-empty context (no groups, max_suffix_len 0)");
 
-  if (p->num_requests > parrot::kMaxRequests)
-    return fail(PARROT_ERR_UNSUPPORTED, "num_requests %d > %d per call", p->num_requests, parrot::kMaxRequests);
   if (p->max_prefix_depth < 0) return fail(PARROT_ERR_INVALID_ARGUMENT, "max_prefix_depth %d < 0", p->max_prefix_depth);
   if (p->max_prefix_depth > parrot::kMaxDepth)
     return fail(PARROT_ERR_UNSUPPORTED, "max_prefix_depth %d > %d", p->max_prefix_depth, parrot::kMaxDepth);
@@ -332,8 +330,37 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
       b.scale_log2 = scale_log2;
       pa.n_pre = p->num_groups * pl.seg_p * p->num_heads * pl.prefix_qtiles;
     }
-    PARROT_TRY(launched(parrot::launch_partials(pa, dt, D, s, ev(tr.partials_start), ev(tr.partials_stop)),
-                        "partials kernel"));
+    // The split-KV role holds its per-request scan in LDS for up to
+    // kMaxRequests requests, so a larger batch is streamed in slices of that
+    // many requests, one launch each (every per-request pointer moved to the
+    // slice); the prefix-group role covers every request in the first launch,
+    // and one merge follows.  The trace brackets all of them.
+    const int R = p->num_requests, H = p->num_heads;
+    const size_t elt = p->dtype == PARROT_DTYPE_F32 ? 4 : 2;
+    for (int r0 = 0; r0 < R; r0 += parrot::kMaxRequests) {
+      const int rn = std::min(parrot::kMaxRequests, R - r0);
+      parrot::PartialsArgs slice = pa;
+      parrot::SplitKVArgs& c = slice.skv;
+      const size_t rows = (size_t)r0 * H;
+      c.q = static_cast<const char*>(q) + rows * D * elt;
+      c.stab = stab + (size_t)r0 * p->suffix_table_stride;
+      c.slen = slen + r0;
+      c.gid = gid + r0;
+      if (k_new) {
+        c.k_new = static_cast<const char*>(k_new) + rows * D * elt;
+        c.v_new = static_cast<const char*>(v_new) + rows * D * elt;
+      }
+      c.o_part = o_part + rows * pl.seg * D;
+      c.lse_part = lse_part + rows * pl.seg;
+      c.merge_meta = merge_meta + (size_t)r0 * parrot::kMetaInts;
+      c.R = rn;
+      if (r0 > 0) slice.n_pre = 0;
+      const bool first = r0 == 0, last = r0 + rn == R;
+      PARROT_TRY(launched(parrot::launch_partials(slice, dt, D, s,
+                                                  first ? ev(tr.partials_start) : nullptr,
+                                                  last ? ev(tr.partials_stop) : nullptr),
+                          "partials kernel"));
+    }
   }
   {
     parrot::MergeArgs a{};

@@ -389,7 +389,7 @@ static hipError_t launch_prefill_t(const PrefillArgs& a, hipStream_t s, hipEvent
 
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0,
                           hipEvent_t e1) {
-  if (a.R > kMaxRequests || a.R < 1 || a.T < 1 || a.H < 1 || a.seg_s < 1 || a.qtiles_o < 1)
+  if (a.R < 1 || a.T < 1 || a.H < 1 || a.seg_s < 1 || a.qtiles_o < 1)
     return hipErrorInvalidValue;
   if (a.cp % 32 != 0 || a.co % 32 != 0 || a.cp > kPrefillMaxBlocks * kBlock ||
       a.co > kPrefillMaxBlocks * kBlock || a.cp < 32 || a.co < 32)

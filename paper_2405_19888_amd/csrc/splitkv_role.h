@@ -27,6 +27,13 @@
 
 namespace parrot {
 
+#ifndef PARROT_SPLITKV_STREAM_SCALAR_TABLE
+#define PARROT_SPLITKV_STREAM_SCALAR_TABLE 0
+#endif
+// Streaming path: block-table entries as scalar loads (the next block's loads
+// then issue while the current block is in flight) instead of vector loads.
+constexpr bool kStreamScalarTable = PARROT_SPLITKV_STREAM_SCALAR_TABLE != 0;
+
 // LDS bytes the split-KV role needs: six per-request arrays and a total.
 constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 
@@ -174,13 +181,14 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     const char* vp;
     int entry, nblk, ntok;
     if (b < nbp) {
-      entry = STREAM ? a.ptab[(long)s_g[r] * a.pstride + b]
-                     : ld_uniform(a.ptab + (long)s_g[r] * a.pstride + b);
+      entry = (STREAM && !kStreamScalarTable) ? a.ptab[(long)s_g[r] * a.pstride + b]
+                                              : ld_uniform(a.ptab + (long)s_g[r] * a.pstride + b);
       kp = (const char*)a.pk; vp = (const char*)a.pv; nblk = a.npblk;
       ntok = s_plen[r] - b * kBlock;
     } else {
       const int bs = b - nbp;
-      entry = STREAM ? a.stab[(long)r * a.sstride + bs] : ld_uniform(a.stab + (long)r * a.sstride + bs);
+      entry = (STREAM && !kStreamScalarTable) ? a.stab[(long)r * a.sstride + bs]
+                                              : ld_uniform(a.stab + (long)r * a.sstride + bs);
       kp = (const char*)a.sk; vp = (const char*)a.sv; nblk = a.nsblk;
       ntok = s_slen[r] - bs * kBlock;
     }

@@ -62,6 +62,16 @@ def test_abi_version(parrot_lib):
     assert B.parrot_abi_version() == 6
 
 
+def test_batches_above_1024_requests_are_sized(parrot_lib):
+    """No per-call request cap: decode and prefill size batches of any count
+    (the split-KV role streams them in slices of 1024 requests)."""
+    for R in (1024, 1025, 2500, 20000):
+        w = B.parrot_workspace_bytes(base_problem(num_requests=R))
+        assert w >= R * 32 * 129 * 4, R
+        rows = B.make_prefill_rows(R, 1, R)
+        assert B.parrot_prefill_workspace_bytes(base_problem(num_requests=R), rows) > 0
+
+
 def test_read_ceiling_rejects_bad_arguments_without_a_device(parrot_lib):
     f = parrot_lib.parrot_hbm_read_ceiling
     buf = ctypes.create_string_buffer(64)
