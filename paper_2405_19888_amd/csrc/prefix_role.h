@@ -100,13 +100,20 @@ template <> struct Mfma<kBF16> {
 }  // namespace prefix_detail
 
 constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
+#ifndef PARROT_PREFIX_RING
+#define PARROT_PREFIX_RING 3
+#endif
+// Stage buffers of the decode prefix role's ring (kDecodeRing - 1 stages in
+// flight per workgroup).
+constexpr int kDecodeRing = PARROT_PREFIX_RING;
+static_assert(kDecodeRing >= 3 && kDecodeRing <= 8, "decode prefix ring depth");
 // LDS bytes of a query tile of up to `rows` rows whose key range spans up to
 // `blocks` blocks: the stage ring, the tile's query rows, the key block ids, a
 // count, and the rows' last visible key (causal tiles).
 constexpr int tile_lds_bytes(int blocks, int rows = kPrefixWaves * 16, int ring = prefix_detail::kRing) {
   return ring * prefix_detail::kStageBytes + (2 * rows + blocks + 4) * 4;
 }
-constexpr int kPrefixLds = tile_lds_bytes(prefix_detail::kMaxChunkBlocks);
+constexpr int kPrefixLds = tile_lds_bytes(prefix_detail::kMaxChunkBlocks, kPrefixWaves * 16, kDecodeRing);
 
 // LDS views shared by the tile's set-up code and the tile cores.
 struct TileLds {
@@ -141,8 +148,9 @@ struct TileJob {
 // them) against key tokens [t0, t1) whose blocks are in tl.tbl; with CAUSAL,
 // row i sees only keys up to tl.lim[i].  Rows and blocks must be in LDS and
 // visible to every wave.  Writes one partial result (normalised output and
-// base-2 log-sum-exp; a row that sees no key gets 0 and -inf) per row.
-template <int DT, int D, bool CAUSAL>
+// base-2 log-sum-exp; a row that sees no key gets 0 and -inf) per row.  RING:
+// stage buffers of tl.smem (RING - 1 stages in flight).
+template <int DT, int D, bool CAUSAL, int RING = prefix_detail::kRing>
 __device__ __forceinline__ void tile_core(const TileJob& j, const TileLds& tl, int nq);
 
 // One workgroup of the prefix role; `wg` is the role-local workgroup index.
@@ -150,7 +158,7 @@ template <int DT, int D>
 __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int wg) {
   using namespace prefix_detail;
   constexpr int W = kPrefixWaves;
-  const TileLds tl(lds);
+  const TileLds tl(lds, kMaxChunkBlocks, W * 16, kDecodeRing);
   int* members = tl.rows;
   int* s_tbl = tl.tbl;
   int& s_count = tl.count[0];
@@ -214,10 +222,10 @@ __device__ __forceinline__ void prefix_role(const PrefixArgs& a, char* lds, int 
   job.q = a.q; job.pk = a.pk; job.pv = a.pv; job.npool = a.npblk; job.H = H; job.h = h;
   job.t0 = t0; job.t1 = t1; job.o_part = a.o_part; job.lse_part = a.lse_part;
   job.seg = a.seg; job.slot = lvl * a.seg_p + c; job.scale_log2 = a.scale_log2;
-  tile_core<DT, D, false>(job, tl, nq);
+  tile_core<DT, D, false, kDecodeRing>(job, tl, nq);
 }
 
-template <int DT, int D, bool CAUSAL>
+template <int DT, int D, bool CAUSAL, int RING>
 __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, int nq) {
   using namespace prefix_detail;
   constexpr int W = kPrefixWaves;
@@ -415,13 +423,14 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
     }
   };
 
-  // Ring of kRing stage buffers, kRing - 1 stages in flight while one is
+  // Ring of RING stage buffers, RING - 1 stages in flight while one is
   // computed.  At iteration st the wave's loads for st are the oldest outstanding ones,
-  // so vmcnt((kRing - 2) * PER_WAVE) means st has landed; the barrier then
+  // so vmcnt((RING - 2) * PER_WAVE) means st has landed; the barrier then
   // makes every wave's part visible and guarantees every wave is done with
-  // buffer (st - 1) % kRing, which stage st + kRing - 1 overwrites.
+  // buffer (st - 1) % RING, which stage st + RING - 1 overwrites.
+  static_assert((RING - 2) * PER_WAVE < 64, "vmcnt range");
 #pragma unroll
-  for (int i = 0; i < kRing - 1; ++i) issue(min(i, last), i);
+  for (int i = 0; i < RING - 1; ++i) issue(min(i, last), i);
   // The compiler tracks the query loads but not the direct-to-LDS loads; make
   // it wait for the queries here, once, instead of at their first use inside
   // the loop (where its wait would also drain the stage ring every iteration).
@@ -435,8 +444,8 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   }
   wait_vmcnt<0>();
   for (int st = 0; st < nstages; ++st) {
-    const int buf = st % kRing;
-    wait_vmcnt<(kRing - 2) * PER_WAVE>();
+    const int buf = st % RING;
+    wait_vmcnt<(RING - 2) * PER_WAVE>();
     lds_sync();
     if (st == last && (t1 & (kBlock - 1)) != 0) {
       // zero the V rows past the end of the chunk's last, partly filled block
@@ -450,7 +459,7 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
       }
       lds_sync();
     }
-    issue(min(st + kRing - 1, last), (st + kRing - 1) % kRing);
+    issue(min(st + RING - 1, last), (st + RING - 1) % RING);
     if (has_q) compute(st, buf);
   }
   wait_vmcnt<0>();   // the re-read stages issued by the last iterations

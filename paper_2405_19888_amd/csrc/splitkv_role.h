@@ -82,16 +82,39 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
   const int R = a.R, H = a.H;
 
   if (wave_in_wg == 0) {
+    // Every request's own length (and, on the per-request path, its group and
+    // prefix length) is loaded before the scan: one memory round trip (two on
+    // the per-request path) instead of one per 64 requests.  Addresses are
+    // clamped into [0, R) so every load is unconditional.
+    constexpr int kIt = kMaxRequests / kWave;
+    int s_in[kIt], g_in[kIt], p_in[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) s_in[i] = a.slen[min(i * kWave + lane, R - 1)];
+    if (a.with_prefix) {
+#pragma unroll
+      for (int i = 0; i < kIt; ++i) {
+        const int g = a.gid[min(i * kWave + lane, R - 1)];
+        g_in[i] = (g >= 0 && g < a.NG) ? g : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kIt; ++i) p_in[i] = 0;
+      if (a.NG > 0) {                        // no prefix lengths exist without groups
+#pragma unroll
+        for (int i = 0; i < kIt; ++i) p_in[i] = a.plen[g_in[i] >= 0 ? g_in[i] : 0];
+      }
+    }
     int carry = 0;
-    for (int base = 0; base < R; base += kWave) {
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int base = i * kWave;
+      if (base >= R) break;
       const int r = base + lane;
       const bool valid = r < R;
-      const int S = valid ? clampi(a.slen[r], 0, a.max_s) : 0;
+      const int S = valid ? clampi(s_in[i], 0, a.max_s) : 0;
       int g = -1, P = 0;
       if (a.with_prefix && valid) {
-        g = a.gid[r];
-        g = (g >= 0 && g < a.NG) ? g : -1;
-        P = g >= 0 ? clampi(a.plen[g], 0, a.max_p) : 0;
+        g = g_in[i];
+        P = g >= 0 ? clampi(p_in[i], 0, a.max_p) : 0;
       }
       const int nbp = (P + kBlock - 1) / kBlock;
       const int cnt = nbp + (S + kBlock - 1) / kBlock;
