@@ -82,12 +82,15 @@ def append_plan(kind, dtype, D, seed=0):
     if kind == "single":
         return build_plan(heads=1, head_dim=D, block_size=16, dtype=dtype, group_of_request=[-1],
                           prefix_lens=[], suffix_lens=[1], sm_scale=scale, rng=rng)
+    if kind == "many_heads":
+        from test_parity_gpu import many_heads_plan
+        return many_heads_plan(dtype, D, rng)
     raise ValueError(kind)
 
 
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("kind", ["mixed", "single"])
+@pytest.mark.parametrize("kind", ["mixed", "single", "many_heads"])
 def test_append_parity(kind, dtype, D):
     say("append", kind, dtype, D)
     plan = append_plan(kind, dtype, D)

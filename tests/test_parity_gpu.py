@@ -86,11 +86,25 @@ def edge_plan(kind, dtype, D, seed=0):
                           prefix_lens=[4200, 1025, 1023, 3000, 17, 2049, 4096, 700],
                           suffix_lens=rng.integers(0, 100, size=len(gor)).tolist(), sm_scale=scale,
                           shuffle=True, rng=rng)
+    if kind == "many_heads":
+        return many_heads_plan(dtype, D, rng)
     raise ValueError(kind)
 
 
+def many_heads_plan(dtype, D, rng):
+    """128 heads (16 split-KV waves per head on a 256-CU device): long runs of
+    the flat column list that cross many requests; ragged lengths, two groups
+    and ungrouped requests."""
+    gor = [0] * 12 + [1] * 12 + [-1] * 12
+    sl = rng.integers(150, 400, size=len(gor)).tolist()
+    sl[5], sl[30] = 0, 1
+    return build_plan(heads=128, head_dim=D, block_size=16, dtype=dtype, group_of_request=gor,
+                      prefix_lens=[300, 1000], suffix_lens=sl, sm_scale=1.0 / math.sqrt(D),
+                      shuffle=True, rng=rng)
+
+
 EDGE_KINDS = ["boundaries", "big_group", "ungrouped", "single_key", "chunk_multiples",
-              "long_prefix_4g", "long_prefix_8g"]
+              "long_prefix_4g", "long_prefix_8g", "many_heads"]
 
 
 @pytest.mark.parametrize("D", [64, 128])
