@@ -80,23 +80,48 @@ PARROT_DEV void store4(void* p, const f32x4& v) {
   }
 }
 
-// acc plus the four probabilities packed in `pk`, read as the PV MFMA reads
-// them (each rounded to the cache type).  Dividing the products by this sum
-// makes the output a weighted mean of the values with exactly the weights the
-// products used, so the rounding of a dominant weight cancels (with the lazy
-// reference a dominant weight is rarely 1); the lse keeps the sum of the
-// unrounded probabilities.  A dot2 with (1, 1) adds two packed halves into
-// fp32 exactly.
+// Two probabilities rounded to the cache type, packed as the PV MFMA reads them.
 template <int DT>
-PARROT_DEV float add_packed(unsigned long long pk, float acc) {
-  const unsigned lo = (unsigned)pk, hi = (unsigned)(pk >> 32);
+PARROT_DEV unsigned pack2(float a, float b) {
+  if constexpr (DT == kF16) {
+    const f16x2 x = {(_Float16)a, (_Float16)b};
+    return __builtin_bit_cast(unsigned, x);
+  } else {
+    const bf16x2 x = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(unsigned, x);
+  }
+}
+
+// acc plus the two packed probabilities of `w` (a dot2 with (1, 1) adds two
+// packed halves into fp32 exactly).
+template <int DT>
+PARROT_DEV float add_pair(unsigned w, float acc) {
   if constexpr (DT == kF16) {
     const f16x2 one = {(_Float16)1.f, (_Float16)1.f};
-    return __builtin_amdgcn_fdot2(as_f16x2(hi), one, __builtin_amdgcn_fdot2(as_f16x2(lo), one, acc, false), false);
+    return __builtin_amdgcn_fdot2(as_f16x2(w), one, acc, false);
   } else {
     const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
-    return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(hi), one,
-                                           __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(lo), one, acc, false), false);
+    return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(w), one, acc, false);
+  }
+}
+
+// LDS reads at a byte address held in a register plus a compile-time offset
+// (one instruction with an immediate offset).
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+PARROT_DEV u32x4 lds_read16(unsigned addr, int off) {
+  return *reinterpret_cast<const lds_u32x4*>((prefix_detail::lds_char*)addr + off);
+}
+template <int DT>
+PARROT_DEV unsigned long long lds_read_tr(unsigned addr, int off) {
+  if constexpr (DT == kF16) {
+    typedef __fp16 fp16x4_ __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) fp16x4_ lds_fp16x4;
+    fp16x4_ v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_fp16x4*)((prefix_detail::lds_char*)addr + off));
+    return __builtin_bit_cast(unsigned long long, v);
+  } else {
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)((prefix_detail::lds_char*)addr + off));
+    return __builtin_bit_cast(unsigned long long, v);
   }
 }
 
@@ -127,6 +152,7 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
   // times |scale| is the scaled max; a zero scale is taken as 1e-30, which
   // leaves every finite logit at 0 (to within 1e-22) and a masked one at -inf
   const float scale = fmaxf(fabsf(a.scale_log2), 1e-30f);
+  const float inv_scale = 1.f / scale;   // any rounding of it only shifts the lazy threshold
   const unsigned qsign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
 
   constexpr int NS = kWideSets;
@@ -174,10 +200,13 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
   // first visible key its reference is -FLT_MAX, finite: every finite logit
   // moves it, and exp2(logit * scale - reference) needs no guard (a masked
   // logit, -inf, gives 0)
-  float mref[NS], lsum[NS], lsr[NS];
+  float mref[NS], thr[NS], lsum[NS], lsr[NS];
   f32x4 o[NS][DT16];
 #pragma unroll
-  for (int c = 0; c < NS; ++c) { mref[c] = -FLT_MAX; lsum[c] = 0.f; lsr[c] = 0.f; }
+  for (int c = 0; c < NS; ++c) {
+    mref[c] = -FLT_MAX; lsum[c] = 0.f; lsr[c] = 0.f;
+    thr[c] = -INFINITY;                 // a row's first finite logit moves its reference
+  }
 #pragma unroll
   for (int c = 0; c < NS; ++c)
 #pragma unroll
@@ -187,6 +216,25 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
   const int vt_row = 4 * (lane >> 4) + ((lane & 15) >> 2);    // V^T: token row
   const int vt_half = 8 * (lane & 1);
   const int vt_pair = (lane & 3) >> 1;
+  // LDS byte addresses of this lane's K fragment (k-step ks) and V^T fragment
+  // (d tile dt) in block 0 of ring buffer 0; buffers and blocks add
+  // compile-time offsets.  Kept opaque, so the compiler holds one register
+  // per fragment and every read is one instruction with an immediate offset.
+  unsigned ka[KS], va[DT16];
+  {
+    const unsigned base = lds_addr(&smem[0][0]);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      ka[ks] = base + kt_row * ROW_B + (((4 * ks + (lane >> 4)) ^ swz_wide<GRAN>(kt_row)) << 4);
+      asm volatile("" : "+v"(ka[ks]));
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT16; ++dt) {
+      va[dt] = base + kTensorStage + vt_row * ROW_B + vt_half +
+               (((2 * dt + vt_pair) ^ swz_wide<GRAN>(vt_row)) << 4);
+      asm volatile("" : "+v"(va[dt]));
+    }
+  }
 
   // One pass over key tokens [t0, t1) (t0 a multiple of 16) of the pools
   // pk / pv, whose block ids the LDS table holds from t0 / 16 on.  Causal
@@ -219,34 +267,30 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
     // one pair of blocks (32 tokens) of stage buffer `buf`, first block `bl`;
     // `tok0` is the pair's first key token; `masked` selects the masking path
     auto pair = [&](int buf, int bl, int tok0, bool masked) {
-      const char* kb = &smem[buf][bl * BLK_B];
-      const char* vb = &smem[buf][kTensorStage + bl * BLK_B];
+      const int kb = buf * kStageBytes + bl * BLK_B;       // K of the pair's first block
       // K fragments feed the QK^T MFMAs of both sets; the V^T fragments are
       // read next to their PV MFMAs.  Reading them all ahead (or all K ahead)
       // needs about 24 more registers, which costs the third wave per SIMD;
       // with three waves the other waves hide the LDS latency better (measured).
       u32x4 kf[2][KS];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const char* krow = kb + b * BLK_B + kt_row * ROW_B;
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          kf[b][ks] = *reinterpret_cast<const u32x4*>(krow + (((4 * ks + (lane >> 4)) ^ swz_wide<GRAN>(kt_row)) << 4));
-      }
+        for (int ks = 0; ks < KS; ++ks) kf[b][ks] = lds_read16(ka[ks], kb + b * BLK_B);
       f32x4 s[NS][2];
 #pragma unroll
       for (int c = 0; c < NS; ++c)
 #pragma unroll
         for (int b = 0; b < 2; ++b) s[c][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // four accumulator chains, each MFMA four issues after the one it adds to
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int c = 0; c < NS; ++c) s[c][b] = Mfma<DT>::qk(kf[b][ks], qf[c][ks], s[c][b]);
-        }
 
-      unsigned long long pk2[NS][2];
+      unsigned pw[NS][4];
 #pragma unroll
       for (int c = 0; c < NS; ++c) {
         float x[8];
@@ -259,11 +303,13 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
           for (int i = 0; i < 8; ++i) x[i] = (i >> 2) * kBlock + (i & 3) < rel ? x[i] : -INFINITY;
         }
         // The row's reference only has to move when some lane's own logits
-        // exceed it by more than kLazy: that test needs no cross-lane max, and
-        // the cross-lane max is taken only in the (rare) branch that moves it.
+        // exceed it by more than kLazy, i.e. exceed thr = (mref + kLazy) /
+        // scale in logit units: that test needs no cross-lane max, and the
+        // cross-lane max is taken only in the (rare) branch that moves it.
         // (scale > 0: the scaled max of a masked lane stays -inf, no NaN)
-        const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-        if (__builtin_amdgcn_ballot_w64(__builtin_fmaf(lm, scale, -mref[c]) > kLazy) != 0) {
+        const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]),
+                               fmaxf(fmaxf(fmaxf(x[3], x[4]), x[5]), fmaxf(x[6], x[7])));
+        if (__builtin_amdgcn_ballot_w64(lm > thr[c]) != 0) {
           const float mn = fmaxf(mref[c], max_xor32(max_xor16(lm)) * scale);
           const float alpha = fast_exp2(mref[c] - mn);      // 0 after -FLT_MAX, 1 if unmoved
           lsum[c] *= alpha;
@@ -271,23 +317,35 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
 #pragma unroll
           for (int dt = 0; dt < DT16; ++dt) o[c][dt] *= alpha;
           mref[c] = mn;
+          thr[c] = (mn + kLazy) * inv_scale;
         }
         float p[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(x[i], scale, -mref[c]));   // masked: 0
         lsum[c] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-        pk2[c][0] = Mfma<DT>::pack_p(p);
-        pk2[c][1] = Mfma<DT>::pack_p(p + 4);
-        lsr[c] = add_packed<DT>(pk2[c][1], add_packed<DT>(pk2[c][0], lsr[c]));
+        // lsr: the probabilities as the PV MFMA reads them (rounded to the
+        // cache type).  Dividing the products by this sum makes the output a
+        // weighted mean of the values with exactly the weights the products
+        // used, so the rounding of a dominant weight cancels (with the lazy
+        // reference a dominant weight is rarely 1); the lse keeps the sum of
+        // the unrounded probabilities.
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pw[c][i] = pack2<DT>(p[2 * i], p[2 * i + 1]);
+          lsr[c] = add_pair<DT>(pw[c][i], lsr[c]);
+        }
       }
-      const char* vrow = vb + vt_row * ROW_B + vt_half;
+      const int vb = buf * kStageBytes + bl * BLK_B;       // V^T of the pair's first block
 #pragma unroll
       for (int dt = 0; dt < DT16; ++dt) {
-        const int off = ((2 * dt + vt_pair) ^ swz_wide<GRAN>(vt_row)) << 4;
-        const unsigned long long va = Mfma<DT>::tr_read(vrow + off);
-        const unsigned long long vb2 = Mfma<DT>::tr_read(vrow + BLK_B + off);
+        const unsigned long long va0 = lds_read_tr<DT>(va[dt], vb);
+        const unsigned long long va1 = lds_read_tr<DT>(va[dt], vb + BLK_B);
 #pragma unroll
-        for (int c = 0; c < NS; ++c) o[c][dt] = Mfma<DT>::pv2(va, vb2, pk2[c][0], pk2[c][1], o[c][dt]);
+        for (int c = 0; c < NS; ++c) {
+          const unsigned long long b0 = pw[c][0] | ((unsigned long long)pw[c][1] << 32);
+          const unsigned long long b1 = pw[c][2] | ((unsigned long long)pw[c][3] << 32);
+          o[c][dt] = Mfma<DT>::pv2(va0, va1, b0, b1, o[c][dt]);
+        }
       }
     };
 
