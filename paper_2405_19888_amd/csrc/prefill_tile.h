@@ -269,9 +269,11 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
     auto pair = [&](int buf, int bl, int tok0, bool masked) {
       const int kb = buf * kStageBytes + bl * BLK_B;       // K of the pair's first block
       // K fragments feed the QK^T MFMAs of both sets; the V^T fragments are
-      // read next to their PV MFMAs.  Reading them all ahead (or all K ahead)
-      // needs about 24 more registers, which costs the third wave per SIMD;
-      // with three waves the other waves hide the LDS latency better (measured).
+      // read next to their PV MFMAs, two d tiles (four reads) per wait, so each
+      // LDS round trip is covered by four MFMAs instead of two.  Reading them
+      // all ahead (or all K ahead, or the first V^T reads above the softmax)
+      // needs more registers than three waves per SIMD leave: the compiler
+      // spills, or the third wave is lost; either was slower (measured).
       u32x4 kf[2][KS];
 #pragma unroll
       for (int b = 0; b < 2; ++b)
@@ -336,16 +338,23 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
         }
       }
       const int vb = buf * kStageBytes + bl * BLK_B;       // V^T of the pair's first block
+      static_assert(DT16 % 2 == 0, "d tiles are read in pairs");
 #pragma unroll
-      for (int dt = 0; dt < DT16; ++dt) {
-        const unsigned long long va0 = lds_read_tr<DT>(va[dt], vb);
-        const unsigned long long va1 = lds_read_tr<DT>(va[dt], vb + BLK_B);
+      for (int dt = 0; dt < DT16; dt += 2) {
+        unsigned long long vt[2][2];
 #pragma unroll
-        for (int c = 0; c < NS; ++c) {
-          const unsigned long long b0 = pw[c][0] | ((unsigned long long)pw[c][1] << 32);
-          const unsigned long long b1 = pw[c][2] | ((unsigned long long)pw[c][3] << 32);
-          o[c][dt] = Mfma<DT>::pv2(va0, va1, b0, b1, o[c][dt]);
+        for (int u = 0; u < 2; ++u) {
+          vt[u][0] = lds_read_tr<DT>(va[dt + u], vb);
+          vt[u][1] = lds_read_tr<DT>(va[dt + u], vb + BLK_B);
         }
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int c = 0; c < NS; ++c) {
+            const unsigned long long b0 = pw[c][0] | ((unsigned long long)pw[c][1] << 32);
+            const unsigned long long b1 = pw[c][2] | ((unsigned long long)pw[c][3] << 32);
+            o[c][dt + u] = Mfma<DT>::pv2(vt[u][0], vt[u][1], b0, b1, o[c][dt + u]);
+          }
       }
     };
 
