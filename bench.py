@@ -273,6 +273,49 @@ def read_ceiling(torch, gib: int = 4, reps: int = 3) -> dict:
                          f"HIP events on the launch stream"}
 
 
+def read_probe_same_bytes(torch, nbytes: int, steps: int = 48) -> dict:
+    """The read probe over exactly ``nbytes`` (a stream's own byte count),
+    cycling distinct cold buffers, each launch timed with events attached to
+    it as the decode kernels are; best shape.  A short stream pays its start
+    and drain once per launch whatever reads it, so this is the read ceiling
+    at that size."""
+    import numpy as np
+    from paper_2405_19888_amd import ParrotTrace, parrot_hbm_read_ceiling
+    n = nbytes // 4096 * 4096
+    copies = max(2, min(8, (1536 << 20) // max(n, 1)))
+    bufs = [torch.ones(n // 4, dtype=torch.int32, device="cuda") for _ in range(copies)]
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    stream = torch.cuda.current_stream()
+    best = None
+    for spans in (True, False):
+        for wpc in (1, 2):
+            for unroll in (8, 16):
+                evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+                for e in evs:
+                    for x in e:
+                        x.record(stream)
+                torch.cuda.synchronize()
+                trs = [ParrotTrace(*[x.cuda_event for x in e]) for e in evs]
+                for i in range(copies):
+                    parrot_hbm_read_ceiling(bufs[i], sink, cus * wpc, unroll, spans, stream=stream)
+                for i in range(steps):
+                    parrot_hbm_read_ceiling(bufs[i % copies], sink, cus * wpc, unroll, spans,
+                                            stream=stream, trace=trs[i])
+                torch.cuda.synchronize()
+                us = float(np.median([e[0].elapsed_time(e[1]) * 1e3 for e in evs]))
+                if best is None or us < best["us"]:
+                    best = {"us": round(us, 3), "order": "wave_spans" if spans else "grid_stride",
+                            "workgroups_per_cu": wpc, "loads_per_thread": unroll}
+    del bufs
+    torch.cuda.empty_cache()
+    best["bytes"] = n
+    best["gbps"] = round(n / (best["us"] * 1e-6) / 1e9, 1)
+    best["note"] = (f"parrot_hbm_read_ceiling over {n} bytes ({copies} cold buffers cycled), "
+                    "median launch time by attached events, best shape")
+    return best
+
+
 def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
     """Read + write GB/s of a plain device-to-device copy (measured in the
     same process; a copy both reads and writes, so it is not the read
@@ -480,6 +523,11 @@ def decode_leg(cfg_name: str, steps: int, warmup: int, one_layer_copies: int, tr
         }
         if read_gbps:
             roles["suffix_merge"]["frac_of_read_ceiling"] = round(sm_gbps / read_gbps, 4)
+        # the same own-token bytes read by the read probe: what a plain read
+        # of that size achieves, start and drain included
+        probe = read_probe_same_bytes(torch, ab["suffix_kv"])
+        probe["partials_speed_vs_probe"] = round(probe["us"] / per_s["partials_us"], 4)
+        roles["suffix_merge"]["read_probe_same_bytes"] = probe
         if ab["prefix_flops"] > 0:
             pre_us = per_p["partials_us"]
             roles["prefix"] = {

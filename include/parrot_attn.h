@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 6
+#define PARROT_ABI_VERSION 7
 
 typedef enum {
   PARROT_OK = 0,
@@ -400,14 +400,19 @@ parrot_status parrot_validate_prefill_inputs(
  * (consecutive lanes of the whole grid read consecutive 16-byte pieces);
  * 1: the buffer is cut into one contiguous span per wave, read front to back
  * 1 KiB per instruction (the order of a KV stream).  Enqueued on `stream`;
- * the caller times it (bytes / elapsed is the read bandwidth).  Errors: NULL
+ * the caller times it (bytes / elapsed is the read bandwidth), optionally with
+ *   trace                (host) NULL, or timing hooks whose partials pair is
+ *                        attached to the probe's launch (the merge pair is
+ *                        unused), so the probe is timed exactly as the decode
+ *                        kernels are.  Errors: NULL
  * or misaligned pointers, a size that is not a multiple of 16, workgroups < 1
  * or wave_spans not 0 or 1 give PARROT_ERR_INVALID_ARGUMENT, another
  * loads_per_thread PARROT_ERR_UNSUPPORTED; nothing is enqueued then.
  */
 parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* sink,
                                       int32_t workgroups, int32_t loads_per_thread,
-                                      int32_t wave_spans, void* stream);
+                                      int32_t wave_spans, void* stream,
+                                      const parrot_trace* trace);
 
 /* Message for the last failed call on this thread ("" if none).  Valid until
  * the next call of this library on the same thread. */

@@ -125,7 +125,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.parrot_prefill_single_pass.argtypes = [prob_p, rows_p, ctypes.c_int]
     lib.parrot_prefill_single_pass.restype = ctypes.c_int
     lib.parrot_hbm_read_ceiling.argtypes = [vp, sz, vp, ctypes.c_int32, ctypes.c_int32,
-                                            ctypes.c_int32, vp]
+                                            ctypes.c_int32, vp, ctypes.POINTER(ParrotTrace)]
     lib.parrot_hbm_read_ceiling.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
@@ -221,13 +221,15 @@ def parrot_shared_prefix_decode_noalloc(problem, q, prefix_k, prefix_v, suffix_k
 
 
 def parrot_hbm_read_ceiling(src, sink, workgroups: int, loads_per_thread: int = 8,
-                            wave_spans: bool = True, nbytes=None, stream=None):
+                            wave_spans: bool = True, nbytes=None, stream=None, trace=None):
     """Enqueue the read-bandwidth probe over ``src`` (a device tensor; all of
-    it unless ``nbytes``) folding into ``sink`` (a device uint32/int32)."""
+    it unless ``nbytes``) folding into ``sink`` (a device uint32/int32);
+    ``trace`` (a ParrotTrace) attaches its partials pair to the launch."""
     n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     _check(load_library().parrot_hbm_read_ceiling(_ptr(src), n, _ptr(sink), int(workgroups),
                                                   int(loads_per_thread), 1 if wave_spans else 0,
-                                                  _stream_handle(stream)))
+                                                  _stream_handle(stream),
+                                                  ctypes.byref(trace) if trace is not None else None))
 
 
 def parrot_per_request_decode(problem, q, prefix_k, prefix_v, suffix_k, suffix_v,

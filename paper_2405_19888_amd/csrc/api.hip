@@ -827,7 +827,8 @@ parrot_status parrot_validate_prefill_inputs(const parrot_problem* p, const parr
 
 parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* sink,
                                       int32_t workgroups, int32_t loads_per_thread,
-                                      int32_t wave_spans, void* stream) {
+                                      int32_t wave_spans, void* stream,
+                                      const parrot_trace* trace) {
   if (!src || !sink) return fail(PARROT_ERR_INVALID_ARGUMENT, "src and sink must not be NULL");
   if (!aligned(src, 16) || !aligned(sink, 4))
     return fail(PARROT_ERR_INVALID_ARGUMENT, "src must be 16-byte and sink 4-byte aligned");
@@ -839,7 +840,9 @@ parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* s
     return fail(PARROT_ERR_INVALID_ARGUMENT, "wave_spans %d is not 0 or 1", wave_spans);
   PARROT_TRY(launched(parrot::launch_read_ceiling(src, bytes, sink, workgroups, loads_per_thread,
                                                   wave_spans != 0,
-                                                  reinterpret_cast<hipStream_t>(stream)),
+                                                  reinterpret_cast<hipStream_t>(stream),
+                                                  trace ? ev(trace->partials_start) : nullptr,
+                                                  trace ? ev(trace->partials_stop) : nullptr),
                       "read-ceiling kernel"));
   g_err.clear();
   return PARROT_OK;

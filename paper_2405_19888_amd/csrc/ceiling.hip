@@ -65,24 +65,26 @@ __global__ __launch_bounds__(256) void k_read_spans(const u32x4* __restrict__ sr
   publish(acc, sink);
 }
 
+// The optional (e0, e1) events are attached to the launch itself, as the
+// decode kernels' are.
 template <int UNROLL>
 static void launch_read(const u32x4* p, size_t n16, unsigned* sink, int workgroups, bool spans,
-                        hipStream_t s) {
+                        hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const dim3 grid((unsigned)workgroups), block(256);
   if (spans)
-    hipLaunchKernelGGL(k_read_spans<UNROLL>, grid, block, 0, s, p, n16, sink);
+    hipExtLaunchKernelGGL(k_read_spans<UNROLL>, grid, block, 0, s, e0, e1, 0, p, n16, sink);
   else
-    hipLaunchKernelGGL(k_read_grid_stride<UNROLL>, grid, block, 0, s, p, n16, sink);
+    hipExtLaunchKernelGGL(k_read_grid_stride<UNROLL>, grid, block, 0, s, e0, e1, 0, p, n16, sink);
 }
 
 hipError_t launch_read_ceiling(const void* src, size_t bytes, unsigned* sink, int workgroups,
-                               int unroll, bool spans, hipStream_t s) {
+                               int unroll, bool spans, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   const size_t n16 = bytes / 16;
   const u32x4* p = reinterpret_cast<const u32x4*>(src);
   switch (unroll) {
-    case 4: launch_read<4>(p, n16, sink, workgroups, spans, s); break;
-    case 8: launch_read<8>(p, n16, sink, workgroups, spans, s); break;
-    case 16: launch_read<16>(p, n16, sink, workgroups, spans, s); break;
+    case 4: launch_read<4>(p, n16, sink, workgroups, spans, s, e0, e1); break;
+    case 8: launch_read<8>(p, n16, sink, workgroups, spans, s, e0, e1); break;
+    case 16: launch_read<16>(p, n16, sink, workgroups, spans, s, e0, e1); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

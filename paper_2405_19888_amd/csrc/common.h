@@ -121,7 +121,7 @@ hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
 // `unroll` loads in flight per thread, in grid-stride order or one
 // contiguous span per wave (`spans`), XOR-folded into *sink.
 hipError_t launch_read_ceiling(const void* src, size_t bytes, unsigned* sink, int workgroups,
-                               int unroll, bool spans, hipStream_t s);
+                               int unroll, bool spans, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 // ------------------------------------------------------------ device helpers
 #if defined(__HIP_DEVICE_COMPILE__)

@@ -59,7 +59,7 @@ def test_binding_matches_header_arity(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 6
+    assert B.parrot_abi_version() == 7
 
 
 def test_batches_above_1024_requests_are_sized(parrot_lib):
@@ -76,13 +76,13 @@ def test_read_ceiling_rejects_bad_arguments_without_a_device(parrot_lib):
     f = parrot_lib.parrot_hbm_read_ceiling
     buf = ctypes.create_string_buffer(64)
     base = ctypes.addressof(buf) + (-ctypes.addressof(buf)) % 16
-    assert f(None, 16, base, 1, 8, 1, None) == B.PARROT_ERR_INVALID_ARGUMENT
-    assert f(base, 16, None, 1, 8, 1, None) == B.PARROT_ERR_INVALID_ARGUMENT
-    assert f(base + 8, 16, base, 1, 8, 1, None) == B.PARROT_ERR_INVALID_ARGUMENT     # misaligned
-    assert f(base, 20, base, 1, 8, 1, None) == B.PARROT_ERR_INVALID_ARGUMENT         # not 16 x n
-    assert f(base, 16, base, 0, 8, 1, None) == B.PARROT_ERR_INVALID_ARGUMENT         # no workgroups
-    assert f(base, 16, base, 1, 8, 2, None) == B.PARROT_ERR_INVALID_ARGUMENT         # order flag
-    assert f(base, 16, base, 1, 5, 1, None) == B.PARROT_ERR_UNSUPPORTED
+    assert f(None, 16, base, 1, 8, 1, None, None) == B.PARROT_ERR_INVALID_ARGUMENT
+    assert f(base, 16, None, 1, 8, 1, None, None) == B.PARROT_ERR_INVALID_ARGUMENT
+    assert f(base + 8, 16, base, 1, 8, 1, None, None) == B.PARROT_ERR_INVALID_ARGUMENT     # misaligned
+    assert f(base, 20, base, 1, 8, 1, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # not 16 x n
+    assert f(base, 16, base, 0, 8, 1, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # no workgroups
+    assert f(base, 16, base, 1, 8, 2, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # order flag
+    assert f(base, 16, base, 1, 5, 1, None, None) == B.PARROT_ERR_UNSUPPORTED
     assert "loads_per_thread" in B.parrot_last_error()
 
 
