@@ -316,6 +316,36 @@ def read_probe_same_bytes(torch, nbytes: int, steps: int = 48) -> dict:
     return best
 
 
+def mfma_issue_ceiling(torch, vx4_list=(0, 11), waves_per_simd: int = 3, iters: int = 4000,
+                       reps: int = 5) -> dict:
+    """The matrix cores' issue rate from the library's register-only probe
+    (16x16x32 fp16 MFMAs, with vx4 / 4 vector instructions issued per MFMA),
+    on every SIMD at the prefill tile's occupancy; best of `reps` launches,
+    each timed by events attached to it."""
+    from paper_2405_19888_amd import ParrotTrace, parrot_mfma_issue_ceiling
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    wgs = cus * waves_per_simd                   # 4 waves per workgroup, one per SIMD
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {}
+    for vx4 in vx4_list:
+        parrot_mfma_issue_ceiling(sink, wgs, 64, vx4, stream=stream)
+        best = None
+        for _ in range(reps):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            for x in e:
+                x.record(stream)
+            torch.cuda.synchronize()
+            parrot_mfma_issue_ceiling(sink, wgs, iters, vx4, stream=stream,
+                                      trace=ParrotTrace(*[x.cuda_event for x in e]))
+            torch.cuda.synchronize()
+            ms = e[0].elapsed_time(e[1])
+            best = ms if best is None else min(best, ms)
+        flops = wgs * 4 * iters * 8 * 16384
+        out[f"vector_per_mfma_{vx4 / 4:g}"] = round(flops / (best * 1e-3) / 1e12, 1)
+    return out
+
+
 def copy_ceiling(torch, mib: int = 1024, reps: int = 5) -> float:
     """Read + write GB/s of a plain device-to-device copy (measured in the
     same process; a copy both reads and writes, so it is not the read
@@ -738,6 +768,15 @@ def prefill_leg(cfg_name: str, steps: int, warmup: int, n_layers: int, baselines
         "kernels_us": {k: round(v, 3) for k, v in per.items()},
         "tflops_step": round(flops / (wall / steps) / 1e12, 1),
     }
+    # what the matrix cores issue on this box alone and with the tile's share
+    # of vector work (about 2.75 vector instructions per MFMA: the softmax)
+    issue = mfma_issue_ceiling(torch)
+    mixed = issue["vector_per_mfma_2.75"]
+    out["roofline"]["issue_ceiling_tflops"] = issue
+    out["roofline"]["frac_of_issue_ceiling"] = round(achieved / mixed, 4)
+    out["roofline"]["issue_note"] = ("parrot_mfma_issue_ceiling: registers only, 3 waves per SIMD "
+                                     "(the tile's occupancy), 16x16x32 fp16 MFMAs alone and with "
+                                     "2.75 vector instructions per MFMA between them")
     if baselines:
         # no sharing: each request its own group (same kernels and blocks)
         solo = one_group_per_request(plan)

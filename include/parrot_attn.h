@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PARROT_ABI_VERSION 7
+#define PARROT_ABI_VERSION 8
 
 typedef enum {
   PARROT_OK = 0,
@@ -413,6 +413,26 @@ parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* s
                                       int32_t workgroups, int32_t loads_per_thread,
                                       int32_t wave_spans, void* stream,
                                       const parrot_trace* trace);
+
+/*
+ * Measurement aid: the matrix cores' issue rate on this device with a given
+ * share of vector instructions between the products, the attainable ceiling
+ * of an MFMA kernel whose softmax interleaves vector work with its matrix
+ * products (the prefill tile; Section 7, Fill with a parent context).  Each
+ * of `workgroups` workgroups of 256 threads runs `iters` iterations of eight
+ * independent v_mfma_f32_16x16x32_f16 per wave (8 x 16384 flop) with
+ * valu_x4 / 4 vector instructions per MFMA issued between them (four
+ * v_exp_f32 per iteration, the rest v_fmac_f32; valu_x4 in {0, 8, 10, 11, 12,
+ * 16}), registers only, and XOR-folds the results into
+ *   sink                 one uint32 of device memory (read-modify-written)
+ * so that nothing is dropped.  Enqueued on `stream`; flops / elapsed is the
+ * rate; `trace` (host, may be NULL) attaches its partials pair to the launch.
+ * Errors: a NULL or misaligned sink, workgroups < 1 or iters < 1 give
+ * PARROT_ERR_INVALID_ARGUMENT, another valu_x4 PARROT_ERR_UNSUPPORTED;
+ * nothing is enqueued then.
+ */
+parrot_status parrot_mfma_issue_ceiling(uint32_t* sink, int32_t workgroups, int32_t iters,
+                                        int32_t valu_x4, void* stream, const parrot_trace* trace);
 
 /* Message for the last failed call on this thread ("" if none).  Valid until
  * the next call of this library on the same thread. */

@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     make_problem,
     parrot_abi_version,
     parrot_hbm_read_ceiling,
+    parrot_mfma_issue_ceiling,
     parrot_last_error,
     parrot_nested_prefix_decode,
     parrot_per_request_decode,

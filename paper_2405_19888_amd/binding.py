@@ -74,7 +74,7 @@ EXPORTED = (
     "parrot_validate_inputs", "parrot_validate_nested_inputs",
     "parrot_prefill_workspace_bytes", "parrot_prefill_single_pass", "parrot_shared_prefix_prefill",
     "parrot_validate_prefill_inputs", "parrot_last_error", "parrot_abi_version",
-    "parrot_shared_prefix_decode_noalloc", "parrot_hbm_read_ceiling",
+    "parrot_shared_prefix_decode_noalloc", "parrot_hbm_read_ceiling", "parrot_mfma_issue_ceiling",
 )
 
 STATIC_SCRATCH_BYTES = 64 << 20   # PARROT_STATIC_SCRATCH_BYTES
@@ -127,6 +127,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.parrot_hbm_read_ceiling.argtypes = [vp, sz, vp, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.c_int32, vp, ctypes.POINTER(ParrotTrace)]
     lib.parrot_hbm_read_ceiling.restype = ctypes.c_int
+    lib.parrot_mfma_issue_ceiling.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp,
+                                              ctypes.POINTER(ParrotTrace)]
+    lib.parrot_mfma_issue_ceiling.restype = ctypes.c_int
     lib.parrot_last_error.argtypes = []
     lib.parrot_last_error.restype = ctypes.c_char_p
     lib.parrot_abi_version.argtypes = []
@@ -218,6 +221,15 @@ def parrot_shared_prefix_decode_noalloc(problem, q, prefix_k, prefix_v, suffix_k
         _ptr(suffix_v), _ptr(prefix_block_tables), _ptr(prefix_lens), _ptr(suffix_block_tables),
         _ptr(suffix_lens), _ptr(group_ids), _ptr(out), _ptr(lse), _stream_handle(stream),
         ctypes.byref(trace) if trace is not None else None))
+
+
+def parrot_mfma_issue_ceiling(sink, workgroups: int, iters: int, valu_x4: int = 0, stream=None,
+                              trace=None):
+    """Enqueue the matrix-core issue probe (8 x 16384 flop per wave and
+    iteration, valu_x4 / 4 vector instructions per MFMA) folding into ``sink``."""
+    _check(load_library().parrot_mfma_issue_ceiling(_ptr(sink), int(workgroups), int(iters),
+                                                    int(valu_x4), _stream_handle(stream),
+                                                    ctypes.byref(trace) if trace is not None else None))
 
 
 def parrot_hbm_read_ceiling(src, sink, workgroups: int, loads_per_thread: int = 8,

@@ -11,6 +11,7 @@
 #include <string>
 
 #include "parrot_attn.h"
+#include "ceiling.h"
 #include "common.h"
 #include "errors.h"
 #include "prefill_args.h"
@@ -844,6 +845,23 @@ parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* s
                                                   trace ? ev(trace->partials_start) : nullptr,
                                                   trace ? ev(trace->partials_stop) : nullptr),
                       "read-ceiling kernel"));
+  g_err.clear();
+  return PARROT_OK;
+}
+
+parrot_status parrot_mfma_issue_ceiling(uint32_t* sink, int32_t workgroups, int32_t iters,
+                                        int32_t valu_x4, void* stream, const parrot_trace* trace) {
+  if (!sink) return fail(PARROT_ERR_INVALID_ARGUMENT, "sink must not be NULL");
+  if (!aligned(sink, 4)) return fail(PARROT_ERR_INVALID_ARGUMENT, "sink must be 4-byte aligned");
+  if (workgroups < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "workgroups %d < 1", workgroups);
+  if (iters < 1) return fail(PARROT_ERR_INVALID_ARGUMENT, "iters %d < 1", iters);
+  if (valu_x4 != 0 && valu_x4 != 8 && valu_x4 != 10 && valu_x4 != 11 && valu_x4 != 12 && valu_x4 != 16)
+    return fail(PARROT_ERR_UNSUPPORTED, "valu_x4 %d (built for 0, 8, 10, 11, 12 and 16)", valu_x4);
+  PARROT_TRY(launched(parrot::launch_mfma_issue(sink, workgroups, iters, valu_x4,
+                                                reinterpret_cast<hipStream_t>(stream),
+                                                trace ? ev(trace->partials_start) : nullptr,
+                                                trace ? ev(trace->partials_stop) : nullptr),
+                      "matrix-core issue kernel"));
   g_err.clear();
   return PARROT_OK;
 }

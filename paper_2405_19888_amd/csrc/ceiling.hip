@@ -1,9 +1,13 @@
-// Read-bandwidth ceiling of the device (a measurement aid for the roofline of
+// Measurement aids.  The read-bandwidth ceiling of the device (the roofline of
 // the bandwidth-bound decode kernels; Section 8.3 of the paper notes that
-// token generation is bound by memory bandwidth).  Every 16-byte piece of a
+// token generation is bound by memory bandwidth), and the matrix-core issue
+// ceiling with a given share of vector instructions (the roofline of the
+// MFMA-bound prefill tile, whose softmax interleaves vector work with its
+// products).  Every 16-byte piece of a
 // buffer is read once with a nontemporal global_load_dwordx4, the way the
 // split-KV role streams KV blocks; the values are folded with XOR and each
 // wave adds its fold to one word, so no load can be dropped.
+#include "ceiling.h"
 #include "common.h"
 
 namespace parrot {
@@ -85,6 +89,86 @@ hipError_t launch_read_ceiling(const void* src, size_t bytes, unsigned* sink, in
     case 4: launch_read<4>(p, n16, sink, workgroups, spans, s, e0, e1); break;
     case 8: launch_read<8>(p, n16, sink, workgroups, spans, s, e0, e1); break;
     case 16: launch_read<16>(p, n16, sink, workgroups, spans, s, e0, e1); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Matrix-core issue probe: registers only.  Each iteration issues eight
+// independent v_mfma_f32_16x16x32_f16 (eight accumulator chains) and, spread
+// evenly between them, VX4 / 4 vector instructions per MFMA (four v_exp_f32
+// per iteration, the rest v_fmac_f32 on independent registers).  The instructions are inline
+// assembly in the written order, so the compiler neither drops nor regroups
+// them; every result is folded into the sink at the end.  A kernel whose
+// softmax issues about VX4 / 4 vector instructions per MFMA cannot beat this
+// rate.
+#define PARROT_PROBE_MFMA(c) \
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b))
+#define PARROT_PROBE_EXP(x) asm volatile("v_exp_f32 %0, %0" : "+v"(x))
+#define PARROT_PROBE_FMA(x) asm volatile("v_fmac_f32 %0, %0, %1" : "+v"(x) : "v"(k))
+
+template <int VX4>
+__global__ __launch_bounds__(256) void k_mfma_issue(int iters, unsigned* sink) {
+  constexpr int NV = VX4 * 2;                         // vector instructions per iteration
+  static_assert(NV == 0 || (NV >= 8 && NV <= 32), "vector share");
+  const int lane = threadIdx.x & 63;
+  f16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) { a[i] = (_Float16)(0.001f * (lane + i)); b[i] = (_Float16)(0.001f * (lane - i)); }
+  f32x4 c[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) c[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float e[4], f[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) e[j] = -0.001f * (lane + j);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = 0.001f * (lane - j);
+  const float k = 0.5f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      PARROT_PROBE_MFMA(c[j]);
+      // after MFMA j: NV / 8 vector instructions (one more on the first NV % 8
+      // slots), the even slots' first one an exp
+      constexpr int base = NV / 8, extra = NV % 8;
+      const int n = base + (j < extra ? 1 : 0);
+#pragma unroll
+      for (int u = 0; u < 5; ++u) {
+        if (u < n) {
+          if (u == 0 && j % 2 == 0) PARROT_PROBE_EXP(e[j / 2]);
+          else PARROT_PROBE_FMA(f[(j + u) % 8]);
+        }
+      }
+    }
+  }
+  // the last MFMA results are read by plain vector code below: let them land
+  // (the accumulators are operands, so no read of them moves above the wait)
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+               : "+v"(c[0]), "+v"(c[1]), "+v"(c[2]), "+v"(c[3]), "+v"(c[4]), "+v"(c[5]), "+v"(c[6]), "+v"(c[7]));
+  unsigned acc = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    acc ^= __float_as_uint(c[j][0]) ^ __float_as_uint(c[j][1]) ^ __float_as_uint(c[j][2]) ^ __float_as_uint(c[j][3]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc ^= __float_as_uint(e[j]);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc ^= __float_as_uint(f[j]);
+  publish(acc, sink);
+}
+#undef PARROT_PROBE_MFMA
+#undef PARROT_PROBE_EXP
+#undef PARROT_PROBE_FMA
+
+hipError_t launch_mfma_issue(unsigned* sink, int workgroups, int iters, int vx4, hipStream_t s,
+                             hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid((unsigned)workgroups), block(256);
+  switch (vx4) {
+    case 0: hipExtLaunchKernelGGL(k_mfma_issue<0>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
+    case 8: hipExtLaunchKernelGGL(k_mfma_issue<8>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
+    case 10: hipExtLaunchKernelGGL(k_mfma_issue<10>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
+    case 11: hipExtLaunchKernelGGL(k_mfma_issue<11>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
+    case 12: hipExtLaunchKernelGGL(k_mfma_issue<12>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
+    case 16: hipExtLaunchKernelGGL(k_mfma_issue<16>, grid, block, 0, s, e0, e1, 0, iters, sink); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -117,11 +117,6 @@ struct PartialsArgs {
 hipError_t launch_partials(const PartialsArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_merge(const MergeArgs& a, int dtype, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_validate(const ValidateArgs& a, hipStream_t s);
-// Read-bandwidth probe: every 16-byte piece of src read once (nontemporal),
-// `unroll` loads in flight per thread, in grid-stride order or one
-// contiguous span per wave (`spans`), XOR-folded into *sink.
-hipError_t launch_read_ceiling(const void* src, size_t bytes, unsigned* sink, int workgroups,
-                               int unroll, bool spans, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 // ------------------------------------------------------------ device helpers
 #if defined(__HIP_DEVICE_COMPILE__)

@@ -59,7 +59,7 @@ def test_binding_matches_header_arity(parrot_lib):
 
 
 def test_abi_version(parrot_lib):
-    assert B.parrot_abi_version() == 7
+    assert B.parrot_abi_version() == 8
 
 
 def test_batches_above_1024_requests_are_sized(parrot_lib):
@@ -84,6 +84,18 @@ def test_read_ceiling_rejects_bad_arguments_without_a_device(parrot_lib):
     assert f(base, 16, base, 1, 8, 2, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # order flag
     assert f(base, 16, base, 1, 5, 1, None, None) == B.PARROT_ERR_UNSUPPORTED
     assert "loads_per_thread" in B.parrot_last_error()
+
+
+def test_mfma_issue_ceiling_rejects_bad_arguments_without_a_device(parrot_lib):
+    f = parrot_lib.parrot_mfma_issue_ceiling
+    buf = ctypes.create_string_buffer(16)
+    base = ctypes.addressof(buf) + (-ctypes.addressof(buf)) % 4
+    assert f(None, 1, 1, 0, None, None) == B.PARROT_ERR_INVALID_ARGUMENT
+    assert f(base + 2, 1, 1, 0, None, None) == B.PARROT_ERR_INVALID_ARGUMENT     # misaligned
+    assert f(base, 0, 1, 0, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # no workgroups
+    assert f(base, 1, 0, 0, None, None) == B.PARROT_ERR_INVALID_ARGUMENT         # no iterations
+    assert f(base, 1, 1, 9, None, None) == B.PARROT_ERR_UNSUPPORTED
+    assert "valu_x4" in B.parrot_last_error()
 
 
 def test_noalloc_refuses_batches_above_its_array_without_a_device(parrot_lib):
