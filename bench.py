@@ -316,12 +316,13 @@ def read_probe_same_bytes(torch, nbytes: int, steps: int = 48) -> dict:
     return best
 
 
-def mfma_issue_ceiling(torch, vx4_list=(0, 11), waves_per_simd: int = 3, iters: int = 4000,
+def mfma_issue_ceiling(torch, vx4_list=(0, 11), waves_per_simd: int = 3, iters: int = 12000,
                        reps: int = 5) -> dict:
     """The matrix cores' issue rate from the library's register-only probe
     (16x16x32 fp16 MFMAs, with vx4 / 4 vector instructions issued per MFMA),
-    on every SIMD at the prefill tile's occupancy; best of `reps` launches,
-    each timed by events attached to it."""
+    on every SIMD at the prefill tile's occupancy; median of `reps` launches
+    of about the prefill kernel's length (so the clock is the one a sustained
+    matrix-core load holds), each timed by events attached to it."""
     from paper_2405_19888_amd import ParrotTrace, parrot_mfma_issue_ceiling
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     wgs = cus * waves_per_simd                   # 4 waves per workgroup, one per SIMD
@@ -329,8 +330,8 @@ def mfma_issue_ceiling(torch, vx4_list=(0, 11), waves_per_simd: int = 3, iters: 
     stream = torch.cuda.current_stream()
     out = {}
     for vx4 in vx4_list:
-        parrot_mfma_issue_ceiling(sink, wgs, 64, vx4, stream=stream)
-        best = None
+        parrot_mfma_issue_ceiling(sink, wgs, iters, vx4, stream=stream)   # clocks up
+        times = []
         for _ in range(reps):
             e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             for x in e:
@@ -339,10 +340,10 @@ def mfma_issue_ceiling(torch, vx4_list=(0, 11), waves_per_simd: int = 3, iters: 
             parrot_mfma_issue_ceiling(sink, wgs, iters, vx4, stream=stream,
                                       trace=ParrotTrace(*[x.cuda_event for x in e]))
             torch.cuda.synchronize()
-            ms = e[0].elapsed_time(e[1])
-            best = ms if best is None else min(best, ms)
+            times.append(e[0].elapsed_time(e[1]))
+        ms = sorted(times)[len(times) // 2]
         flops = wgs * 4 * iters * 8 * 16384
-        out[f"vector_per_mfma_{vx4 / 4:g}"] = round(flops / (best * 1e-3) / 1e12, 1)
+        out[f"vector_per_mfma_{vx4 / 4:g}"] = round(flops / (ms * 1e-3) / 1e12, 1)
     return out
 
 
