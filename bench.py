@@ -102,11 +102,19 @@ def algorithmic_bytes(plan):
 
 # ------------------------------------------------------------------ CPU side
 def cpu_model() -> str | None:
+    """lscpu's model name with the vendor, family, model and stepping numbers
+    (a virtualised host may report only a generic name)."""
     try:
         out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        f = {}
         for line in out.splitlines():
-            if line.lower().startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if ":" in line:
+                k, v = line.split(":", 1)
+                f[k.strip().lower()] = v.strip()
+        if "model name" in f:
+            ids = ", ".join(f"{k} {f[k]}" for k in ("vendor id", "cpu family", "model", "stepping")
+                            if k in f)
+            return f"{f['model name']} ({ids})" if ids else f["model name"]
     except (OSError, subprocess.SubprocessError):
         pass
     try:
