@@ -309,8 +309,9 @@ __device__ __forceinline__ void wide_tile_impl(const TileJob& a, const TileLds& 
         // scale in logit units: that test needs no cross-lane max, and the
         // cross-lane max is taken only in the (rare) branch that moves it.
         // (scale > 0: the scaled max of a masked lane stays -inf, no NaN)
-        const float lm = fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]),
-                               fmaxf(fmaxf(fmaxf(x[3], x[4]), x[5]), fmaxf(x[6], x[7])));
+        // (grouped as v_max3 takes them: four instructions for eight values)
+        const float lm = fmaxf(fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]), fmaxf(fmaxf(x[3], x[4]), x[5])),
+                               fmaxf(x[6], x[7]));
         if (__builtin_amdgcn_ballot_w64(lm > thr[c]) != 0) {
           const float mn = fmaxf(mref[c], max_xor32(max_xor16(lm)) * scale);
           const float alpha = fast_exp2(mref[c] - mn);      // 0 after -FLT_MAX, 1 if unmoved
