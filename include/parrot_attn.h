@@ -404,10 +404,10 @@ parrot_status parrot_validate_prefill_inputs(
  *   trace                (host) NULL, or timing hooks whose partials pair is
  *                        attached to the probe's launch (the merge pair is
  *                        unused), so the probe is timed exactly as the decode
- *                        kernels are.  Errors: NULL
- * or misaligned pointers, a size that is not a multiple of 16, workgroups < 1
- * or wave_spans not 0 or 1 give PARROT_ERR_INVALID_ARGUMENT, another
- * loads_per_thread PARROT_ERR_UNSUPPORTED; nothing is enqueued then.
+ *                        kernels are.
+ * Errors: NULL or misaligned pointers, a size that is not a multiple of 16,
+ * workgroups < 1 or wave_spans not 0 or 1 give PARROT_ERR_INVALID_ARGUMENT,
+ * another loads_per_thread PARROT_ERR_UNSUPPORTED; nothing is enqueued then.
  */
 parrot_status parrot_hbm_read_ceiling(const void* src, size_t bytes, uint32_t* sink,
                                       int32_t workgroups, int32_t loads_per_thread,
