@@ -28,6 +28,8 @@
 // its fixed LDS slot.
 #pragma once
 
+#include <cfloat>
+
 #include "common.h"
 
 namespace parrot {
@@ -64,6 +66,13 @@ template <> struct Mfma<kF16> {
   PARROT_DEV static f32x4 pv(unsigned long long a, unsigned long long b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b), c, 0, 0, 0);
   }
+  // acc plus the four probabilities packed in w, as rounded (dot2 with (1, 1)
+  // adds two packed halves into fp32 exactly)
+  PARROT_DEV static float sum_p(unsigned long long w, float acc) {
+    const f16x2 one = {(_Float16)1.f, (_Float16)1.f};
+    acc = __builtin_amdgcn_fdot2(as_f16x2((unsigned)w), one, acc, false);
+    return __builtin_amdgcn_fdot2(as_f16x2((unsigned)(w >> 32)), one, acc, false);
+  }
   // k = 32 over two blocks: operand halves (lo, hi) hold block A and block B
   PARROT_DEV static f32x4 pv2(unsigned long long alo, unsigned long long ahi, unsigned long long blo,
                                unsigned long long bhi, f32x4 c) {
@@ -89,6 +98,11 @@ template <> struct Mfma<kBF16> {
   PARROT_DEV static f32x4 pv(unsigned long long a, unsigned long long b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a), __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
   }
+  PARROT_DEV static float sum_p(unsigned long long w, float acc) {
+    const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2((unsigned)w), one, acc, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2((unsigned)(w >> 32)), one, acc, false);
+  }
   PARROT_DEV static f32x4 pv2(unsigned long long alo, unsigned long long ahi, unsigned long long blo,
                                unsigned long long bhi, f32x4 c) {
     const u32x4 a = {(unsigned)alo, (unsigned)(alo >> 32), (unsigned)ahi, (unsigned)(ahi >> 32)};
@@ -100,6 +114,11 @@ template <> struct Mfma<kBF16> {
 }  // namespace prefix_detail
 
 constexpr int kPrefixWaves = 4;   // 16 queries per wave, 64 per workgroup
+#ifndef PARROT_PREFIX_VT_AHEAD
+#define PARROT_PREFIX_VT_AHEAD 4
+#endif
+// d tiles whose V^T fragments a decode prefix tile reads ahead of its scores
+constexpr int kVtAhead = PARROT_PREFIX_VT_AHEAD;
 #ifndef PARROT_PREFIX_RING
 #define PARROT_PREFIX_RING 3
 #endif
@@ -255,6 +274,18 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   const bool q_ok = qi < nq;
   const int rq = q_ok ? members[qi] : 0;
 
+  // 16-bit caches keep a lazy reference max, as the prefill tile does: the
+  // reference mref (scaled log2 units) moves only when some lane's raw logits
+  // exceed thr = (mref + kLazy) / scale, so the probabilities stay below
+  // 2^kLazy and most pairs need no cross-lane max and no rescale.  lsr sums
+  // the probabilities as rounded for the PV products and normalises the
+  // output; lsum (unrounded) gives the lse.  A negative scale flips the sign
+  // of q (exact), so the test runs on |scale|; a zero scale is taken as 1e-30.
+  constexpr float kLazy = 8.f;
+  const float scale = fmaxf(fabsf(a.scale_log2), 1e-30f);
+  const float inv_scale = 1.f / scale;
+  const unsigned qsign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
+
   // query operand (B of S^T = K Q^T): lane holds query lane%16, k-slice lane/16
   u32x4 qf16[(DT == kF32) ? 1 : KS];
   float qf32[(DT == kF32) ? KS : 1];
@@ -266,8 +297,10 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
         qf32[ks] = q_ok ? reinterpret_cast<const float*>(qrow)[4 * ks + (lane >> 4)] : 0.f;
     } else {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qf16[ks] = q_ok ? ld16(qrow + (32 * ks + 8 * (lane >> 4)) * 2) : u32x4{0u, 0u, 0u, 0u};
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 v = q_ok ? ld16(qrow + (32 * ks + 8 * (lane >> 4)) * 2) : u32x4{0u, 0u, 0u, 0u};
+        qf16[ks] = v ^ u32x4{qsign, qsign, qsign, qsign};
+      }
     }
   }
   // Direct-to-LDS stage loads.  Wave w issues chunks w, w + W, ... of each
@@ -275,9 +308,8 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   // i.e. block bl, token row t, granule slot pos, and fetches the global
   // granule pos ^ f(t) of that row.
   const size_t blk_stride = (size_t)H * BLK_B;
-  const char* pool_k = (const char*)a.pk + (size_t)h * BLK_B;
-  const char* pool_v = (const char*)a.pv + (size_t)h * BLK_B;
-  int c_bl[PER_WAVE], c_src[PER_WAVE];
+  int c_bl[PER_WAVE];
+  unsigned c_src[PER_WAVE];
   bool c_v[PER_WAVE];
 #pragma unroll
   for (int j = 0; j < PER_WAVE; ++j) {
@@ -287,20 +319,32 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
     c_bl[j] = off / BLK_B;
     const int t = (off % BLK_B) / ROW_B;
     const int pos = (off % ROW_B) / 16;
-    c_src[j] = t * ROW_B + ((pos ^ swz(t)) << 4);
+    c_src[j] = (unsigned)(h * BLK_B + t * ROW_B + ((pos ^ swz(t)) << 4));
   }
   const int nstages = (nb + STAGE_BLK - 1) / STAGE_BLK;
   const int last = nstages - 1;
-  auto issue = [&](int st, int buf) {
+  // Block ids of a stage (wave-uniform: a chunk lies inside one block) are read
+  // from the LDS table one stage before its loads are issued, so issuing waits
+  // on nothing; each load takes the block's base in scalar registers and the
+  // lane's offset in a vector register.
+  int tb[PER_WAVE];
+  auto table = [&](int st) {
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) tb[j] = s_tbl[min(st * STAGE_BLK + c_bl[j], nb - 1)];   // past the chunk: re-read, unused
+  };
+  auto issue = [&](int buf) {
 #pragma unroll
     for (int j = 0; j < PER_WAVE; ++j) {
-      const int b = min(st * STAGE_BLK + c_bl[j], nb - 1);   // past the chunk: re-read, unused
-      const char* src = (c_v[j] ? pool_v : pool_k) + (size_t)s_tbl[b] * blk_stride + c_src[j];
-      lds_dma16(src, lds_addr(&smem[buf][(wave + j * W) * 1024]));
+      // block ids are clamped when the table is filled; clamping again here
+      // keeps every load inside the pool whatever the LDS table holds
+      const unsigned blk = min((unsigned)__builtin_amdgcn_readfirstlane(tb[j]), (unsigned)(a.npool - 1));
+      const char* base = (const char*)(c_v[j] ? a.pv : a.pk) + (size_t)blk * blk_stride;
+      lds_dma16_sbase(base, c_src[j], lds_addr(&smem[buf][(wave + j * W) * 1024]));
     }
   };
 
-  float m = -INFINITY, lsum = 0.f;
+  float m = -INFINITY, lsum = 0.f;          // fp32 caches: running max, sum
+  float mref = -FLT_MAX, thr = -INFINITY, lsr = 0.f;   // 16-bit caches (lsum shared)
   f32x4 o[DT16];
 #pragma unroll
   for (int i = 0; i < DT16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -357,6 +401,40 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
     m = mn;
   };
 
+  // 16-bit caches: mask the logits of tokens past the range end (and, for a
+  // causal tile, past each row's limit); x[i] holds token tok0 + 16 (i / 4) +
+  // 4 (lane / 16) + i % 4
+  auto mask16 = [&](float* x, int n, int tok0) {
+    const int tb = tok0 + 4 * (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < n; ++i) {
+      const int tok = tb + (i >> 2) * kBlock + (i & 3);
+      const bool vis = tok < t1 && (!CAUSAL || tok <= lim);
+      x[i] = vis ? x[i] : -INFINITY;
+    }
+  };
+  // lazy reference test (rare branch: move the reference, rescale the state),
+  // then the probabilities and their unrounded sum
+  auto lazy16 = [&](const float* x, float* p, int n) {
+    float lm = x[0];
+#pragma unroll
+    for (int i = 1; i < n; ++i) lm = fmaxf(lm, x[i]);
+    if (__builtin_amdgcn_ballot_w64(lm > thr) != 0) {
+      const float mn = fmaxf(mref, max_xor32(max_xor16(lm)) * scale);
+      const float alpha = fast_exp2(mref - mn);      // 0 after -FLT_MAX, 1 if unmoved
+      lsum *= alpha;
+      lsr *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
+      mref = mn;
+      thr = (mn + kLazy) * inv_scale;
+    }
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < n; ++i) { p[i] = fast_exp2(__builtin_fmaf(x[i], scale, -mref)); ps += p[i]; }
+    lsum += ps;
+  };
+
   auto compute = [&](int st, int buf) {
     const int nbl = min(STAGE_BLK, nb - st * STAGE_BLK);
     int bl = 0;
@@ -365,32 +443,35 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
       for (; bl + 1 < nbl; bl += 2) {
         const char* kbA = &smem[buf][bl * BLK_B];
         const char* vbA = &smem[buf][kTensorStage + bl * BLK_B];
+        const int tok0 = (b0 + st * STAGE_BLK + bl) * kBlock;
+        const char* vrowA = vbA + vt_row * ROW_B + vt_half;
+        // V^T fragments of the first kVtAhead d tiles, read before the scores
+        // so that their LDS round trip overlaps the QK^T products and softmax
+        unsigned long long vt[kVtAhead > 0 ? kVtAhead : 1][2];
+#pragma unroll
+        for (int dt = 0; dt < kVtAhead; ++dt) {
+          const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+          vt[dt][0] = Mfma<DT>::tr_read(vrowA + off);
+          vt[dt][1] = Mfma<DT>::tr_read(vrowA + BLK_B + off);
+        }
         const f32x4 sA = scores(kbA);
         const f32x4 sB = scores(kbA + BLK_B);
-        float s[8], p[8];
-        logits(sA, st * STAGE_BLK + bl, s);
-        logits(sB, st * STAGE_BLK + bl + 1, s + 4);
-        {
-          float bm = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
-          bm = max_xor32(max_xor16(bm));
-          const float mn = fmaxf(m, bm);
-          const float mref = (CAUSAL && mn == -INFINITY) ? 0.f : mn;
-          const float alpha = fast_exp2(m - mref);
-          float ps = 0.f;
+        float x[8], p[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) { p[i] = fast_exp2(s[i] - mref); ps += p[i]; }
-          lsum = lsum * alpha + ps;
-#pragma unroll
-          for (int dt = 0; dt < DT16; ++dt) o[dt] *= alpha;
-          m = mn;
-        }
+        for (int i = 0; i < 4; ++i) { x[i] = sA[i]; x[4 + i] = sB[i]; }
+        if (CAUSAL || tok0 + 2 * kBlock > t1) mask16(x, 8, tok0);
+        lazy16(x, p, 8);
         const unsigned long long pA = Mfma<DT>::pack_p(p), pB = Mfma<DT>::pack_p(p + 4);
-        const char* vrowA = vbA + vt_row * ROW_B + vt_half;
+        lsr = Mfma<DT>::sum_p(pB, Mfma<DT>::sum_p(pA, lsr));
 #pragma unroll
         for (int dt = 0; dt < DT16; ++dt) {
-          const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
-          o[dt] = Mfma<DT>::pv2(Mfma<DT>::tr_read(vrowA + off), Mfma<DT>::tr_read(vrowA + BLK_B + off),
-                                pA, pB, o[dt]);
+          if (dt < kVtAhead) {
+            o[dt] = Mfma<DT>::pv2(vt[dt < kVtAhead ? dt : 0][0], vt[dt < kVtAhead ? dt : 0][1], pA, pB, o[dt]);
+          } else {
+            const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
+            o[dt] = Mfma<DT>::pv2(Mfma<DT>::tr_read(vrowA + off), Mfma<DT>::tr_read(vrowA + BLK_B + off),
+                                  pA, pB, o[dt]);
+          }
         }
       }
     }
@@ -398,8 +479,17 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
       const char* kb = &smem[buf][bl * BLK_B];
       const char* vb = &smem[buf][kTensorStage + bl * BLK_B];
       float s[4], p[4];
-      logits(scores(kb), st * STAGE_BLK + bl, s);
-      update(s, p, 4);
+      if constexpr (DT == kF32) {
+        logits(scores(kb), st * STAGE_BLK + bl, s);
+        update(s, p, 4);
+      } else {
+        const f32x4 s4 = scores(kb);
+        const int tok0 = (b0 + st * STAGE_BLK + bl) * kBlock;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[i] = s4[i];
+        if (CAUSAL || tok0 + kBlock > t1) mask16(s, 4, tok0);
+        lazy16(s, p, 4);
+      }
       if constexpr (DT == kF32) {
         // O^T[d][q] += V^T[d][t] P^T[t][q] with k index kk <-> token 4*kk + kt
 #pragma unroll
@@ -414,6 +504,7 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
         }
       } else {
         const unsigned long long pb = Mfma<DT>::pack_p(p);
+        lsr = Mfma<DT>::sum_p(pb, lsr);
         // lane k of 16-lane group G reads V[4G + k/4][dt*16 + 4*(k%4) .. +3]
         const char* vrow = vb + vt_row * ROW_B + vt_half;
 #pragma unroll
@@ -430,7 +521,11 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   // buffer (st - 1) % RING, which stage st + RING - 1 overwrites.
   static_assert((RING - 2) * PER_WAVE < 64, "vmcnt range");
 #pragma unroll
-  for (int i = 0; i < RING - 1; ++i) issue(min(i, last), i);
+  for (int i = 0; i < RING - 1; ++i) {
+    table(min(i, last));
+    issue(i);
+  }
+  table(min(RING - 1, last));
   // The compiler tracks the query loads but not the direct-to-LDS loads; make
   // it wait for the queries here, once, instead of at their first use inside
   // the loop (where its wait would also drain the stage ring every iteration).
@@ -459,7 +554,8 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
       }
       lds_sync();
     }
-    issue(min(st + RING - 1, last), (st + RING - 1) % RING);
+    issue((st + RING - 1) % RING);
+    table(min(st + RING, last));
     if (has_q) compute(st, buf);
   }
   wait_vmcnt<0>();   // the re-read stages issued by the last iterations
@@ -467,13 +563,17 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   if (!has_q) return;
   float lt = sum_xor16(lsum);
   lt = sum_xor32(lt);
+  // the output is normalised by the sum of the weights the products used
+  float lw = lt;
+  if constexpr (DT != kF32) lw = sum_xor32(sum_xor16(lsr));
+  const float mfin = DT == kF32 ? m : mref;
   if (q_ok) {
     const size_t slot = (size_t)(rq * H + h) * a.seg + a.slot;
-    const float inv = (CAUSAL && lt == 0.f) ? 0.f : 1.f / lt;
+    const float inv = (CAUSAL && lw == 0.f) ? 0.f : 1.f / lw;
     float* dst = a.o_part + slot * D + 4 * (lane >> 4);
 #pragma unroll
     for (int dt = 0; dt < DT16; ++dt) *reinterpret_cast<f32x4*>(dst + dt * 16) = o[dt] * inv;
-    if (lane < 16) a.lse_part[slot] = (CAUSAL && lt == 0.f) ? -INFINITY : m + fast_log2(lt);
+    if (lane < 16) a.lse_part[slot] = (CAUSAL && lt == 0.f) ? -INFINITY : mfin + fast_log2(lt);
   }
 }
 
