@@ -405,10 +405,10 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
   // causal tile, past each row's limit); x[i] holds token tok0 + 16 (i / 4) +
   // 4 (lane / 16) + i % 4
   auto mask16 = [&](float* x, int n, int tok0) {
-    const int tb = tok0 + 4 * (lane >> 4);
+    const int tlane = tok0 + 4 * (lane >> 4);
 #pragma unroll
     for (int i = 0; i < n; ++i) {
-      const int tok = tb + (i >> 2) * kBlock + (i & 3);
+      const int tok = tlane + (i >> 2) * kBlock + (i & 3);
       const bool vis = tok < t1 && (!CAUSAL || tok <= lim);
       x[i] = vis ? x[i] : -INFINITY;
     }
@@ -466,7 +466,8 @@ __device__ __forceinline__ void tile_core(const TileJob& a, const TileLds& tl, i
 #pragma unroll
         for (int dt = 0; dt < DT16; ++dt) {
           if (dt < kVtAhead) {
-            o[dt] = Mfma<DT>::pv2(vt[dt < kVtAhead ? dt : 0][0], vt[dt < kVtAhead ? dt : 0][1], pA, pB, o[dt]);
+            const int r = dt < kVtAhead ? dt : 0;      // in range in the untaken branch too
+            o[dt] = Mfma<DT>::pv2(vt[r][0], vt[r][1], pA, pB, o[dt]);
           } else {
             const int off = ((2 * dt + vt_pair) ^ swz(vt_row)) << 4;
             o[dt] = Mfma<DT>::pv2(Mfma<DT>::tr_read(vrowA + off), Mfma<DT>::tr_read(vrowA + BLK_B + off),
