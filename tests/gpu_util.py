@@ -74,20 +74,25 @@ def oracle_for(batch_like, plan, requests=None, pools=None):
         requests=requests, prefix_parents=plan.prefix_parents if plan.nested else None)
 
 
-def assert_close(out, lse, ref_out, ref_lse, dtype: str, what: str = ""):
+def assert_close(out, lse, ref_out, ref_lse, dtype: str, what: str = "", out_tol=None,
+                 rel_l2=None):
+    """Element-wise comparison with the oracle; ``out_tol`` / ``rel_l2``
+    replace the dtype's internal bars for inputs whose logits are far from unit
+    scale (the caller states the derivation)."""
     out = np.asarray(out, dtype=np.float64)
     lse = np.asarray(lse, dtype=np.float64)
     assert np.all(np.isfinite(out)), f"{what}: non-finite output"
     assert np.all(np.isfinite(lse)), f"{what}: non-finite lse"
     err = np.max(np.abs(out - ref_out)) if out.size else 0.0
     lerr = np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) if lse.size else 0.0
-    tol = OUT_TOL_INTERNAL.get(dtype, OUT_TOL[dtype])
+    tol = out_tol if out_tol is not None else OUT_TOL_INTERNAL.get(dtype, OUT_TOL[dtype])
     assert err <= tol, f"{what}: max |out err| {err:.3e} > {tol:.1e}"
     assert lerr <= LSE_RTOL, f"{what}: max lse rel err {lerr:.3e} > {LSE_RTOL:.0e}"
     ref_norm = float(np.linalg.norm(ref_out))
     if ref_norm > 0.0:
         rel = float(np.linalg.norm(out - ref_out)) / ref_norm
-        assert rel <= REL_L2[dtype], f"{what}: relative L2 of out {rel:.3e} > {REL_L2[dtype]:.0e}"
+        bar = rel_l2 if rel_l2 is not None else REL_L2[dtype]
+        assert rel <= bar, f"{what}: relative L2 of out {rel:.3e} > {bar:.0e}"
     return err, lerr
 
 

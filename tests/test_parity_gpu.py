@@ -221,6 +221,61 @@ def test_spike_probe(dtype):
                 assert np.max(np.abs(l[r] - s) / np.abs(s)) < 1e-5, f"spike lse r={r} j={j}"
 
 
+# ------------------------------------------------------ scale and logit range
+def scale_plan(dtype, sm_scale):
+    """Groups of 70 (two 64-query tiles), 5 and 1 members over prefixes long
+    enough for many stages, plus two ungrouped requests."""
+    rng = np.random.default_rng(11)
+    gor = [0] * 70 + [1] * 5 + [2] + [-1, -1]
+    return build_plan(heads=2, head_dim=128, block_size=16, dtype=dtype, group_of_request=gor,
+                      prefix_lens=[1500, 700, 33],
+                      suffix_lens=rng.integers(0, 120, size=len(gor)).tolist(), sm_scale=sm_scale,
+                      shuffle=True, rng=rng)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("kind", ["negative_scale", "zero_scale", "ramp"])
+def test_scale_and_logit_range(kind, dtype):
+    """sm_scale < 0 and sm_scale = 0, and logits that climb along a long prefix
+    (the softmax reference moves again and again within a chunk), against the
+    oracle on both paths."""
+    say("scale / logit range", kind, dtype)
+    D = 128
+    scale = {"negative_scale": -1 / math.sqrt(D), "zero_scale": 0.0, "ramp": 1 / math.sqrt(D)}[kind]
+    plan = scale_plan(dtype, scale)
+    batch = make_batch(plan, seed=5)
+    if kind == "ramp":
+        # group 0's members share a query direction u (plus noise); its prefix key
+        # j is ramp_j / (scale |u|^2) u plus noise, so every member's logit of key j
+        # is about ramp_j, climbing from 0 to 200 over the prefix: about 17 per
+        # 128-token chunk, several moves of a lazily kept reference per chunk
+        g = 0
+        P = int(plan.prefix_lens[g])
+        td = batch.q.dtype
+        q = batch.q.float()
+        k = batch.k_pool.float()
+        u = torch.randn((plan.heads, D), generator=torch.Generator().manual_seed(9))
+        for r in np.flatnonzero(plan.group_ids == g):
+            q[r] = u + 0.05 * q[r]
+        for j in range(P):
+            blk, slot = int(plan.prefix_tables[g][j // plan.block_size]), j % plan.block_size
+            for h in range(plan.heads):
+                c = 200.0 * j / P / (scale * float(u[h] @ u[h]))
+                k[blk, h, slot] = c * u[h] + 0.05 * k[blk, h, slot]
+        batch = type(batch)(plan=plan, q=q.to(td), k_pool=k.to(td), v_pool=batch.v_pool)
+    # fp32 caches: a logit near 200 carries a rounding error of about
+    # sqrt(D) 2^-24 200 = 1.4e-4 from its fp32 dot product, and so does each
+    # weight relatively; with |v| up to about 4 that bounds the output error by
+    # 6e-4 (relative L2 by 2e-4), above the 1e-5 kept for unit-scale logits
+    loose = kind == "ramp" and dtype == "float32"
+    ref = oracle_for(batch, plan)
+    dev = batch.to("cuda")
+    for shared in (True, False):
+        out, lse = run_gpu(plan, dev, shared=shared)
+        assert_close(*to_np(out, lse), *ref, dtype, f"{kind} {dtype} shared={shared}",
+                     out_tol=6e-4 if loose else None, rel_l2=2e-4 if loose else None)
+
+
 # ------------------------------------------------------------ other properties
 def test_bitwise_reproducible():
     say("reproducibility")
