@@ -8,6 +8,7 @@ workspace first; unused cache slots hold NaN.
 """
 import math
 import sys
+from dataclasses import replace
 
 import numpy as np
 import pytest
@@ -366,6 +367,54 @@ def test_prefill_zero_query_probe(path, dtype, monkeypatch):
         half_ulp = 2.0 ** -8 if dtype == "bfloat16" else 2.0 ** -11
         bound = half_ulp * np.maximum(np.abs(ref_o), 2.0 ** -6) + 1e-5
         assert np.all(np.abs(o - ref_o) <= bound), kind
+
+
+SCALE_CASES = ([(k, d, "split") for k in ("negative_scale", "zero_scale", "ramp")
+                for d in ("float16", "bfloat16", "float32")]
+               + [(k, d, "single") for k in ("negative_scale", "zero_scale", "ramp")
+                  for d in ("float16", "bfloat16")])
+
+
+@pytest.mark.parametrize("kind,dtype,path", SCALE_CASES)
+def test_prefill_scale_and_logit_range(kind, dtype, path, monkeypatch):
+    """sm_scale < 0 and sm_scale = 0, and prefix logits that climb from 0 to
+    200 over 1100 tokens (the softmax reference moves several times per
+    stage run), on both prefill plans, against the oracle."""
+    monkeypatch.setenv("PARROT_PREFILL_SINGLE_PASS", PLANS[path])
+    say("prefill scale / logit range", kind, dtype, path)
+    D = 128
+    scale = {"negative_scale": -1 / math.sqrt(D), "zero_scale": 0.0, "ramp": 1 / math.sqrt(D)}[kind]
+    plan, qr = prefill_case("wide_group", dtype, D)
+    plan = replace(plan, sm_scale=scale)
+    batch = make_batch(plan, seed=5)
+    q, off = make_prefill_queries(plan, qr, seed=5)
+    if kind == "ramp":
+        # every row shares a query direction u (plus noise); prefix key j is
+        # ramp_j / (scale |u|^2) u plus noise, so each row's logit of key j is
+        # about ramp_j = 200 j / P
+        g, P = 0, int(plan.prefix_lens[0])
+        td = q.dtype
+        qf = q.float()
+        k = batch.k_pool.float()
+        u = torch.randn((plan.heads, D), generator=torch.Generator().manual_seed(9))
+        qf = u[None] + 0.05 * qf
+        for j in range(P):
+            blk, slot = int(plan.prefix_tables[g][j // plan.block_size]), j % plan.block_size
+            for h in range(plan.heads):
+                c = 200.0 * j / P / (scale * float(u[h] @ u[h]))
+                k[blk, h, slot] = c * u[h] + 0.05 * k[blk, h, slot]
+        q = qf.to(td)
+        batch = type(batch)(plan=plan, q=batch.q, k_pool=k.to(td), v_pool=batch.v_pool)
+    keep = []
+    out, lse = run_prefill(plan, device_dict(batch, q, off), off, keep=keep)
+    assert workspace_untouched(keep[0]) == (path == "single"), "unexpected prefill path"
+    ref = oracle_prefill_for(batch, plan, q, off)
+    # fp32 caches: logits near 200 carry about sqrt(D) 2^-24 200 = 1.4e-4 of
+    # rounding from their fp32 dot products, and so does each weight relatively;
+    # with |v| up to about 4 the output error stays below 6e-4
+    loose = kind == "ramp" and dtype == "float32"
+    assert_close(*to_np(out, lse), *ref, dtype, f"prefill {kind} {dtype} {path}",
+                 out_tol=6e-4 if loose else None, rel_l2=2e-4 if loose else None)
 
 
 @pytest.mark.parametrize("path", ["single", "split"])
