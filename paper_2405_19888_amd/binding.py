@@ -384,12 +384,20 @@ def problem_from_host(*, num_heads, head_dim, block_size, dtype, sm_scale, group
     readers = np.zeros(max(ng, 1), dtype=np.int64)
     depth = 1 if ng else 0
     par = None if prefix_parents is None else np.asarray(prefix_parents)
+    # walks stop after ng steps: parents outside [-1, g) (which the validator
+    # rejects) cannot loop them
     for g in gid:
-        n, x = 0, int(g)
-        while x >= 0:
+        x, n = int(g), 0
+        while 0 <= x < ng and n < ng:
             readers[x] += 1
             n += 1
             x = int(par[x]) if par is not None else -1
+    # max_prefix_depth bounds every group's chain, read or not
+    for g in range(ng if par is not None else 0):
+        n, x = 0, g
+        while 0 <= x < ng and n < ng:
+            n += 1
+            x = int(par[x])
         depth = max(depth, n)
     return make_problem(
         num_requests=gid.shape[0], num_heads=num_heads, head_dim=head_dim,

@@ -410,3 +410,23 @@ def test_prefill_rows_from_host():
     assert (rows.num_query_rows, rows.max_query_rows, rows.max_group_rows) == (12, 7, 10)
     flat = B.prefill_rows_from_host(off, group_ids=[0, 1, 1, -1], num_groups=2)
     assert flat.max_group_rows == 7
+
+
+def test_problem_from_host_sizes_every_chain():
+    """max_prefix_depth covers every group's chain, also one that no request
+    reads; max_group_size counts each group's members and descendants'."""
+    common = dict(num_heads=2, head_dim=128, block_size=16, dtype=1, sm_scale=0.1,
+                  prefix_table_stride=8, suffix_table_stride=8, num_prefix_blocks=64,
+                  num_suffix_blocks=64)
+    # groups 0 <- 1 <- 2 <- 3; requests read only groups 0 and 1
+    p = B.problem_from_host(group_ids=[0, 1, 1, -1], prefix_lens=[16, 16, 16, 16],
+                            suffix_lens=[1, 2, 3, 4], prefix_parents=[-1, 0, 1, 2], **common)
+    assert p.max_prefix_depth == 4
+    assert p.max_group_size == 3          # group 0: its member and group 1's two
+    flat = B.problem_from_host(group_ids=[0, 1, 1, -1], prefix_lens=[16, 16, 16, 16],
+                               suffix_lens=[1, 2, 3, 4], **common)
+    assert (flat.max_prefix_depth, flat.max_group_size) == (0, 2)
+    # a parent outside [-1, g) (rejected later by the validator) must not hang
+    cyc = B.problem_from_host(group_ids=[0], prefix_lens=[16, 16], suffix_lens=[1],
+                              prefix_parents=[1, 0], **common)
+    assert cyc.max_prefix_depth <= 2
