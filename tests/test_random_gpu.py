@@ -1,5 +1,6 @@
 """Seeded random plans against the float64 oracle: decode (flat groups on both
-paths, nested chains on the nested entry point) and prefill (both plans).
+paths, nested chains on the nested entry point), decode with append, and
+prefill (both plans).
 
 Each seed draws the head count, head size, cache type, softmax scale (unit
 or half, either sign), group structure (empty groups, groups above one
@@ -119,3 +120,20 @@ def test_random_prefill(seed, plan_path, monkeypatch):
     out, lse = run_prefill(plan, dev, off)
     ref = oracle_prefill_for(batch, plan, q, off)
     assert_close(*to_np(out, lse), *ref, plan.dtype, f"prefill seed {seed} {plan_path}")
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_random_append(seed):
+    """Decode with append on random flat plans: the output against the oracle
+    on pools that hold each request's new token, and the cache afterwards."""
+    import torch
+    from test_append_gpu import run_append
+    plan, _ = random_plan(seed, nested=False)
+    say("random append", seed, plan.dtype, "D", plan.head_dim, "H", plan.heads, "R",
+        plan.num_requests)
+    batch = make_batch(plan, seed=seed)
+    out, lse, dev, k_new, v_new, kref, vref = run_append(plan, batch, seed=seed)
+    ref = oracle_for(batch, plan, pools=(kref, vref))
+    assert_close(*to_np(out, lse), *ref, plan.dtype, f"append seed {seed}")
+    assert torch.equal(dev["k_pool"].cpu().nan_to_num(7.0), kref.nan_to_num(7.0))
+    assert torch.equal(dev["v_pool"].cpu().nan_to_num(7.0), vref.nan_to_num(7.0))
