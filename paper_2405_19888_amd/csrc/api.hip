@@ -68,10 +68,18 @@ bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) %
 #ifndef PARROT_SPLITKV_MIN_BLOCKS
 #define PARROT_SPLITKV_MIN_BLOCKS 2
 #endif
+#ifndef PARROT_SPLITKV_HPW
+#define PARROT_SPLITKV_HPW 2            // heads per split-KV wave on the shared path (1 or 2)
+#endif
+#ifndef PARROT_SPLITKV_WGS_PER_CU_HPW2
+#define PARROT_SPLITKV_WGS_PER_CU_HPW2 1
+#endif
 constexpr int kPrefixChunk = PARROT_PREFIX_CHUNK;
 constexpr int kPrefixChunkMax = 1024;   // the prefix role's table stage holds 64 blocks
 constexpr int kSplitkvWgsPerCu = PARROT_SPLITKV_WGS_PER_CU;
 constexpr int kSplitkvMinBlocks = PARROT_SPLITKV_MIN_BLOCKS;
+constexpr int kSplitkvHpw = PARROT_SPLITKV_HPW;
+constexpr int kSplitkvWgsPerCuHpw2 = PARROT_SPLITKV_WGS_PER_CU_HPW2;
 
 // Compute units of the current device (cached per device; no device sync).
 int num_cus() {
@@ -86,12 +94,38 @@ int num_cus() {
   return v;
 }
 
+// Heads per split-KV wave on the shared path.  Two adjacent heads give each
+// wave one contiguous 8 KiB piece per tensor and block instead of 4 KiB: a read
+// probe over random 128 KiB blocks reaches 7.0 TB/s with 8 KiB pieces at four
+// waves per CU against 6.7 TB/s with 4 KiB pieces at eight (the same bytes in
+// flight), and the own-token stream ran 2-3.5 % faster on the 32-layer mixed,
+// system-prompt and map-reduce workloads.  Its kernel runs two waves per SIMD
+// (twice the registers per fetched block), which leaves fewer slots for the
+// prefix workgroups once the own-token stream drains, so it is taken when the
+// prefix tokens (bound: groups x max_prefix_len) are at most half the own
+// tokens (bound: requests x max_suffix_len): at a 16384-token prefix over 32
+// requests it was 2.3 % slower.  Even head counts and 16-bit caches only (an
+// fp32 block is twice the registers).  Decode with append takes the same
+// layout as the plain call, so the two give the same bits.
+int splitkv_hpw(const parrot_problem* p, bool shared) {
+  if (kSplitkvHpw != 2 || !shared || p->num_heads % 2 != 0 || p->dtype == PARROT_DTYPE_F32) return 1;
+  const double prefix_tokens = (double)p->num_groups * p->max_prefix_len;
+  const double own_tokens = (double)p->num_requests * p->max_suffix_len;
+  return 2.0 * prefix_tokens <= own_tokens ? 2 : 1;
+}
+
 // Split-KV workgroups of a decode launch: a fixed number per CU, and at least
-// one wave per head.
-long splitkv_workgroups(int heads) {
-  long n = (long)num_cus() * kSplitkvWgsPerCu;
-  if (n * parrot::kSkvWaves < heads) n = ceil_div(heads, parrot::kSkvWaves);
+// one wave per head group.
+long splitkv_workgroups(int heads, int hpw = 1) {
+  long n = (long)num_cus() * (hpw == 2 ? kSplitkvWgsPerCuHpw2 : kSplitkvWgsPerCu);
+  const long hg = heads / hpw;
+  if (n * parrot::kSkvWaves < hg) n = ceil_div(hg, parrot::kSkvWaves);
   return n;
+}
+
+// Column groups of the split-KV role (waves per head group).
+long splitkv_groups(int heads, int hpw) {
+  return splitkv_workgroups(heads, hpw) * parrot::kSkvWaves / (heads / hpw);
 }
 
 // Prefix chunk length.  One prefix-group workgroup streams one chunk of one
@@ -182,8 +216,11 @@ parrot_status check_problem(const parrot_problem* p, parrot::Plan* pl) {
   // group of its first column).
   const long nbp_max = p->num_groups > 0 ? ceil_div(p->max_prefix_len, B) : 0;
   const long nbs_max = ceil_div(p->max_suffix_len, B);
-  const long groups = splitkv_workgroups(p->num_heads) * parrot::kSkvWaves / p->num_heads;
-  const long pieces_shared = nbs_max > 0 ? std::min(ceil_div(nbs_max, pl->skv_min_q) + 1, groups) : 0;
+  // the shared path streams one or two heads per wave, the per-request path
+  // one; a bound on the pieces covers either
+  const long groups = splitkv_groups(p->num_heads, 1);
+  const long groups_shared = std::max(groups, splitkv_groups(p->num_heads, splitkv_hpw(p, true)));
+  const long pieces_shared = nbs_max > 0 ? std::min(ceil_div(nbs_max, pl->skv_min_q) + 1, groups_shared) : 0;
   const long pieces_naive = std::min(ceil_div(nbp_max + nbs_max, pl->skv_min_q) + 1, groups);
   pl->seg_p = p->num_groups > 0 ? (int)ceil_div(p->max_prefix_len, pl->cp) : 0;
   if (pl->seg_p > 0xFFFF)
@@ -314,8 +351,9 @@ parrot_status decode(bool shared, const parrot_problem* p, const void* q, const 
     a.npblk = p->num_groups > 0 ? p->num_prefix_blocks : 1; a.nsblk = p->num_suffix_blocks;
     a.seg = pl.seg; a.seg_pre = shared ? pl.seg_pre : 0; a.cp = pl.cp;
     a.with_prefix = shared ? 0 : 1;
-    // a fixed grid of split-KV workgroups per CU, at least one wave per head
-    pa.n_skv = (int)splitkv_workgroups(a.H);
+    // a fixed grid of split-KV workgroups per CU, at least one wave per head group
+    a.hpw = splitkv_hpw(p, shared);
+    pa.n_skv = (int)splitkv_workgroups(a.H, a.hpw);
     a.nwaves = pa.n_skv * parrot::kSkvWaves;
     a.min_q = pl.skv_min_q;
     a.scale_log2 = scale_log2;

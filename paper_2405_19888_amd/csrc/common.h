@@ -65,6 +65,7 @@ struct SplitKVArgs {
   int with_prefix;       // 1: each sequence is the group prefix, then the own tokens
   int nwaves;            // waves launched
   int min_q;             // blocks per wave >= min_q
+  int hpw;               // heads per split-KV wave: 1, or 2 (shared path, H even)
   float scale_log2;      // sm_scale * log2(e)
 };
 

@@ -56,8 +56,9 @@ constexpr int kSplitkvLds = (6 * kMaxRequests + 4) * 4;
 // (S_r-1)%16) while the block is reduced, so the cache holds it for later
 // steps.  The lane that writes a 16-byte piece is the lane that would have
 // read it, and no other wave reads that (block, head) in the call.
-template <int DT, int D, bool STREAM, bool APPEND = false>
+template <int DT, int D, bool STREAM, bool APPEND = false, int HPW = 1>
 __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, int wg) {
+  static_assert(HPW == 1 || HPW == 2, "one or two heads per wave");
   using E = Elem<DT>;
   constexpr int ROW_B = D * E::kBytes;        // bytes per token row
   constexpr int LPT = ROW_B / 16;             // lanes per token
@@ -134,7 +135,8 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
   }
   __syncthreads();
   const int C = s_total;                                      // flat block columns
-  const int G = a.nwaves / H;                                 // column groups
+  const int HG = H / HPW;                                     // head groups (H % HPW == 0)
+  const int G = a.nwaves / HG;                                // column groups
   const int Qg = (C + G - 1) / G;
   const int Q = Qg > a.min_q ? Qg : a.min_q;                  // columns per group
   if (wg == 0) {
@@ -165,8 +167,8 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     }
   }
   const int w = wg * kSkvWaves + wave_in_wg;
-  const int grp = w / H;
-  int h = w % H;
+  const int grp = w / HG;
+  const int h = (w % HG) * HPW;               // first head of the wave (HPW adjacent heads)
   const int c0 = grp * Q;
   if (grp >= G || c0 >= C) return;
   const int nblk_run = (C - c0 < Q) ? (C - c0) : Q;
@@ -188,15 +190,16 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
   const int tg = lane / LPT;                  // token group
   const size_t blk_stride = (size_t)H * BLK_B;
 
-  // One fetched block: K and V slices, the matching query slice, and the
-  // metadata needed to reduce it and to close its piece.
+  // One fetched block: K and V slices of the wave's heads (adjacent in the
+  // pool, so HPW * 4 KiB contiguous per tensor), the matching query slices,
+  // and the metadata needed to reduce it and to close its piece.
   struct Blk {
-    u32x4 k[IPB], v[IPB], q;
+    u32x4 k[HPW * IPB], v[HPW * IPB], q[HPW];
     int ntok;      // valid tokens in the block
-    int seq;       // r * H + h
+    int seq;       // r * H + h (first head)
     int piece_end; // last block of its sequence
-    int app;       // APPEND: load index holding this lane's piece of the new token, else -1
-    size_t app_off;  // APPEND: pool byte offset of this lane's load `app`
+    int app;       // APPEND: piece (of a head's IPB loads) holding this lane's share of the new token, else -1
+    size_t app_off;  // APPEND: pool byte offset of that piece for the first head
   };
   auto fetch = [&](Blk& B) {
     const int nbp = s_nbp[r];
@@ -224,25 +227,28 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
         const int last = (s_slen[r] - 1) % kBlock;
         if (tg == last % TPI) B.app = last / TPI;
       }
-      B.app_off = off + (size_t)(B.app < 0 ? 0 : B.app) * 1024;
-      const size_t noff = ((size_t)(r * H + h) * D) * E::kBytes + (size_t)sub * 16;
-      const char* kn = (const char*)a.k_new + noff;
-      const char* vn = (const char*)a.v_new + noff;
+      B.app_off = off + (size_t)(B.app < 0 ? 0 : B.app) * 1024;   // first head's piece
 #pragma unroll
-      for (int i = 0; i < IPB; ++i) {
-        const char* ks = (i == B.app) ? kn : kp + off + i * 1024;
-        const char* vs = (i == B.app) ? vn : vp + off + i * 1024;
+      for (int i = 0; i < HPW * IPB; ++i) {
+        // load i is piece i % IPB of head h + i / IPB; the new token's pieces
+        // come from k_new / v_new
+        const size_t noff = ((size_t)(r * H + h + i / IPB) * D) * E::kBytes + (size_t)sub * 16;
+        const bool nw = (i % IPB) == B.app;
+        const char* ks = nw ? (const char*)a.k_new + noff : kp + off + i * 1024;
+        const char* vs = nw ? (const char*)a.v_new + noff : vp + off + i * 1024;
         B.k[i] = STREAM ? ld16_stream(ks) : ld16(ks);
         B.v[i] = STREAM ? ld16_stream(vs) : ld16(vs);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < IPB; ++i) {
+      for (int i = 0; i < HPW * IPB; ++i) {
         B.k[i] = STREAM ? ld16_stream(kp + off + i * 1024) : ld16(kp + off + i * 1024);
         B.v[i] = STREAM ? ld16_stream(vp + off + i * 1024) : ld16(vp + off + i * 1024);
       }
     }
-    B.q = ld16((const char*)a.q + ((size_t)(r * H + h) * D + sub * EPL) * E::kBytes);
+#pragma unroll
+    for (int u = 0; u < HPW; ++u)
+      B.q[u] = ld16((const char*)a.q + ((size_t)(r * H + h + u) * D + sub * EPL) * E::kBytes);
     B.ntok = ntok < kBlock ? ntok : kBlock;
     B.seq = r * H + h;
     B.piece_end = (b == cnt - 1);
@@ -254,86 +260,105 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     }
   };
 
-  float m = -INFINITY, l = 0.f;
-  float acc[EPL];
+  float m[HPW], l[HPW];
+  float acc[HPW][EPL];
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+  for (int u = 0; u < HPW; ++u) {
+    m[u] = -INFINITY; l[u] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[u][e] = 0.f;
+  }
 
   // close the current piece of sequence `seq`: combine the token groups,
   // write the normalised output and log-sum-exp, reset the state
+  // close the current piece of sequences seq .. seq + HPW - 1 (the wave's
+  // heads): combine the token groups, write the normalised output and
+  // log-sum-exp, reset the state
   auto close_piece = [&](int seq) {
-#pragma unroll
-    for (int off = LPT; off < kWave; off <<= 1) {
-      const float mo = __shfl_xor(m, off);
-      const float lo = __shfl_xor(l, off);
-      const float mn = fmaxf(m, mo);
-      const float mref = (mn == -INFINITY) ? 0.f : mn;
-      const float sa = fast_exp2(m - mref), sb = fast_exp2(mo - mref);
-      l = l * sa + lo * sb;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * sa + __shfl_xor(acc[e], off) * sb;
-      m = mn;
-    }
     const int piece = grp - s_excl[seq / H] / Q;
-    if (tg == 0) {
-      const size_t slot = (size_t)seq * a.seg + a.seg_pre + piece;
-      const float inv = 1.f / l;
-      float* o = a.o_part + slot * D + sub * EPL;
 #pragma unroll
-      for (int e = 0; e < EPL; e += 4)
-        *reinterpret_cast<f32x4*>(o + e) = f32x4{acc[e] * inv, acc[e + 1] * inv, acc[e + 2] * inv, acc[e + 3] * inv};
-      if (lane == 0) a.lse_part[slot] = m + fast_log2(l);
+    for (int u = 0; u < HPW; ++u) {
+#pragma unroll
+      for (int off = LPT; off < kWave; off <<= 1) {
+        const float mo = __shfl_xor(m[u], off);
+        const float lo = __shfl_xor(l[u], off);
+        const float mn = fmaxf(m[u], mo);
+        const float mref = (mn == -INFINITY) ? 0.f : mn;
+        const float sa = fast_exp2(m[u] - mref), sb = fast_exp2(mo - mref);
+        l[u] = l[u] * sa + lo * sb;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[u][e] = acc[u][e] * sa + __shfl_xor(acc[u][e], off) * sb;
+        m[u] = mn;
+      }
+      if (tg == 0) {
+        const size_t slot = (size_t)(seq + u) * a.seg + a.seg_pre + piece;
+        const float inv = 1.f / l[u];
+        float* o = a.o_part + slot * D + sub * EPL;
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4)
+          *reinterpret_cast<f32x4*>(o + e) = f32x4{acc[u][e] * inv, acc[u][e + 1] * inv,
+                                                   acc[u][e + 2] * inv, acc[u][e + 3] * inv};
+        if (lane == 0) a.lse_part[slot] = m[u] + fast_log2(l[u]);
+      }
+      m[u] = -INFINITY; l[u] = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[u][e] = 0.f;
     }
-    m = -INFINITY; l = 0.f;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
   };
 
   auto reduce = [&](Blk& B, bool run_end) {
     if constexpr (APPEND) {
       if (B.app >= 0) {                        // write this step's token into the cache
 #pragma unroll
+        for (int u = 0; u < HPW; ++u)
+#pragma unroll
+          for (int i = 0; i < IPB; ++i) {
+            if (i == B.app) {
+              const size_t wo = B.app_off + (size_t)u * BLK_B;       // head h + u
+              *reinterpret_cast<u32x4*>((char*)a.app_k + wo) = B.k[u * IPB + i];
+              *reinterpret_cast<u32x4*>((char*)a.app_v + wo) = B.v[u * IPB + i];
+            }
+          }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < HPW; ++u) {
+      u32x4* bk = B.k + u * IPB;
+      u32x4* bv = B.v + u * IPB;
+      float s[IPB];
+#pragma unroll
+      for (int i = 0; i < IPB; ++i) s[i] = group_sum<LPT>(E::dot(bk[i], B.q[u])) * a.scale_log2;
+      if (B.ntok < kBlock) {                  // partly filled block: mask the tail
+#pragma unroll
         for (int i = 0; i < IPB; ++i) {
-          if (i == B.app) {
-            *reinterpret_cast<u32x4*>((char*)a.app_k + B.app_off) = B.k[i];
-            *reinterpret_cast<u32x4*>((char*)a.app_v + B.app_off) = B.v[i];
+          if (i * TPI + tg >= B.ntok) {
+            s[i] = -INFINITY;
+            bv[i] = u32x4{0u, 0u, 0u, 0u};    // 0 * NaN would poison the sum
           }
         }
       }
-    }
-    float s[IPB];
+      float bm = s[0];
 #pragma unroll
-    for (int i = 0; i < IPB; ++i) s[i] = group_sum<LPT>(E::dot(B.k[i], B.q)) * a.scale_log2;
-    if (B.ntok < kBlock) {                    // partly filled block: mask the tail
+      for (int i = 1; i < IPB; ++i) bm = fmaxf(bm, s[i]);
+      const float mn = fmaxf(m[u], bm);
+      const float mref = (mn == -INFINITY) ? 0.f : mn;
+      const float alpha = fast_exp2(m[u] - mref);
+      float psum = 0.f;
+      float p[IPB];
+#pragma unroll
+      for (int i = 0; i < IPB; ++i) { p[i] = fast_exp2(s[i] - mref); psum += p[i]; }
+      l[u] = l[u] * alpha + psum;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[u][e] *= alpha;
 #pragma unroll
       for (int i = 0; i < IPB; ++i) {
-        if (i * TPI + tg >= B.ntok) {
-          s[i] = -INFINITY;
-          B.v[i] = u32x4{0u, 0u, 0u, 0u};     // 0 * NaN would poison the sum
-        }
+        float v[EPL];
+        E::to_f32(bv[i], v);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[u][e] = __builtin_fmaf(p[i], v[e], acc[u][e]);
       }
+      m[u] = mn;
     }
-    float bm = s[0];
-#pragma unroll
-    for (int i = 1; i < IPB; ++i) bm = fmaxf(bm, s[i]);
-    const float mn = fmaxf(m, bm);
-    const float mref = (mn == -INFINITY) ? 0.f : mn;
-    const float alpha = fast_exp2(m - mref);
-    float psum = 0.f;
-    float p[IPB];
-#pragma unroll
-    for (int i = 0; i < IPB; ++i) { p[i] = fast_exp2(s[i] - mref); psum += p[i]; }
-    l = l * alpha + psum;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] *= alpha;
-#pragma unroll
-    for (int i = 0; i < IPB; ++i) {
-      float v[EPL];
-      E::to_f32(B.v[i], v);
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(p[i], v[e], acc[e]);
-    }
-    m = mn;
     if (B.piece_end || run_end) close_piece(B.seq);
   };
 
