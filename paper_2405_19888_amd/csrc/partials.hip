@@ -6,13 +6,14 @@
 //   workgroups [n_skv, n_skv + n_pre) prefix-group role: each group's shared
 //                                    prefix, read once for all of its members
 //
-// The split-KV grid is two workgroups per CU and the prefix-group work of the
-// benchmark workloads is about one more per CU, so every workgroup is resident
-// from the start (measured: each CU holds eight split-KV waves and four
-// prefix-group waves) and the prefix work overlaps the own-token stream.  Both
-// roles fit one launch shape: 256 threads, the LDS union of both roles (about
-// 48 KiB, three workgroups per CU) and a register budget of three waves per
-// SIMD.
+// The split-KV grid is two workgroups per CU (one when each wave streams two
+// heads) and the prefix-group work of the benchmark workloads is about one
+// more per CU, so every workgroup is resident from the start (measured: each
+// CU holds eight split-KV waves and four prefix-group waves) and the prefix
+// work overlaps the own-token stream.  Both roles fit one launch shape: 256
+// threads, the LDS union of both roles (about 48 KiB, three workgroups per CU)
+// and a register budget of three waves per SIMD (two for the two-heads
+// instance).
 #include "prefix_role.h"
 #include "splitkv_role.h"
 
