@@ -7,7 +7,9 @@
 // of Q columns ("column groups").  Wave (g, h) reduces head h over column
 // group g, so every wave streams the same number of bytes, and the H waves of
 // a group walk the same physical blocks at the same time, reading all heads
-// of a 16-token block (one contiguous H*4 KiB region per tensor) together.
+// of a 16-token block (one contiguous region of H token blocks per tensor)
+// together.  With HPW = 2 a wave reduces the adjacent heads h, h + 1 (H / 2
+// waves per group): one contiguous piece of two heads per block and tensor.
 // The role's grid is a fixed number of 4-wave workgroups per CU, so the
 // per-CU load is even too.  A run
 // may cross request boundaries: the wave then emits one partial result
@@ -269,8 +271,6 @@ __device__ __forceinline__ void splitkv_role(const SplitKVArgs& a, char* lds, in
     for (int e = 0; e < EPL; ++e) acc[u][e] = 0.f;
   }
 
-  // close the current piece of sequence `seq`: combine the token groups,
-  // write the normalised output and log-sum-exp, reset the state
   // close the current piece of sequences seq .. seq + HPW - 1 (the wave's
   // heads): combine the token groups, write the normalised output and
   // log-sum-exp, reset the state
